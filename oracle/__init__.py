@@ -1,0 +1,324 @@
+"""CPU oracle for the block join-agg hot path -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product library never loads it, and
+it imports nothing from the product package: the two share no code.  The only
+module both sides use is ``synth`` (seeded input generators, no arithmetic of
+the method).
+
+Each function computes the plain dense definition of a result in fp64 (C loops
+in ``ea_oracle.c``, OpenMP over output rows).  Blocks appear only where they are
+the result itself: the block layout, the join's tuple table and the
+repartition.  Citations refer to "Every Kernel Is a Join" (Einsummable): its
+sections, definitions and examples.
+
+Partitions are given as a list with one entry per dim, each entry the split
+points ``[0, s1, ..., extent]`` of that dim (non-uniform splits allowed).
+
+Pin status (what each function is checked against, in tests/test_oracle_pins.py):
+  rne_bf16 ......... torch's round-to-nearest-even cast (library routine)
+  layout/pack ...... 1-block identity, explicit small-case byte positions
+  repartition ...... round trips, dense-view equality, the overlay example
+  join ............. the paper's worked matmul example (Section 3.2/3.3),
+                     the product-of-intervals count rule, causal closed-form count
+  einsum ........... numpy.einsum (library), brute-force max, decomposition
+                     invariance with integer data (bit-exact)
+  matmul ........... numpy.matmul (library), identity/zero closed forms
+  rmsnorm .......... torch rms_norm (library), constant-row closed form
+  softmax .......... torch softmax (library), constant-row 1/(q+1) closed form
+  attention ........ torch scaled_dot_product_attention (library), equal-V and
+                     zero-K closed forms
+  llama_block ...... composition of the pinned parts only: the paper does not
+                     define the block, so its chain is "parity unpinned" beyond
+                     that composition
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ea_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+JOIN_MUL, JOIN_ADD = 0, 1
+AGG_NONE, AGG_SUM, AGG_MAX = 0, 1, 2
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (plain C, OpenMP, no BLAS)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O3", "-fopenmp", "-fPIC", "-shared", "-std=c11",
+                               "-Wall", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        L = ctypes.CDLL(_LIB)
+        i64p = ctypes.POINTER(ctypes.c_int64)
+        dp = ctypes.POINTER(ctypes.c_double)
+        L.or_num_threads.restype = ctypes.c_int
+        L.or_rne_bf16.argtypes = [ctypes.c_int64, dp, dp]
+        L.or_layout.argtypes = [ctypes.c_int, i64p, i64p, ctypes.c_int64, i64p, i64p]
+        L.or_pack.argtypes = [ctypes.c_int, i64p, i64p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+        L.or_unpack.argtypes = L.or_pack.argtypes
+        L.or_join.restype = ctypes.c_int64
+        L.or_join.argtypes = [ctypes.c_char_p, i64p, i64p, ctypes.c_char_p, ctypes.c_char, ctypes.c_char,
+                              ctypes.POINTER(ctypes.c_int32), ctypes.c_int64, i64p, ctypes.c_int64, i64p]
+        L.or_einsum.argtypes = [ctypes.c_char_p, ctypes.c_int, ctypes.c_int, i64p,
+                                ctypes.POINTER(dp), dp]
+        L.or_matmul.argtypes = [ctypes.c_int64] * 3 + [dp, dp, dp]
+        L.or_rmsnorm.argtypes = [ctypes.c_int64, ctypes.c_int64, dp, dp, ctypes.c_double, dp]
+        L.or_softmax.argtypes = [ctypes.c_int64] * 3 + [dp, ctypes.c_int, dp]
+        L.or_attention.argtypes = [ctypes.c_int64] * 4 + [dp, dp, dp, ctypes.c_int, ctypes.c_double, dp]
+        L.or_silu_mul.argtypes = [ctypes.c_int64, dp, dp, dp]
+        L.or_add.argtypes = [ctypes.c_int64, dp, dp, dp]
+        _lib = L
+    return _lib
+
+
+def num_threads() -> int:
+    return int(lib().or_num_threads())
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+
+
+def _dp(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _i64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int64))
+
+
+def _i64p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise ValueError(f"oracle {what} failed with code {rc}")
+
+
+# --------------------------------------------------------------------------
+# rounding
+# --------------------------------------------------------------------------
+def rne_bf16(x) -> np.ndarray:
+    """fp64 -> bf16 round-to-nearest-even, returned as fp64 values."""
+    x = _f64(x)
+    y = np.empty_like(x)
+    _check(lib().or_rne_bf16(x.size, _dp(x), _dp(y)), "rne_bf16")
+    return y
+
+
+# --------------------------------------------------------------------------
+# relation layout (Section 3.1 tensor types / tilings; Section 1 relations)
+# --------------------------------------------------------------------------
+def _flat_partition(partition):
+    nb = _i64([len(s) - 1 for s in partition])
+    sp = _i64([p for s in partition for p in s])
+    return nb, sp
+
+
+def layout(partition, elem_size: int):
+    """Byte offset of every block (row-major block order) and total bytes."""
+    nb, sp = _flat_partition(partition)
+    n = int(np.prod(nb))
+    offs = np.empty(n, dtype=np.int64)
+    nbytes = np.zeros(1, dtype=np.int64)
+    _check(lib().or_layout(len(partition), _i64p(nb), _i64p(sp), elem_size, _i64p(offs), _i64p(nbytes)),
+           "layout")
+    return offs, int(nbytes[0])
+
+
+def pack(dense: np.ndarray, partition) -> np.ndarray:
+    """Dense row-major tensor -> block-major relation bytes (uint8)."""
+    dense = np.ascontiguousarray(dense)
+    shape = tuple(s[-1] for s in partition)
+    if dense.shape != shape:
+        raise ValueError(f"dense shape {dense.shape} does not match partition extents {shape}")
+    es = dense.dtype.itemsize
+    _, nbytes = layout(partition, es)
+    out = np.zeros(nbytes, dtype=np.uint8)
+    nb, sp = _flat_partition(partition)
+    _check(lib().or_pack(len(partition), _i64p(nb), _i64p(sp), es, dense.ctypes.data, out.ctypes.data), "pack")
+    return out
+
+
+def unpack(blocked: np.ndarray, partition, dtype) -> np.ndarray:
+    """Block-major relation bytes -> dense row-major tensor of ``dtype``."""
+    dtype = np.dtype(dtype)
+    shape = tuple(s[-1] for s in partition)
+    _, nbytes = layout(partition, dtype.itemsize)
+    blocked = np.ascontiguousarray(blocked).view(np.uint8)
+    if blocked.size < nbytes:
+        raise ValueError("relation buffer smaller than its layout")
+    out = np.empty(shape, dtype=dtype)
+    nb, sp = _flat_partition(partition)
+    _check(lib().or_unpack(len(partition), _i64p(nb), _i64p(sp), dtype.itemsize, blocked.ctypes.data,
+                           out.ctypes.data), "unpack")
+    return out
+
+
+def repartition(blocked: np.ndarray, src_partition, dst_partition, dtype) -> np.ndarray:
+    """The same dense tensor under a new partition: dst block b, element r is
+    dense[lo_b + r] (Section 5.3: decompose into atoms, recompose)."""
+    return pack(unpack(blocked, src_partition, dtype), dst_partition)
+
+
+# --------------------------------------------------------------------------
+# join (Section 3.2 Definitions "Join-agg spec" and "Implementation" step 1)
+# --------------------------------------------------------------------------
+def join(spec: str, partitions, group: str | None = None, causal: tuple[str, str] | None = None):
+    """Brute-force join of block relations.
+
+    partitions: one partition per operand (inputs, then the output).
+    group: letters whose block coordinates form the group key (default: the
+    output letters).  causal: (q_letter, k_letter) keeps a tuple iff its k
+    block starts at or before its last q position.
+    Returns (tuples int32 [n, 1 + n_in] = (out_block, in_blocks...), group_off int64).
+    """
+    out_letters = spec.split("->")[1]
+    if group is None:
+        group = out_letters
+    nb = _i64([len(s) - 1 for part in partitions for s in part])
+    sp = _i64([p for part in partitions for s in part for p in s])
+    n_in = len(spec.split("->")[0].split(","))
+    ng = np.zeros(1, dtype=np.int64)
+    cq = causal[0].encode() if causal else b"\0"
+    ck = causal[1].encode() if causal else b"\0"
+    L = lib()
+    n = L.or_join(spec.encode(), _i64p(nb), _i64p(sp), group.encode(), cq, ck, None, 0, None, 0, _i64p(ng))
+    if n < 0:
+        raise ValueError(f"oracle join failed with code {n}")
+    tuples = np.zeros((max(n, 1), n_in + 1), dtype=np.int32)
+    goff = np.zeros(int(ng[0]) + 1, dtype=np.int64)
+    n2 = L.or_join(spec.encode(), _i64p(nb), _i64p(sp), group.encode(), cq, ck,
+                   tuples.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), tuples.shape[0],
+                   _i64p(goff), goff.size, _i64p(ng))
+    if n2 != n:
+        raise ValueError(f"oracle join failed with code {n2}")
+    return tuples[:n], goff
+
+
+# --------------------------------------------------------------------------
+# dense numerics (fp64)
+# --------------------------------------------------------------------------
+def einsum(spec: str, inputs, join_op: int = JOIN_MUL, agg_op: int = AGG_SUM, out_shape=None) -> np.ndarray:
+    """Dense join-agg: out[o] = AGG over contracted letters of JOIN(inputs)."""
+    ins = [_f64(a) for a in inputs]
+    lhs, rhs = spec.split("->")
+    in_specs = lhs.split(",")
+    if len(in_specs) != len(ins):
+        raise ValueError("input count does not match the spec")
+    sizes = {}
+    for s, a in zip(in_specs, ins):
+        for l, n in zip(s, a.shape):
+            sizes[l] = n
+    oshape = tuple(sizes[l] for l in rhs) if out_shape is None else tuple(out_shape)
+    out = np.empty(oshape, dtype=np.float64)
+    shapes = _i64([n for a in ins for n in a.shape] + list(oshape))
+    arr = (ctypes.POINTER(ctypes.c_double) * len(ins))(*[_dp(a) for a in ins])
+    _check(lib().or_einsum(spec.encode(), join_op, agg_op, _i64p(shapes), arr, _dp(out)), "einsum")
+    return out
+
+
+def matmul(a, b) -> np.ndarray:
+    a, b = _f64(a), _f64(b)
+    M, K = a.shape
+    K2, N = b.shape
+    if K != K2:
+        raise ValueError("inner dims differ")
+    c = np.empty((M, N), dtype=np.float64)
+    _check(lib().or_matmul(M, K, N, _dp(a), _dp(b), _dp(c)), "matmul")
+    return c
+
+
+def rmsnorm(x, w, eps: float) -> np.ndarray:
+    x, w = _f64(x), _f64(w)
+    T, C = x.shape
+    y = np.empty_like(x)
+    _check(lib().or_rmsnorm(T, C, _dp(x), _dp(w), eps, _dp(y)), "rmsnorm")
+    return y
+
+
+def softmax(s, causal: bool) -> np.ndarray:
+    s = _f64(s)
+    H, Q, K = s.shape
+    p = np.empty_like(s)
+    _check(lib().or_softmax(H, Q, K, _dp(s), int(causal), _dp(p)), "softmax")
+    return p
+
+
+def attention(q, k, v, causal: bool, scale: float) -> np.ndarray:
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    B, H, S, D = q.shape
+    o = np.empty_like(q)
+    _check(lib().or_attention(B, H, S, D, _dp(q), _dp(k), _dp(v), int(causal), scale, _dp(o)), "attention")
+    return o
+
+
+def silu_mul(g, u) -> np.ndarray:
+    g, u = _f64(g), _f64(u)
+    y = np.empty_like(g)
+    _check(lib().or_silu_mul(g.size, _dp(g), _dp(u), _dp(y)), "silu_mul")
+    return y
+
+
+def add(a, b) -> np.ndarray:
+    a, b = _f64(a), _f64(b)
+    y = np.empty_like(a)
+    _check(lib().or_add(a.size, _dp(a), _dp(b), _dp(y)), "add")
+    return y
+
+
+# --------------------------------------------------------------------------
+# composite: one GPU's share of a pre-norm LLaMA-shaped block
+# --------------------------------------------------------------------------
+def llama_block(x, n1, wqkv, wo, wg, wu, wd, n2, heads: int, d_head: int, eps: float):
+    """The block chain with a bf16 round-to-nearest-even at every relation
+    boundary (each arrow of the chain below stores a bf16 relation):
+
+      h1 = RMSNorm(x; n1) -> qkv = h1 W_qkv -> attn = CausalAttn(q, k, v)
+      -> x2 = x + attn W_o -> h2 = RMSNorm(x2; n2)
+      -> a = SiLU(h2 W_g) * (h2 W_u) -> y = x2 + a W_d
+
+    qkv's columns are [Q heads | K heads | V heads], head h of each taking
+    columns [h*d_head, (h+1)*d_head).  RoPE is not part of the chain.  Causal
+    attention makes row t of every output depend only on rows <= t of x, so a
+    prefix of x yields the same prefix of y.  All inputs are fp64 values.
+    Returns every boundary relation as a dict of dense fp64 arrays.
+    """
+    r = rne_bf16
+    T = x.shape[0]
+    hd = heads * d_head
+    h1 = r(rmsnorm(x, n1, eps))
+    qkv = r(matmul(h1, wqkv))
+
+    def heads_view(cols):
+        return np.ascontiguousarray(cols.reshape(T, heads, d_head).transpose(1, 0, 2))[None]
+
+    q = heads_view(qkv[:, 0:hd])
+    k = heads_view(qkv[:, hd:2 * hd])
+    v = heads_view(qkv[:, 2 * hd:3 * hd])
+    o = r(attention(q, k, v, True, 1.0 / np.sqrt(d_head)))
+    attn = np.ascontiguousarray(o[0].transpose(1, 0, 2).reshape(T, hd))
+    x2 = r(add(x, matmul(attn, wo)))
+    h2 = r(rmsnorm(x2, n2, eps))
+    a = r(silu_mul(matmul(h2, wg), matmul(h2, wu)))
+    y = r(add(x2, matmul(a, wd)))
+    return dict(h1=h1, qkv=qkv, attn=attn, x2=x2, h2=h2, a=a, y=y)
