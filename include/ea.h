@@ -1,0 +1,224 @@
+/*
+ * ea.h -- C ABI of libea, one GPU's share of a block join-agg on AMD MI355X
+ * (gfx950).
+ *
+ * Model (paper: "Every Kernel Is a Join: Automatic Multi-GPU Parallelism for
+ * AI Computations in Einsummable"):
+ *  - A tensor relation is a set of (sub_tensor_key, sub_tensor) pairs
+ *    (Section 1).  Here a relation is a dense zero-bounded tensor type
+ *    (Section 3.1, Definition "Tensor type") cut by a block partition whose
+ *    blocks tile it (Section 3.1, Definition "Tiling").  A block's key is its
+ *    per-dim block index; its sub-tensor type is (lo, hi) per dim.
+ *  - An operation runs as the three steps of Section 3.2, Definition
+ *    "Implementation": Join (tuples of one block per input whose shared
+ *    einsum letters have identical intervals, each tuple fed to a concrete
+ *    per-tuple kernel), Aggregate (tuple results with the same output key
+ *    combined by an associative, commutative operator), Recompose (each
+ *    aggregated block stored into its slot of the output relation).
+ *  - A repartition re-blocks a relation through the overlay of both
+ *    partitions (Section 5.3: atoms, decompose and recompose kernels).
+ *
+ * Memory.  Relation data live in caller-owned device memory (for example a
+ * torch uint8 tensor).  Handles hold only host metadata and never free data.
+ * Block layout: blocks in row-major order of their block coordinates; each
+ * block row-major (C order) over its own extents; each block starts at a
+ * multiple of 256 bytes from the relation's base; the relation's size ends at
+ * the last element of the last block (ea_layout_nbytes).  Padding bytes are
+ * never read for results and never written.
+ *
+ * Plans.  ea_joinagg / ea_repartition resolve their join (or overlay) once per
+ * configuration -- spec, ops, dtypes and partitions, not data pointers -- and
+ * keep the resulting tuple table in a library-owned device buffer (a plan).
+ * The first call for a configuration allocates that buffer, uploads block
+ * tables, runs the GPU join enumerator on the caller's stream and waits for
+ * it; later calls only enqueue kernels and never synchronize.  Plans live
+ * until ea_plan_cache_clear() or process exit.  Two calls that share a plan
+ * must not run concurrently on different streams (an attention plan holds a
+ * scratch area for its key-split partial results).
+ *
+ * Streams are hipStream_t passed as void*; NULL is the default stream.
+ *
+ * Errors.  Every call returns EA_OK (0) or a negative EA_ERR_* code and sets a
+ * thread-local message (ea_last_error).  No exception crosses the ABI.
+ * Argument, spec, partition and join validation runs on the host before any
+ * HIP call, so it works without a GPU.  Kernel faults surface as EA_ERR_HIP at
+ * the call that observes them.
+ */
+#ifndef EA_H
+#define EA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EA_VERSION 1
+#define EA_MAX_RANK 8
+#define EA_MAX_INPUTS 4
+
+/* ---- return codes ---------------------------------------------------- */
+#define EA_OK 0
+#define EA_ERR_ARG (-1)         /* NULL pointer, bad rank/size/enum value     */
+#define EA_ERR_DTYPE (-2)       /* dtype not supported for this operation     */
+#define EA_ERR_PARTITION (-3)   /* split points do not tile the shape         */
+#define EA_ERR_CAPACITY (-4)    /* buffer smaller than the layout / table     */
+#define EA_ERR_SPEC (-5)        /* einsum spec malformed or not matching      */
+#define EA_ERR_JOIN (-6)        /* shared letter split differently, or output */
+                                /* partition not the one the inputs induce    */
+#define EA_ERR_UNSUPPORTED (-7) /* valid request outside what is implemented  */
+#define EA_ERR_HIP (-8)         /* a HIP runtime call or kernel failed        */
+
+/* ---- element types --------------------------------------------------- */
+#define EA_F32 0
+#define EA_BF16 1
+#define EA_F16 2
+
+/* ---- join operations (the concrete operator f run on each tuple) ------ */
+/* Generic einsum join: the scalar join of the inputs' elements.            */
+#define EA_JOIN_MUL 0  /* product of the inputs (plain einsum)              */
+#define EA_JOIN_ADD 1  /* sum of the inputs                                 */
+/* Fused operators (each a join-agg with a fixed spec shape):               */
+#define EA_OP_RMSNORM 16   /* "<r>c,c-><r>c": y = w*x/sqrt(mean_c x^2 + eps) */
+#define EA_OP_SOFTMAX 17   /* "<r>k-><r>k": softmax over the last letter      */
+#define EA_OP_ATTENTION 18 /* "<b>qd,<b>kd,<b>kd-><b>qd": softmax(s*QK^T) V   */
+#define EA_OP_SWIGLU 19    /* "tj,jk,jk->tk": silu(X W1) * (X W2)              */
+
+/* ---- aggregation operations (the combiner of tuples sharing a key) ---- */
+#define EA_AGG_NONE 0 /* no aggregation: at most one tuple per output key    */
+#define EA_AGG_SUM 1  /* addition, identity 0                                */
+#define EA_AGG_MAX 2  /* maximum, identity -inf                              */
+#define EA_AGG_LSE 3  /* online softmax: (m, l, O) pairs combined by
+                         m = max(m1, m2), l = l1 e^(m1-m) + l2 e^(m2-m),
+                         O = O1 e^(m1-m) + O2 e^(m2-m)                       */
+
+typedef struct ea_relation ea_relation;
+
+/* Per-call parameters.  Zero-initialise and set what the operation uses. */
+typedef struct ea_params {
+  float eps;    /* EA_OP_RMSNORM: added to the mean square (e.g. 1e-6)       */
+  float scale;  /* EA_OP_ATTENTION: multiplier of the q.k scores             */
+  int32_t causal; /* EA_OP_SOFTMAX / EA_OP_ATTENTION: 1 = key position k is
+                     visible to query position q iff k <= q (0-based)        */
+  int32_t reserved;
+  /* Optional relation added to the aggregated result before the store
+     (fused residual): same shape and partition as the output.  Used by the
+     einsum path (EA_JOIN_MUL / EA_JOIN_ADD).  NULL = none.                  */
+  const ea_relation* residual;
+} ea_params;
+
+/* ---- version and errors ---------------------------------------------- */
+int ea_version(void);
+/* Message for the last non-zero return on this thread ("" if none).  The
+   pointer stays valid until the next ea_* call on the same thread. */
+const char* ea_last_error(void);
+/* Bytes per element of a dtype, or EA_ERR_DTYPE. */
+int ea_dtype_size(int32_t dtype);
+
+/* ---- layout and relations (Section 3.1) ------------------------------- */
+/* Bytes a relation of this shape, dtype and partition occupies.
+   rank in [1, 8]; shape[d] >= 1; nblocks[d] >= 1; splits concatenates, per
+   dim, nblocks[d]+1 strictly increasing points from 0 to shape[d].
+   Errors: EA_ERR_ARG, EA_ERR_DTYPE, EA_ERR_PARTITION. */
+int ea_layout_nbytes(int32_t rank, const int64_t* shape, int32_t dtype,
+                     const int32_t* nblocks, const int64_t* splits, int64_t* nbytes);
+
+/* Create a relation handle over caller-owned device memory.
+   data: base of the block-major storage (may be NULL for metadata-only use;
+   compute calls then fail with EA_ERR_ARG); capacity: its size in bytes,
+   >= ea_layout_nbytes unless data is NULL.  Arrays are copied.
+   Errors: EA_ERR_ARG, EA_ERR_DTYPE, EA_ERR_PARTITION, EA_ERR_CAPACITY. */
+int ea_relation_create(int32_t rank, const int64_t* shape, int32_t dtype,
+                       const int32_t* nblocks, const int64_t* splits,
+                       void* data, int64_t capacity, ea_relation** out);
+/* Free the handle (never the data).  NULL is accepted and ignored. */
+int ea_relation_destroy(ea_relation* rel);
+/* Re-point a relation at other memory of at least its layout's size. */
+int ea_relation_set_data(ea_relation* rel, void* data, int64_t capacity);
+int ea_relation_num_blocks(const ea_relation* rel, int64_t* n);
+int ea_relation_nbytes(const ea_relation* rel, int64_t* nbytes);
+/* Block b's key as its sub-tensor type: lo[d] inclusive, hi[d] exclusive
+   (arrays of the relation's rank), and its byte offset from the base. */
+int ea_relation_block(const ea_relation* rel, int64_t b, int64_t* lo, int64_t* hi,
+                      int64_t* byte_off);
+
+/* ---- join-agg (Section 3.2, Definitions "Join-agg spec", "Implementation")
+   spec: explicit einsum "ij,jk->ik" over letters a-z/A-Z.  in[i] takes the
+   letters of the i-th operand; out the letters after "->".  Every letter
+   shared by two or more operands must have the same extent and the same
+   split points in each (EA_ERR_JOIN otherwise: repartition first); the
+   output's partition on each letter must equal the inputs' (EA_ERR_JOIN).
+   Tuples are grouped by output key; inside a group they are combined by
+   agg_op in ascending order of the contracted letters' blocks, so results
+   are deterministic (no atomics in the combine).
+
+   join_op EA_JOIN_MUL / EA_JOIN_ADD, agg_op NONE / SUM / MAX: out[o] =
+     AGG over contracted letter values of JOIN(in_1[..], ..., in_n[..]),
+     then + residual if given.  NONE requires no contracted letters.  Inputs
+     and output f32, bf16 or f16; arithmetic in f32.  A two-operand product
+     "ab,bc->ac" or "ab,cb->ac" with bf16 inputs runs on the bf16 matrix
+     cores (fp32 accumulation).
+   EA_OP_RMSNORM, agg SUM: in = (x "<r>c", w "c"); out "<r>c" with x's
+     letters; y = w * x / sqrt(sum_c x^2 / C + eps) over the full extent C
+     of the last letter (params->eps).  The sum of squares is aggregated
+     over all blocks of c.  bf16/f32 data, f32 arithmetic.
+   EA_OP_SOFTMAX, agg LSE: in = s "<r>k" (rank >= 2 if causal), out with the
+     same letters; softmax over the last letter; with params->causal the
+     second-to-last letter is the query position and invisible entries are 0.
+   EA_OP_ATTENTION, agg LSE: in = (Q "<b>qd", K "<b>kd", V "<b>kd"), out
+     "<b>qd"; O = softmax(scale * Q K^T) V per batch letters <b>; d must be
+     a single block of extent 128; q and k block extents multiples of 128;
+     the causal rule needs q and k of the same extent; bf16 data.
+     Scores and softmax in f32; the probabilities are rounded to fp16 and V
+     converted to fp16 for the P.V product (fp32 accumulation), so V values
+     must lie within the fp16 range.
+   EA_OP_SWIGLU, agg SUM: in = (X "tj", W1 "jk", W2 "jk"), out "tk" =
+     silu(X W1) * (X W2), silu(g) = g / (1 + e^-g); bf16 data.
+   Errors: EA_ERR_ARG, EA_ERR_SPEC, EA_ERR_DTYPE, EA_ERR_JOIN,
+   EA_ERR_UNSUPPORTED, EA_ERR_HIP.  Asynchronous on `stream` after the
+   first call of a configuration. */
+int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in,
+               const ea_relation* const* in, ea_relation* out,
+               const ea_params* params, void* stream);
+
+/* ---- the join alone (Section 3.2 step 1, Section 3.3) -------------------
+   Writes the plan's GPU-built tuple table into caller device buffers:
+   tuples[n_tuples][1 + n_in] int32 = (output block, input blocks...),
+   group_off[n_groups + 1] int64 CSR offsets of the groups (groups = all block
+   combinations of the group letters: the output letters, minus the last one
+   for RMSNORM and SOFTMAX).  Order: group-major, then the remaining letters'
+   block coordinates in order of first appearance across the inputs.
+   Causal (params->causal) drops a tuple iff its key block starts after its
+   last query position.  Synchronizes `stream`.  Errors as ea_joinagg, plus
+   EA_ERR_CAPACITY when cap or gcap is too small (counts still written). */
+int ea_join_tuples(const char* spec, int32_t join_op, int32_t n_in,
+                   const ea_relation* const* in, const ea_relation* out,
+                   const ea_params* params, int32_t* tuples, int64_t cap,
+                   int64_t* group_off, int64_t gcap, int64_t* n_tuples,
+                   int64_t* n_groups, void* stream);
+
+/* ---- repartition (Section 5.3: overlay atoms, decompose, recompose) ------
+   dst receives src's dense tensor under dst's partition.  Same rank, shape
+   and dtype (EA_ERR_ARG otherwise); src and dst memory must not overlap.
+   Bit-exact byte movement.  Asynchronous on `stream`. */
+int ea_repartition(const ea_relation* src, ea_relation* dst, void* stream);
+
+/* Overlay of two partitions of one shape (Section 5.3): per dim the sorted
+   union of both split lists.  nblocks_out[rank]; splits_out must hold the
+   sum over dims of (nblocks_a[d] + nblocks_b[d] + 1) entries.  Host only. */
+int ea_overlay(int32_t rank, const int32_t* nblocks_a, const int64_t* splits_a,
+               const int32_t* nblocks_b, const int64_t* splits_b,
+               int32_t* nblocks_out, int64_t* splits_out);
+
+/* ---- plan cache --------------------------------------------------------- */
+/* Number of cached plans (all devices). */
+int64_t ea_plan_cache_size(void);
+/* Free every cached plan.  Must not run while kernels of a plan are in
+   flight (it synchronizes the device of each plan first). */
+int ea_plan_cache_clear(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EA_H */

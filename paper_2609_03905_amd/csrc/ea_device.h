@@ -1,0 +1,65 @@
+// ea_device.h -- element conversions and wavefront helpers shared by libea's
+// kernels.  gfx950, wave64.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "ea_internal.h"
+
+namespace ea {
+
+// bf16 <-> f32.  Widening is exact; narrowing rounds to nearest, ties to even
+// (NaN stays NaN).
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float f16_to_f32(uint16_t h) {
+  _Float16 v;
+  __builtin_memcpy(&v, &h, 2);
+  return (float)v;
+}
+
+__device__ __forceinline__ uint16_t f32_to_f16(float f) {
+  _Float16 v = (_Float16)f;
+  uint16_t h;
+  __builtin_memcpy(&h, &v, 2);
+  return h;
+}
+
+// Load/store one element of a relation given its dtype.
+__device__ __forceinline__ float ld_elem(const char* base, int64_t idx, int dt) {
+  if (dt == EA_F32) return reinterpret_cast<const float*>(base)[idx];
+  const uint16_t h = reinterpret_cast<const uint16_t*>(base)[idx];
+  return dt == EA_BF16 ? bf16_to_f32(h) : f16_to_f32(h);
+}
+
+__device__ __forceinline__ void st_elem(char* base, int64_t idx, int dt, float v) {
+  if (dt == EA_F32) {
+    reinterpret_cast<float*>(base)[idx] = v;
+  } else {
+    reinterpret_cast<uint16_t*>(base)[idx] = dt == EA_BF16 ? f32_to_bf16(v) : f32_to_f16(v);
+  }
+}
+
+// Wavefront (64 lanes) reductions.
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+}  // namespace ea

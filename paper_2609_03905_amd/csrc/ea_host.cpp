@@ -1,0 +1,1321 @@
+// ea_host.cpp -- libea host side: relation handles, layout, validation, spec
+// parsing, join analysis, the plan cache and kernel dispatch.
+//
+// Nothing here computes a result: every step of a join-agg or repartition runs
+// in the HIP kernels.  This file decides, for each call, which kernel runs on
+// which blocks and tuples, and builds the device plan those kernels read.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <sstream>
+#include <string>
+#include <vector>
+
+#include "ea_internal.h"
+
+using namespace ea;
+
+struct ea_relation {
+  int32_t rank = 0;
+  int32_t dtype = 0;
+  int64_t shape[kMaxRank] = {};
+  int32_t nb[kMaxRank] = {};
+  std::vector<int64_t> splits[kMaxRank];
+  std::vector<int64_t> off;  // byte offset of every block
+  int64_t nblocks = 0;
+  int64_t nbytes = 0;
+  void* data = nullptr;
+  int64_t capacity = 0;
+};
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// errors
+// ---------------------------------------------------------------------------
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[1024];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return EA_OK;
+}
+
+#define EA_HIP_TRY(expr)                                                              \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess)                                                             \
+      return fail(EA_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));         \
+  } while (0)
+
+int dtype_size(int32_t dt) {
+  switch (dt) {
+    case EA_F32: return 4;
+    case EA_BF16: return 2;
+    case EA_F16: return 2;
+    default: return EA_ERR_DTYPE;
+  }
+}
+
+int64_t align256(int64_t x) { return (x + 255) / 256 * 256; }
+
+// ---------------------------------------------------------------------------
+// partitions and layout
+// ---------------------------------------------------------------------------
+int check_partition(int32_t rank, const int64_t* shape, const int32_t* nblocks,
+                    const int64_t* splits) {
+  if (rank < 1 || rank > kMaxRank) return fail(EA_ERR_ARG, "rank %d outside [1, %d]", rank, kMaxRank);
+  if (!shape || !nblocks || !splits) return fail(EA_ERR_ARG, "NULL shape, nblocks or splits");
+  const int64_t* s = splits;
+  int64_t total_blocks = 1;
+  for (int d = 0; d < rank; ++d) {
+    if (shape[d] < 1 || shape[d] > INT32_MAX)
+      return fail(EA_ERR_ARG, "extent %lld of dim %d outside [1, 2^31)", (long long)shape[d], d);
+    if (nblocks[d] < 1 || nblocks[d] > shape[d])
+      return fail(EA_ERR_PARTITION, "dim %d: %d blocks for extent %lld", d, nblocks[d],
+                  (long long)shape[d]);
+    if (s[0] != 0) return fail(EA_ERR_PARTITION, "dim %d: first split point is not 0", d);
+    for (int b = 0; b < nblocks[d]; ++b)
+      if (s[b + 1] <= s[b])
+        return fail(EA_ERR_PARTITION, "dim %d: split points not strictly increasing at %d", d, b);
+    if (s[nblocks[d]] != shape[d])
+      return fail(EA_ERR_PARTITION, "dim %d: last split point %lld is not the extent %lld", d,
+                  (long long)s[nblocks[d]], (long long)shape[d]);
+    total_blocks *= nblocks[d];
+    if (total_blocks > INT32_MAX) return fail(EA_ERR_ARG, "too many blocks");
+    s += nblocks[d] + 1;
+  }
+  return EA_OK;
+}
+
+void fill_layout(ea_relation* r) {
+  r->nblocks = 1;
+  for (int d = 0; d < r->rank; ++d) r->nblocks *= r->nb[d];
+  r->off.assign((size_t)r->nblocks, 0);
+  const int es = dtype_size(r->dtype);
+  int64_t pos = 0, end = 0;
+  int32_t c[kMaxRank] = {};
+  for (int64_t b = 0; b < r->nblocks; ++b) {
+    int64_t n = 1;
+    for (int d = 0; d < r->rank; ++d) n *= r->splits[d][c[d] + 1] - r->splits[d][c[d]];
+    pos = align256(pos);
+    r->off[(size_t)b] = pos;
+    end = pos + n * es;
+    pos = end;
+    for (int d = r->rank - 1; d >= 0; --d) {  // next block coordinates, row-major
+      if (++c[d] < r->nb[d]) break;
+      c[d] = 0;
+    }
+  }
+  r->nbytes = end;
+}
+
+void block_coords(const ea_relation* r, int64_t b, int32_t* c) {
+  for (int d = r->rank - 1; d >= 0; --d) {
+    c[d] = (int32_t)(b % r->nb[d]);
+    b /= r->nb[d];
+  }
+}
+
+std::vector<DevBlk> dev_blocks(const ea_relation* r) {
+  std::vector<DevBlk> v((size_t)r->nblocks);
+  int32_t c[kMaxRank];
+  for (int64_t b = 0; b < r->nblocks; ++b) {
+    block_coords(r, b, c);
+    DevBlk& x = v[(size_t)b];
+    memset(&x, 0, sizeof(x));
+    x.off = r->off[(size_t)b];
+    for (int d = 0; d < r->rank; ++d) {
+      x.lo[d] = (int32_t)r->splits[d][c[d]];
+      x.ext[d] = (int32_t)(r->splits[d][c[d] + 1] - r->splits[d][c[d]]);
+    }
+  }
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// einsum spec
+// ---------------------------------------------------------------------------
+struct Spec {
+  int n_in = 0;
+  int rank[kMaxOps] = {};
+  char let[kMaxOps][kMaxRank] = {};
+};
+
+bool is_letter(char ch) { return (ch >= 'a' && ch <= 'z') || (ch >= 'A' && ch <= 'Z'); }
+
+int parse_spec(const char* s, Spec* sp) {
+  if (!s) return fail(EA_ERR_ARG, "NULL spec");
+  *sp = Spec();
+  const char* arrow = strstr(s, "->");
+  if (!arrow) return fail(EA_ERR_SPEC, "spec '%s' has no '->'", s);
+  int op = 0, r = 0;
+  auto add = [&](char ch) -> int {
+    if (!is_letter(ch)) return fail(EA_ERR_SPEC, "spec '%s': bad character '%c'", s, ch);
+    if (r >= kMaxRank) return fail(EA_ERR_SPEC, "spec '%s': operand rank above %d", s, kMaxRank);
+    for (int i = 0; i < r; ++i)
+      if (sp->let[op][i] == ch) return fail(EA_ERR_SPEC, "spec '%s': letter '%c' repeats in an operand", s, ch);
+    sp->let[op][r++] = ch;
+    return EA_OK;
+  };
+  for (const char* p = s; p != arrow; ++p) {
+    if (*p == ',') {
+      if (r == 0) return fail(EA_ERR_SPEC, "spec '%s': empty operand", s);
+      if (op + 1 >= kMaxIn) return fail(EA_ERR_SPEC, "spec '%s': more than %d inputs", s, kMaxIn);
+      sp->rank[op++] = r;
+      r = 0;
+      continue;
+    }
+    int e = add(*p);
+    if (e) return e;
+  }
+  if (r == 0) return fail(EA_ERR_SPEC, "spec '%s': empty operand", s);
+  sp->rank[op++] = r;
+  r = 0;
+  sp->n_in = op;
+  for (const char* p = arrow + 2; *p; ++p) {
+    int e = add(*p);
+    if (e) return e;
+  }
+  if (r == 0) return fail(EA_ERR_SPEC, "spec '%s': empty output", s);
+  sp->rank[op] = r;
+  for (int i = 0; i < r; ++i) {
+    bool found = false;
+    for (int o = 0; o < sp->n_in && !found; ++o)
+      for (int j = 0; j < sp->rank[o]; ++j) found |= sp->let[o][j] == sp->let[op][i];
+    if (!found) return fail(EA_ERR_SPEC, "spec '%s': output letter '%c' in no input", s, sp->let[op][i]);
+  }
+  return EA_OK;
+}
+
+int find_dim(const Spec& sp, int op, char l) {
+  for (int d = 0; d < sp.rank[op]; ++d)
+    if (sp.let[op][d] == l) return d;
+  return -1;
+}
+
+// ---------------------------------------------------------------------------
+// join analysis: letter order, partitions, validation (Section 3.2)
+// ---------------------------------------------------------------------------
+struct JoinInfo {
+  std::vector<char> letters;                  // group letters, then the rest
+  int n_group = 0;
+  std::vector<std::vector<int64_t>> lsplits;  // per letter: its split points
+  std::vector<int64_t> lext;
+  int index(char l) const {
+    for (size_t i = 0; i < letters.size(); ++i)
+      if (letters[i] == l) return (int)i;
+    return -1;
+  }
+};
+
+// ops: n_in inputs then the output.  group: output letters that key a group.
+int analyze_join(const Spec& sp, const ea_relation* const* ops, const std::string& group, JoinInfo* ji) {
+  const int n_ops = sp.n_in + 1;
+  for (int o = 0; o < n_ops; ++o)
+    if (ops[o]->rank != sp.rank[o])
+      return fail(EA_ERR_SPEC, "operand %d has rank %d but the spec gives it %d letters", o, ops[o]->rank,
+                  sp.rank[o]);
+  *ji = JoinInfo();
+  for (char l : group) ji->letters.push_back(l);
+  ji->n_group = (int)group.size();
+  for (int o = 0; o < sp.n_in; ++o)
+    for (int d = 0; d < sp.rank[o]; ++d)
+      if (ji->index(sp.let[o][d]) < 0) ji->letters.push_back(sp.let[o][d]);
+  if ((int)ji->letters.size() > kMaxLetters) return fail(EA_ERR_UNSUPPORTED, "more than %d letters", kMaxLetters);
+  ji->lsplits.assign(ji->letters.size(), {});
+  ji->lext.assign(ji->letters.size(), 0);
+  for (size_t li = 0; li < ji->letters.size(); ++li) {
+    const char l = ji->letters[li];
+    int first_op = -1;
+    for (int o = 0; o < n_ops; ++o) {
+      const int d = find_dim(sp, o, l);
+      if (d < 0) continue;
+      if (first_op < 0) {
+        first_op = o;
+        ji->lsplits[li] = ops[o]->splits[d];
+        ji->lext[li] = ops[o]->shape[d];
+        continue;
+      }
+      if (ops[o]->shape[d] != ji->lext[li])
+        return fail(EA_ERR_SPEC, "letter '%c' has extent %lld in operand %d and %lld in operand %d", l,
+                    (long long)ji->lext[li], first_op, (long long)ops[o]->shape[d], o);
+      if (ops[o]->splits[d] != ji->lsplits[li]) {
+        if (o == sp.n_in)
+          return fail(EA_ERR_JOIN,
+                      "output partition on letter '%c' differs from the inputs' (the output tiling "
+                      "must be the one the join induces)", l);
+        return fail(EA_ERR_JOIN,
+                    "letter '%c' is split differently in operands %d and %d; repartition first", l,
+                    first_op, o);
+      }
+    }
+  }
+  return EA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// plan image: host-built sections uploaded once into the plan's device buffer
+// ---------------------------------------------------------------------------
+struct Image {
+  std::vector<uint8_t> bytes;
+  size_t put(const void* p, size_t n) {
+    size_t o = (size_t)align256((int64_t)bytes.size());
+    bytes.resize(o + std::max<size_t>(n, 1), 0);
+    if (n) memcpy(bytes.data() + o, p, n);
+    return o;
+  }
+  size_t put_zero(size_t n) {
+    size_t o = (size_t)align256((int64_t)bytes.size());
+    bytes.resize(o + std::max<size_t>(n, 1), 0);
+    return o;
+  }
+  template <class T>
+  size_t put_vec(const std::vector<T>& v) { return put(v.data(), v.size() * sizeof(T)); }
+};
+
+enum Kind { K_GENERIC = 1, K_GEMM, K_RMSNORM, K_SOFTMAX, K_ATTENTION, K_REPART };
+
+struct Plan {
+  int device = 0;
+  Kind kind = K_GENERIC;
+  char* dmem = nullptr;
+  size_t dbytes = 0;
+  // join
+  int n_in = 0;
+  int64_t n_groups = 0, tuple_cap = 0;
+  int32_t* d_tuples = nullptr;
+  int32_t* d_goff = nullptr;
+  int32_t* d_count = nullptr;
+  const DevBlk* d_blk[kMaxOps] = {};
+  // kernel-specific
+  const void* d_desc = nullptr;
+  const void* d_work = nullptr;
+  int64_t n_work = 0;
+  // gemm
+  int b_kmajor = 0;
+  // rows
+  int32_t row_len = 0;
+  int32_t row_vec = 0;
+  // attention scratch
+  float* part_o = nullptr;
+  float* part_ml = nullptr;
+  int32_t* counters = nullptr;
+  ~Plan() {
+    if (dmem) {
+      int cur = 0;
+      if (hipGetDevice(&cur) == hipSuccess) {
+        (void)hipSetDevice(device);
+        (void)hipDeviceSynchronize();
+        (void)hipFree(dmem);
+        (void)hipSetDevice(cur);
+      }
+    }
+  }
+};
+
+std::mutex g_cache_mu;
+std::map<std::string, std::unique_ptr<Plan>>& cache() {
+  static auto* m = new std::map<std::string, std::unique_ptr<Plan>>();  // intentionally leaked at exit
+  return *m;
+}
+
+void key_rel(std::ostringstream& k, const ea_relation* r) {
+  k << "|t" << r->dtype << "r" << r->rank;
+  for (int d = 0; d < r->rank; ++d) {
+    k << "[";
+    for (int64_t s : r->splits[d]) k << s << ",";
+    k << "]";
+  }
+}
+
+// Allocate the plan's device buffer (image + extra zeroed scratch) and upload.
+int plan_upload(Plan* p, const Image& img, size_t extra, size_t* extra_off, hipStream_t s) {
+  const size_t base = (size_t)align256((int64_t)img.bytes.size());
+  p->dbytes = base + extra;
+  EA_HIP_TRY(hipGetDevice(&p->device));
+  EA_HIP_TRY(hipMalloc((void**)&p->dmem, p->dbytes));
+  EA_HIP_TRY(hipMemcpyAsync(p->dmem, img.bytes.data(), img.bytes.size(), hipMemcpyHostToDevice, s));
+  if (extra) EA_HIP_TRY(hipMemsetAsync(p->dmem + base, 0, extra, s));
+  if (extra_off) *extra_off = base;
+  return EA_OK;
+}
+
+// Build the enumerator description and reserve the tuple table.
+struct JoinSections {
+  size_t desc, splits, tuples, goff, count;
+  size_t blk[kMaxOps];
+};
+
+int build_join(const Spec& sp, const ea_relation* const* ops, const JoinInfo& ji, int causal, char cq,
+               char ck, Image* img, JoinSections* js, int64_t* n_groups, int64_t* tuple_cap) {
+  EnumDesc e;
+  memset(&e, 0, sizeof(e));
+  e.n_in = sp.n_in;
+  e.n_letters = (int32_t)ji.letters.size();
+  e.n_group_letters = ji.n_group;
+  std::vector<int32_t> sp32;
+  int64_t per_group = 1, ng = 1;
+  for (size_t li = 0; li < ji.letters.size(); ++li) {
+    e.letter_nb[li] = (int32_t)(ji.lsplits[li].size() - 1);
+    e.letter_split[li] = (int32_t)sp32.size();
+    for (int64_t v : ji.lsplits[li]) sp32.push_back((int32_t)v);
+    if ((int)li < ji.n_group) ng *= e.letter_nb[li];
+    else per_group *= e.letter_nb[li];
+  }
+  for (int o = 0; o <= sp.n_in; ++o) {
+    e.op_rank[o] = sp.rank[o];
+    for (int d = 0; d < sp.rank[o]; ++d) {
+      e.op_letter[o][d] = ji.index(sp.let[o][d]);
+      e.op_nb[o][d] = ops[o]->nb[d];
+      e.op_split[o][d] = (int32_t)sp32.size();
+      for (int64_t v : ops[o]->splits[d]) sp32.push_back((int32_t)v);
+    }
+  }
+  e.causal = causal;
+  if (causal) {
+    e.cq = ji.index(cq);
+    e.ck = ji.index(ck);
+    if (e.cq < 0 || e.ck < 0) return fail(EA_ERR_SPEC, "causal letters not in the spec");
+  }
+  e.per_group = per_group;
+  e.n_groups = ng;
+  e.n_cand = per_group * ng;
+  if (e.n_cand > (int64_t)1 << 26) return fail(EA_ERR_UNSUPPORTED, "join space of %lld candidates is too large", (long long)e.n_cand);
+  js->desc = img->put(&e, sizeof(e));
+  js->splits = img->put_vec(sp32);
+  js->tuples = img->put_zero((size_t)e.n_cand * (size_t)(sp.n_in + 1) * sizeof(int32_t));
+  js->goff = img->put_zero((size_t)(ng + 1) * sizeof(int32_t));
+  js->count = img->put_zero(sizeof(int32_t));
+  for (int o = 0; o <= sp.n_in; ++o) js->blk[o] = img->put_vec(dev_blocks(ops[o]));
+  *n_groups = ng;
+  *tuple_cap = e.n_cand;
+  return EA_OK;
+}
+
+int finish_join(Plan* p, const JoinSections& js, int n_ops, hipStream_t s) {
+  p->d_tuples = (int32_t*)(p->dmem + js.tuples);
+  p->d_goff = (int32_t*)(p->dmem + js.goff);
+  p->d_count = (int32_t*)(p->dmem + js.count);
+  for (int o = 0; o < n_ops; ++o) p->d_blk[o] = (const DevBlk*)(p->dmem + js.blk[o]);
+  EA_HIP_TRY(launch_enumerate((const EnumDesc*)(p->dmem + js.desc), (const int32_t*)(p->dmem + js.splits),
+                              p->d_tuples, p->d_goff, p->d_count, s));
+  EA_HIP_TRY(hipStreamSynchronize(s));
+  return EA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// operation classification and validation
+// ---------------------------------------------------------------------------
+struct OpInfo {
+  Kind kind = K_GENERIC;
+  std::string group;   // group letters
+  int causal = 0;      // the kernel masks keys after the query position
+  int join_causal = 0; // the join drops tuples whose key block is fully masked
+  char cq = 0, ck = 0; // causal letters
+  int b_kmajor = 0;
+  int q_dim = 0, k_dim = 0;
+};
+
+bool is_float_dtype(int32_t dt) { return dt == EA_F32 || dt == EA_BF16 || dt == EA_F16; }
+
+int classify(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation* const* ops,
+             const ea_params* prm, OpInfo* oi) {
+  const int n_in = sp.n_in, out = n_in;
+  const ea_relation* o = ops[out];
+  std::string out_letters(sp.let[out], sp.let[out] + sp.rank[out]);
+  *oi = OpInfo();
+  for (int i = 0; i <= n_in; ++i)
+    if (!is_float_dtype(ops[i]->dtype)) return fail(EA_ERR_DTYPE, "operand %d has an unknown dtype", i);
+  switch (join_op) {
+    case EA_JOIN_MUL:
+    case EA_JOIN_ADD: {
+      if (agg_op != EA_AGG_NONE && agg_op != EA_AGG_SUM && agg_op != EA_AGG_MAX)
+        return fail(EA_ERR_ARG, "einsum joins aggregate with NONE, SUM or MAX");
+      bool contracted = false;
+      for (int i = 0; i < n_in; ++i)
+        for (int d = 0; d < sp.rank[i]; ++d) contracted |= find_dim(sp, out, sp.let[i][d]) < 0;
+      if (agg_op == EA_AGG_NONE && contracted)
+        return fail(EA_ERR_SPEC, "aggregation NONE with contracted letters: several tuples share an output key");
+      oi->group = out_letters;
+      oi->kind = K_GENERIC;
+      if (prm && prm->residual) {
+        const ea_relation* r = prm->residual;
+        if (r->rank != o->rank || r->dtype != o->dtype)
+          return fail(EA_ERR_ARG, "residual relation must have the output's rank and dtype");
+        for (int d = 0; d < o->rank; ++d)
+          if (r->splits[d] != o->splits[d]) return fail(EA_ERR_ARG, "residual partition differs from the output's");
+        if (!r->data) return fail(EA_ERR_ARG, "residual relation has no data");
+      }
+      // matrix-core path: "ab,bc->ac" or "ab,cb->ac", 16-bit inputs, SUM of products
+      if (join_op == EA_JOIN_MUL && agg_op == EA_AGG_SUM && n_in == 2 && sp.rank[0] == 2 &&
+          sp.rank[1] == 2 && sp.rank[2] == 2 && ops[0]->dtype == ops[1]->dtype &&
+          (ops[0]->dtype == EA_BF16 || ops[0]->dtype == EA_F16)) {
+        const char a = sp.let[0][0], b = sp.let[0][1];
+        const char* L1 = sp.let[1];
+        const char* L2 = sp.let[2];
+        int kmaj = -1;
+        char c = 0;
+        if (L1[0] == b && L1[1] != a && L1[1] != b) { kmaj = 0; c = L1[1]; }
+        else if (L1[1] == b && L1[0] != a && L1[0] != b) { kmaj = 1; c = L1[0]; }
+        if (kmaj >= 0 && L2[0] == a && L2[1] == c) {
+          bool aligned = true;  // 16-byte vector loads need 8-element-aligned rows
+          for (int64_t v : ops[0]->splits[1]) aligned &= v % 8 == 0;
+          for (int64_t v : ops[1]->splits[1]) aligned &= v % 8 == 0;
+          if (aligned) {
+            oi->kind = K_GEMM;
+            oi->b_kmajor = kmaj;
+          }
+        }
+      }
+      return EA_OK;
+    }
+    case EA_OP_SWIGLU: {
+      if (agg_op != EA_AGG_SUM) return fail(EA_ERR_ARG, "SWIGLU aggregates with SUM");
+      if (n_in != 3 || sp.rank[0] != 2 || sp.rank[1] != 2 || sp.rank[2] != 2 || sp.rank[3] != 2)
+        return fail(EA_ERR_SPEC, "SWIGLU spec must be 'tj,jk,jk->tk' (or 'tj,kj,kj->tk')");
+      const char t = sp.let[0][0], j = sp.let[0][1];
+      int kmaj = -1;
+      char k = 0;
+      if (sp.let[1][0] == j) { kmaj = 0; k = sp.let[1][1]; }
+      else if (sp.let[1][1] == j) { kmaj = 1; k = sp.let[1][0]; }
+      if (kmaj < 0 || k == t || k == j || sp.let[2][0] != sp.let[1][0] || sp.let[2][1] != sp.let[1][1] ||
+          sp.let[3][0] != t || sp.let[3][1] != k)
+        return fail(EA_ERR_SPEC, "SWIGLU spec must be 'tj,jk,jk->tk' (or 'tj,kj,kj->tk')");
+      for (int i = 0; i < 3; ++i)
+        if (ops[i]->dtype != EA_BF16 && ops[i]->dtype != EA_F16)
+          return fail(EA_ERR_DTYPE, "SWIGLU takes bf16 or f16 inputs");
+      if (ops[1]->dtype != ops[0]->dtype || ops[2]->dtype != ops[0]->dtype)
+        return fail(EA_ERR_DTYPE, "SWIGLU inputs must share one dtype");
+      for (int64_t v : ops[0]->splits[1])
+        if (v % 8) return fail(EA_ERR_UNSUPPORTED, "SWIGLU needs contracted block bounds that are multiples of 8");
+      for (int64_t v : ops[1]->splits[1])
+        if (v % 8) return fail(EA_ERR_UNSUPPORTED, "SWIGLU needs weight block bounds that are multiples of 8");
+      if (prm && prm->residual) return fail(EA_ERR_UNSUPPORTED, "SWIGLU takes no residual");
+      oi->kind = K_GEMM;
+      oi->b_kmajor = kmaj;
+      oi->group = out_letters;
+      return EA_OK;
+    }
+    case EA_OP_RMSNORM: {
+      if (agg_op != EA_AGG_SUM) return fail(EA_ERR_ARG, "RMSNORM aggregates its sum of squares with SUM");
+      if (n_in != 2 || sp.rank[1] != 1 || sp.rank[out] != sp.rank[0])
+        return fail(EA_ERR_SPEC, "RMSNORM spec must be '<r>c,c-><r>c'");
+      const char c = sp.let[0][sp.rank[0] - 1];
+      if (sp.let[1][0] != c || out_letters != std::string(sp.let[0], sp.let[0] + sp.rank[0]))
+        return fail(EA_ERR_SPEC, "RMSNORM spec must be '<r>c,c-><r>c'");
+      if (!prm || !(prm->eps >= 0.0f)) return fail(EA_ERR_ARG, "RMSNORM needs params with eps >= 0");
+      if (ops[0]->dtype == EA_F16 || ops[1]->dtype == EA_F16 || o->dtype == EA_F16)
+        return fail(EA_ERR_DTYPE, "RMSNORM takes f32 or bf16");
+      if (prm->residual) return fail(EA_ERR_UNSUPPORTED, "RMSNORM takes no residual");
+      oi->kind = K_RMSNORM;
+      oi->group = out_letters.substr(0, out_letters.size() - 1);
+      return EA_OK;
+    }
+    case EA_OP_SOFTMAX: {
+      if (agg_op != EA_AGG_LSE) return fail(EA_ERR_ARG, "SOFTMAX aggregates with LSE (max, then sum)");
+      if (n_in != 1 || out_letters != std::string(sp.let[0], sp.let[0] + sp.rank[0]))
+        return fail(EA_ERR_SPEC, "SOFTMAX spec must be 'X->X'");
+      if (ops[0]->dtype == EA_F16 || o->dtype == EA_F16) return fail(EA_ERR_DTYPE, "SOFTMAX takes f32 or bf16");
+      const int causal = prm ? prm->causal : 0;
+      if (causal && sp.rank[0] < 2) return fail(EA_ERR_SPEC, "causal SOFTMAX needs a query letter");
+      if (prm && prm->residual) return fail(EA_ERR_UNSUPPORTED, "SOFTMAX takes no residual");
+      // Masked entries of a softmax are stored zeros of the output, so its
+      // join keeps every key block; the kernel applies the mask per element.
+      oi->kind = K_SOFTMAX;
+      oi->group = out_letters.substr(0, out_letters.size() - 1);
+      oi->causal = causal;
+      return EA_OK;
+    }
+    case EA_OP_ATTENTION: {
+      if (agg_op != EA_AGG_LSE) return fail(EA_ERR_ARG, "ATTENTION aggregates with LSE (online softmax)");
+      if (n_in != 3) return fail(EA_ERR_SPEC, "ATTENTION spec must be '<b>qd,<b>kd,<b>kd-><b>qd'");
+      const int r = sp.rank[0];
+      bool good = r >= 2 && sp.rank[1] == r && sp.rank[2] == r && sp.rank[out] == r;
+      char q = 0, k = 0, d = 0;
+      if (good) {
+        q = sp.let[0][r - 2];
+        d = sp.let[0][r - 1];
+        k = sp.let[1][r - 2];
+        good = k != q && k != d && sp.let[1][r - 1] == d && sp.let[2][r - 2] == k && sp.let[2][r - 1] == d;
+        for (int i = 0; i < r - 2 && good; ++i)
+          good = sp.let[1][i] == sp.let[0][i] && sp.let[2][i] == sp.let[0][i];
+        good = good && out_letters == std::string(sp.let[0], sp.let[0] + r);
+      }
+      if (!good) return fail(EA_ERR_SPEC, "ATTENTION spec must be '<b>qd,<b>kd,<b>kd-><b>qd'");
+      for (int i = 0; i < 3; ++i)
+        if (ops[i]->dtype != EA_BF16) return fail(EA_ERR_DTYPE, "ATTENTION takes bf16 Q, K, V");
+      if (o->dtype == EA_F16) return fail(EA_ERR_DTYPE, "ATTENTION writes f32 or bf16");
+      if (ops[0]->shape[r - 1] != 128 || ops[0]->nb[r - 1] != 1)
+        return fail(EA_ERR_UNSUPPORTED, "ATTENTION needs head dim 128 in one block");
+      for (int64_t v : ops[0]->splits[r - 2])
+        if (v % 128) return fail(EA_ERR_UNSUPPORTED, "ATTENTION needs query block bounds that are multiples of 128");
+      for (int64_t v : ops[1]->splits[r - 2])
+        if (v % 128) return fail(EA_ERR_UNSUPPORTED, "ATTENTION needs key block bounds that are multiples of 128");
+      const int causal = prm ? prm->causal : 0;
+      if (causal && ops[0]->shape[r - 2] != ops[1]->shape[r - 2])
+        return fail(EA_ERR_SPEC, "causal ATTENTION needs as many queries as keys");
+      if (!prm || !(std::isfinite(prm->scale))) return fail(EA_ERR_ARG, "ATTENTION needs params with a finite scale");
+      if (prm->residual) return fail(EA_ERR_UNSUPPORTED, "ATTENTION takes no residual");
+      // A fully masked key block contributes nothing to O: the join drops it.
+      oi->kind = K_ATTENTION;
+      oi->group = out_letters;
+      oi->causal = causal;
+      oi->join_causal = causal;
+      oi->cq = q;
+      oi->ck = k;
+      oi->q_dim = r - 2;
+      oi->k_dim = r - 2;
+      return EA_OK;
+    }
+    default:
+      return fail(EA_ERR_ARG, "unknown join op %d", join_op);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// kind-specific plan sections
+// ---------------------------------------------------------------------------
+struct Extra {
+  size_t desc = 0, work = 0;
+  size_t scratch_bytes = 0;
+  int64_t n_work = 0;
+  // attention scratch layout (offsets inside the scratch area)
+  size_t part_o = 0, part_ml = 0, counters = 0;
+};
+
+int build_generic(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation* const* ops,
+                  const JoinInfo& ji, const ea_relation* res, Image* img, Extra* ex) {
+  GenDesc g;
+  memset(&g, 0, sizeof(g));
+  const int out = sp.n_in;
+  g.n_in = sp.n_in;
+  g.join = join_op;
+  g.agg = agg_op;
+  g.has_res = res != nullptr;
+  g.out_rank = sp.rank[out];
+  g.dt_out = ops[out]->dtype;
+  g.dt_res = res ? res->dtype : 0;
+  for (int d = 0; d < sp.rank[out]; ++d) g.out_letter[d] = ji.index(sp.let[out][d]);
+  for (int i = 0; i < sp.n_in; ++i) {
+    g.in_rank[i] = sp.rank[i];
+    g.dt_in[i] = ops[i]->dtype;
+    for (int d = 0; d < sp.rank[i]; ++d) g.in_letter[i][d] = ji.index(sp.let[i][d]);
+  }
+  for (size_t li = 0; li < ji.letters.size(); ++li) {
+    if (find_dim(sp, out, ji.letters[li]) >= 0) continue;
+    for (int i = 0; i < sp.n_in; ++i) {
+      int d = find_dim(sp, i, ji.letters[li]);
+      if (d >= 0) {
+        g.contr_letter[g.n_contr] = (int32_t)li;
+        g.contr_op[g.n_contr] = i;
+        g.contr_dim[g.n_contr] = d;
+        ++g.n_contr;
+        break;
+      }
+    }
+  }
+  std::vector<GenWork> work;
+  const ea_relation* o = ops[out];
+  for (int64_t b = 0; b < o->nblocks; ++b) {
+    int64_t n = 1;
+    int32_t c[kMaxRank];
+    block_coords(o, b, c);
+    for (int d = 0; d < o->rank; ++d) n *= o->splits[d][c[d] + 1] - o->splits[d][c[d]];
+    if (n > INT32_MAX) return fail(EA_ERR_UNSUPPORTED, "output block too large for the generic kernel");
+    for (int64_t s = 0; s < n; s += 256) work.push_back(GenWork{(int32_t)b, (int32_t)s});
+  }
+  ex->desc = img->put(&g, sizeof(g));
+  ex->work = img->put_vec(work);
+  ex->n_work = (int64_t)work.size();
+  return EA_OK;
+}
+
+// Tiles of every output block, ordered so that the tiles one XCD receives
+// (workgroup ids congruent mod 8) come from one contiguous stretch of the
+// natural order and so share operand blocks in that XCD's L2.
+std::vector<GemmTile> gemm_tiles(const ea_relation* c) {
+  std::vector<GemmTile> nat;
+  int32_t co[kMaxRank];
+  for (int64_t b = 0; b < c->nblocks; ++b) {
+    block_coords(c, b, co);
+    const int64_t me = c->splits[0][co[0] + 1] - c->splits[0][co[0]];
+    const int64_t ne = c->splits[1][co[1] + 1] - c->splits[1][co[1]];
+    for (int64_t m0 = 0; m0 < me; m0 += kGemmTM)
+      for (int64_t n0 = 0; n0 < ne; n0 += kGemmTN) nat.push_back(GemmTile{(int32_t)b, (int32_t)m0, (int32_t)n0});
+  }
+  const size_t n = nat.size();
+  const size_t nx = 8;
+  std::vector<std::vector<GemmTile>> q(nx);
+  for (size_t i = 0; i < n; ++i) q[std::min(nx - 1, i * nx / std::max<size_t>(n, 1))].push_back(nat[i]);
+  std::vector<size_t> head(nx, 0);
+  std::vector<GemmTile> out;
+  out.reserve(n);
+  for (size_t p = 0; out.size() < n; ++p) {
+    size_t x = p % nx;
+    if (head[x] < q[x].size()) {
+      out.push_back(q[x][head[x]++]);
+      continue;
+    }
+    for (size_t y = 0; y < nx; ++y)
+      if (head[y] < q[y].size()) { out.push_back(q[y][head[y]++]); break; }
+  }
+  return out;
+}
+
+int build_rows(const Spec& sp, const ea_relation* const* ops, const OpInfo& oi, Image* img, Extra* ex,
+               int32_t* row_len, int32_t* vec) {
+  // rows of a group: points of the group letters' box; every group has the
+  // same structure as block (g) of the output restricted to the group letters.
+  const ea_relation* y = ops[sp.n_in];
+  const int r = y->rank;
+  std::vector<int32_t> tasks;  // (group, first row, n rows, 0)
+  // groups enumerate block coordinates of the first r-1 dims, row-major
+  int64_t n_groups = 1;
+  for (int d = 0; d < r - 1; ++d) n_groups *= y->nb[d];
+  int32_t c[kMaxRank] = {};
+  const int rows_per_task = 4;
+  for (int64_t g = 0; g < n_groups; ++g) {
+    int64_t rem = g;
+    for (int d = r - 2; d >= 0; --d) { c[d] = (int32_t)(rem % y->nb[d]); rem /= y->nb[d]; }
+    int64_t rows = 1;
+    for (int d = 0; d < r - 1; ++d) rows *= y->splits[d][c[d] + 1] - y->splits[d][c[d]];
+    for (int64_t r0 = 0; r0 < rows; r0 += rows_per_task) {
+      tasks.push_back((int32_t)g);
+      tasks.push_back((int32_t)r0);
+      tasks.push_back((int32_t)std::min<int64_t>(rows_per_task, rows - r0));
+      tasks.push_back(0);
+    }
+  }
+  *row_len = (int32_t)y->shape[r - 1];
+  const ea_relation* x = ops[0];
+  const int es = dtype_size(x->dtype);
+  bool aligned = true;
+  for (int b = 0; b < x->nb[r - 1]; ++b) aligned &= (x->splits[r - 1][b + 1] - x->splits[r - 1][b]) * es % 16 == 0;
+  *vec = rows_vec_ok(y->shape[r - 1], x->nb[r - 1], aligned, es) ? 1 : 0;
+  ex->work = img->put_vec(tasks);
+  ex->n_work = (int64_t)tasks.size() / 4;
+  (void)oi;
+  return EA_OK;
+}
+
+int build_attention(const ea_relation* const* ops, const OpInfo& oi, const JoinInfo& ji, int causal, Image* img,
+                    Extra* ex) {
+  // Work units: per group (b.., q block) and per 128-row query tile, the
+  // group's tuples (key blocks) split into runs of at most `chunk` tuples.
+  // Tuple counts per group are known on the host from the causal rule.
+  const ea_relation* Q = ops[0];
+  const ea_relation* K = ops[1];
+  const int r = Q->rank;
+  (void)ji;
+  int64_t n_groups = Q->nblocks;  // group letters are all of Q's letters; d is one block
+  std::vector<AttnUnit> units;
+  int32_t slot = 0, counter = 0;
+  int32_t c[kMaxRank];
+  const int chunk = 4;  // key blocks per unit (the online-softmax partial)
+  for (int64_t g = 0; g < n_groups; ++g) {
+    block_coords(Q, g, c);
+    const int64_t q_lo = Q->splits[r - 2][c[r - 2]];
+    const int64_t q_hi = Q->splits[r - 2][c[r - 2] + 1];
+    // expected tuples of this group (key blocks the causal rule keeps); used
+    // only to size the split -- the kernel reads its tuple range from the
+    // GPU-built group offsets
+    int n_t = 0;
+    for (int kb = 0; kb < K->nb[r - 2]; ++kb) {
+      const int64_t k_lo = K->splits[r - 2][kb];
+      if (!causal || k_lo <= q_hi - 1) ++n_t;
+    }
+    for (int64_t q0 = 0; q0 < q_hi - q_lo; q0 += 128) {
+      const int parts = (n_t + chunk - 1) / chunk;
+      for (int p = 0; p < parts; ++p) {
+        AttnUnit u;
+        u.group = (int32_t)g;
+        u.q0 = (int32_t)q0;
+        u.part = p;
+        u.n_parts = parts;
+        u.weight = (n_t * (p + 1)) / parts - (n_t * p) / parts;
+        if (parts > 1) {
+          u.slot = slot + p;
+          u.first_slot = slot;
+          u.counter = counter;
+        } else {
+          u.slot = -1;
+          u.first_slot = -1;
+          u.counter = -1;
+        }
+        units.push_back(u);
+      }
+      if (parts > 1) {
+        slot += parts;
+        ++counter;
+      }
+    }
+  }
+  // heaviest units first so that the long runs start early
+  std::stable_sort(units.begin(), units.end(),
+                   [](const AttnUnit& a, const AttnUnit& b) { return a.weight > b.weight; });
+  ex->work = img->put_vec(units);
+  ex->n_work = (int64_t)units.size();
+  ex->part_o = 0;
+  ex->part_ml = (size_t)slot * 128 * 128 * sizeof(float);
+  ex->counters = ex->part_ml + (size_t)slot * 128 * 2 * sizeof(float);
+  ex->scratch_bytes = ex->counters + (size_t)std::max(counter, 1) * sizeof(int32_t);
+  (void)oi;
+  return EA_OK;
+}
+
+// Look up or create the plan of a join-agg call.
+int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int32_t agg_op,
+                     const ea_relation* const* ops, const ea_params* prm, const OpInfo& oi, hipStream_t s,
+                     Plan** out) {
+  int dev = 0;
+  EA_HIP_TRY(hipGetDevice(&dev));
+  std::ostringstream k;
+  k << "J|" << dev << "|" << spec_str << "|" << join_op << "|" << agg_op << "|" << oi.causal << oi.join_causal;
+  for (int o = 0; o <= sp.n_in; ++o) key_rel(k, ops[o]);
+  const ea_relation* res = prm ? prm->residual : nullptr;
+  if (res && (oi.kind == K_GEMM || oi.kind == K_GENERIC)) k << "|res" << res->dtype;
+  const std::string key = k.str();
+  std::lock_guard<std::mutex> lk(g_cache_mu);
+  auto it = cache().find(key);
+  if (it != cache().end()) {
+    *out = it->second.get();
+    return EA_OK;
+  }
+  JoinInfo ji;
+  int e = analyze_join(sp, ops, oi.group, &ji);
+  if (e) return e;
+  Image img;
+  JoinSections js;
+  auto p = std::make_unique<Plan>();
+  p->kind = oi.kind;
+  p->n_in = sp.n_in;
+  p->b_kmajor = oi.b_kmajor;
+  e = build_join(sp, ops, ji, oi.join_causal, oi.cq, oi.ck, &img, &js, &p->n_groups, &p->tuple_cap);
+  if (e) return e;
+  Extra ex;
+  switch (oi.kind) {
+    case K_GENERIC: e = build_generic(sp, join_op, agg_op, ops, ji, res, &img, &ex); break;
+    case K_GEMM: {
+      auto tiles = gemm_tiles(ops[sp.n_in]);
+      ex.work = img.put_vec(tiles);
+      ex.n_work = (int64_t)tiles.size();
+      break;
+    }
+    case K_RMSNORM:
+    case K_SOFTMAX: e = build_rows(sp, ops, oi, &img, &ex, &p->row_len, &p->row_vec); break;
+    case K_ATTENTION: e = build_attention(ops, oi, ji, oi.causal, &img, &ex); break;
+    default: e = fail(EA_ERR_UNSUPPORTED, "internal: unknown plan kind");
+  }
+  if (e) return e;
+  size_t scratch_base = 0;
+  e = plan_upload(p.get(), img, ex.scratch_bytes, &scratch_base, s);
+  if (e) return e;
+  p->d_desc = ex.desc ? p->dmem + ex.desc : nullptr;
+  p->d_work = p->dmem + ex.work;
+  p->n_work = ex.n_work;
+  if (oi.kind == K_ATTENTION) {
+    p->part_o = (float*)(p->dmem + scratch_base + ex.part_o);
+    p->part_ml = (float*)(p->dmem + scratch_base + ex.part_ml);
+    p->counters = (int32_t*)(p->dmem + scratch_base + ex.counters);
+  }
+  e = finish_join(p.get(), js, sp.n_in + 1, s);
+  if (e) return e;
+  *out = p.get();
+  cache()[key] = std::move(p);
+  return EA_OK;
+}
+
+int check_rel(const ea_relation* r, const char* what, bool need_data) {
+  if (!r) return fail(EA_ERR_ARG, "NULL %s relation", what);
+  if (need_data && !r->data) return fail(EA_ERR_ARG, "%s relation has no data", what);
+  return EA_OK;
+}
+
+// Common front half of ea_joinagg / ea_join_tuples: validation + plan.
+int prepare(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, const ea_relation* const* in,
+            const ea_relation* out, const ea_params* prm, bool need_data, hipStream_t s, Spec* sp,
+            OpInfo* oi, Plan** plan) {
+  if (!spec) return fail(EA_ERR_ARG, "NULL spec");
+  if (n_in < 1 || n_in > kMaxIn || !in) return fail(EA_ERR_ARG, "n_in %d outside [1, %d] or NULL inputs", n_in, kMaxIn);
+  for (int i = 0; i < n_in; ++i) {
+    int e = check_rel(in[i], "input", need_data);
+    if (e) return e;
+  }
+  int e = check_rel(out, "output", need_data);
+  if (e) return e;
+  e = parse_spec(spec, sp);
+  if (e) return e;
+  if (sp->n_in != n_in) return fail(EA_ERR_SPEC, "spec '%s' has %d inputs, call passes %d", spec, sp->n_in, n_in);
+  const ea_relation* ops[kMaxOps];
+  for (int i = 0; i < n_in; ++i) ops[i] = in[i];
+  ops[n_in] = out;
+  for (int o = 0; o <= n_in; ++o)
+    if (ops[o]->rank != sp->rank[o])
+      return fail(EA_ERR_SPEC, "operand %d has rank %d but the spec gives it %d letters", o, ops[o]->rank,
+                  sp->rank[o]);
+  e = classify(*sp, join_op, agg_op, ops, prm, oi);
+  if (e) return e;
+  // join validation runs here too, before any HIP call
+  JoinInfo ji;
+  e = analyze_join(*sp, ops, oi->group, &ji);
+  if (e) return e;
+  if (!plan) return EA_OK;
+  return get_joinagg_plan(spec, *sp, join_op, agg_op, ops, prm, *oi, s, plan);
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+int ea_version(void) { return EA_VERSION; }
+
+const char* ea_last_error(void) { return g_err.c_str(); }
+
+int ea_dtype_size(int32_t dtype) {
+  int s = dtype_size(dtype);
+  if (s < 0) return fail(EA_ERR_DTYPE, "unknown dtype %d", dtype);
+  return s;
+}
+
+int ea_layout_nbytes(int32_t rank, const int64_t* shape, int32_t dtype, const int32_t* nblocks,
+                     const int64_t* splits, int64_t* nbytes) {
+  if (!nbytes) return fail(EA_ERR_ARG, "NULL nbytes");
+  if (dtype_size(dtype) < 0) return fail(EA_ERR_DTYPE, "unknown dtype %d", dtype);
+  int e = check_partition(rank, shape, nblocks, splits);
+  if (e) return e;
+  ea_relation r;
+  r.rank = rank;
+  r.dtype = dtype;
+  const int64_t* s = splits;
+  for (int d = 0; d < rank; ++d) {
+    r.nb[d] = nblocks[d];
+    r.splits[d].assign(s, s + nblocks[d] + 1);
+    s += nblocks[d] + 1;
+  }
+  fill_layout(&r);
+  *nbytes = r.nbytes;
+  return ok();
+}
+
+int ea_relation_create(int32_t rank, const int64_t* shape, int32_t dtype, const int32_t* nblocks,
+                       const int64_t* splits, void* data, int64_t capacity, ea_relation** out) {
+  if (!out) return fail(EA_ERR_ARG, "NULL out handle");
+  *out = nullptr;
+  if (dtype_size(dtype) < 0) return fail(EA_ERR_DTYPE, "unknown dtype %d", dtype);
+  int e = check_partition(rank, shape, nblocks, splits);
+  if (e) return e;
+  auto r = std::make_unique<ea_relation>();
+  r->rank = rank;
+  r->dtype = dtype;
+  const int64_t* s = splits;
+  for (int d = 0; d < rank; ++d) {
+    r->shape[d] = shape[d];
+    r->nb[d] = nblocks[d];
+    r->splits[d].assign(s, s + nblocks[d] + 1);
+    s += nblocks[d] + 1;
+  }
+  fill_layout(r.get());
+  if (data) {
+    if ((uintptr_t)data % 256) return fail(EA_ERR_ARG, "relation data must be 256-byte aligned");
+    if (capacity < r->nbytes)
+      return fail(EA_ERR_CAPACITY, "capacity %lld below the layout's %lld bytes", (long long)capacity,
+                  (long long)r->nbytes);
+  }
+  r->data = data;
+  r->capacity = capacity;
+  *out = r.release();
+  return ok();
+}
+
+int ea_relation_destroy(ea_relation* rel) {
+  delete rel;
+  return ok();
+}
+
+int ea_relation_set_data(ea_relation* rel, void* data, int64_t capacity) {
+  if (!rel) return fail(EA_ERR_ARG, "NULL relation");
+  if (data && (uintptr_t)data % 256) return fail(EA_ERR_ARG, "relation data must be 256-byte aligned");
+  if (data && capacity < rel->nbytes)
+    return fail(EA_ERR_CAPACITY, "capacity %lld below the layout's %lld bytes", (long long)capacity,
+                (long long)rel->nbytes);
+  rel->data = data;
+  rel->capacity = capacity;
+  return ok();
+}
+
+int ea_relation_num_blocks(const ea_relation* rel, int64_t* n) {
+  if (!rel || !n) return fail(EA_ERR_ARG, "NULL argument");
+  *n = rel->nblocks;
+  return ok();
+}
+
+int ea_relation_nbytes(const ea_relation* rel, int64_t* nbytes) {
+  if (!rel || !nbytes) return fail(EA_ERR_ARG, "NULL argument");
+  *nbytes = rel->nbytes;
+  return ok();
+}
+
+int ea_relation_block(const ea_relation* rel, int64_t b, int64_t* lo, int64_t* hi, int64_t* byte_off) {
+  if (!rel) return fail(EA_ERR_ARG, "NULL relation");
+  if (b < 0 || b >= rel->nblocks) return fail(EA_ERR_ARG, "block %lld outside [0, %lld)", (long long)b,
+                                              (long long)rel->nblocks);
+  int32_t c[kMaxRank];
+  block_coords(rel, b, c);
+  for (int d = 0; d < rel->rank; ++d) {
+    if (lo) lo[d] = rel->splits[d][c[d]];
+    if (hi) hi[d] = rel->splits[d][c[d] + 1];
+  }
+  if (byte_off) *byte_off = rel->off[(size_t)b];
+  return ok();
+}
+
+int ea_overlay(int32_t rank, const int32_t* nblocks_a, const int64_t* splits_a, const int32_t* nblocks_b,
+               const int64_t* splits_b, int32_t* nblocks_out, int64_t* splits_out) {
+  if (rank < 1 || rank > kMaxRank || !nblocks_a || !splits_a || !nblocks_b || !splits_b || !nblocks_out ||
+      !splits_out)
+    return fail(EA_ERR_ARG, "bad overlay arguments");
+  const int64_t* sa = splits_a;
+  const int64_t* sb = splits_b;
+  int64_t* so = splits_out;
+  for (int d = 0; d < rank; ++d) {
+    if (nblocks_a[d] < 1 || nblocks_b[d] < 1) return fail(EA_ERR_PARTITION, "dim %d has no blocks", d);
+    if (sa[nblocks_a[d]] != sb[nblocks_b[d]]) return fail(EA_ERR_ARG, "dim %d: extents differ", d);
+    std::vector<int64_t> u(sa, sa + nblocks_a[d] + 1);
+    u.insert(u.end(), sb, sb + nblocks_b[d] + 1);
+    std::sort(u.begin(), u.end());
+    u.erase(std::unique(u.begin(), u.end()), u.end());
+    nblocks_out[d] = (int32_t)u.size() - 1;
+    std::copy(u.begin(), u.end(), so);
+    so += u.size();
+    sa += nblocks_a[d] + 1;
+    sb += nblocks_b[d] + 1;
+  }
+  return ok();
+}
+
+int ea_join_tuples(const char* spec, int32_t join_op, int32_t n_in, const ea_relation* const* in,
+                   const ea_relation* out, const ea_params* params, int32_t* tuples, int64_t cap,
+                   int64_t* group_off, int64_t gcap, int64_t* n_tuples, int64_t* n_groups, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  int32_t agg = EA_AGG_SUM;
+  if (join_op == EA_OP_SOFTMAX || join_op == EA_OP_ATTENTION) agg = EA_AGG_LSE;
+  if ((join_op == EA_JOIN_MUL || join_op == EA_JOIN_ADD) && spec) {
+    // NONE when nothing is contracted, so that pure joins can be inspected too
+    Spec sp;
+    if (parse_spec(spec, &sp) == EA_OK) {
+      bool contracted = false;
+      for (int i = 0; i < sp.n_in; ++i)
+        for (int d = 0; d < sp.rank[i]; ++d) contracted |= find_dim(sp, sp.n_in, sp.let[i][d]) < 0;
+      if (!contracted) agg = EA_AGG_NONE;
+    }
+  }
+  Spec sp;
+  OpInfo oi;
+  Plan* plan = nullptr;
+  int e = prepare(spec, join_op, agg, n_in, in, out, params, false, s, &sp, &oi, &plan);
+  if (e) return e;
+  int32_t count = 0;
+  EA_HIP_TRY(hipMemcpyAsync(&count, plan->d_count, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  EA_HIP_TRY(hipStreamSynchronize(s));
+  if (n_tuples) *n_tuples = count;
+  if (n_groups) *n_groups = plan->n_groups;
+  if (!tuples || !group_off) return fail(EA_ERR_ARG, "NULL tuple or group buffer");
+  if (cap < count || gcap < plan->n_groups + 1)
+    return fail(EA_ERR_CAPACITY, "need %d tuples and %lld group offsets", count, (long long)plan->n_groups + 1);
+  const int stride = plan->n_in + 1;
+  EA_HIP_TRY(hipMemcpyAsync(tuples, plan->d_tuples, (size_t)count * stride * sizeof(int32_t),
+                            hipMemcpyDeviceToDevice, s));
+  // widen the int32 offsets to int64 through the host (test path only)
+  std::vector<int32_t> g32((size_t)plan->n_groups + 1);
+  EA_HIP_TRY(hipMemcpyAsync(g32.data(), plan->d_goff, g32.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  EA_HIP_TRY(hipStreamSynchronize(s));
+  std::vector<int64_t> g64(g32.begin(), g32.end());
+  EA_HIP_TRY(hipMemcpyAsync(group_off, g64.data(), g64.size() * sizeof(int64_t), hipMemcpyHostToDevice, s));
+  EA_HIP_TRY(hipStreamSynchronize(s));
+  return ok();
+}
+
+int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, const ea_relation* const* in,
+               ea_relation* out, const ea_params* params, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  Spec sp;
+  OpInfo oi;
+  Plan* plan = nullptr;
+  int e = prepare(spec, join_op, agg_op, n_in, in, out, params, true, s, &sp, &oi, &plan);
+  if (e) return e;
+  const ea_relation* res = params ? params->residual : nullptr;
+  switch (plan->kind) {
+    case K_GENERIC: {
+      GenArgs a;
+      memset(&a, 0, sizeof(a));
+      a.desc = (const GenDesc*)plan->d_desc;
+      a.tuples = plan->d_tuples;
+      a.goff = plan->d_goff;
+      for (int o = 0; o <= n_in; ++o) a.blk[o] = plan->d_blk[o];
+      for (int i = 0; i < n_in; ++i) a.in[i] = (const char*)in[i]->data;
+      a.out = (char*)out->data;
+      a.res = res ? (const char*)res->data : nullptr;
+      a.work = (const GenWork*)plan->d_work;
+      a.n_work = plan->n_work;
+      EA_HIP_TRY(launch_generic(a, s));
+      break;
+    }
+    case K_GEMM: {
+      GemmArgs a;
+      memset(&a, 0, sizeof(a));
+      a.tuples = plan->d_tuples;
+      a.goff = plan->d_goff;
+      a.blk_a = plan->d_blk[0];
+      a.blk_b = plan->d_blk[1];
+      a.a = (const char*)in[0]->data;
+      a.b = (const char*)in[1]->data;
+      a.swiglu = join_op == EA_OP_SWIGLU;
+      if (a.swiglu) {
+        a.blk_b2 = plan->d_blk[2];
+        a.b2 = (const char*)in[2]->data;
+      }
+      a.blk_c = plan->d_blk[n_in];
+      a.c = (char*)out->data;
+      a.res = res ? (const char*)res->data : nullptr;
+      a.dt_res = res ? res->dtype : 0;
+      a.tiles = (const GemmTile*)plan->d_work;
+      a.n_tiles = (int32_t)plan->n_work;
+      a.tuple_stride = n_in + 1;
+      a.b_kmajor = plan->b_kmajor;
+      a.dt_in = in[0]->dtype;
+      a.dt_out = out->dtype;
+      EA_HIP_TRY(launch_gemm(a, s));
+      break;
+    }
+    case K_RMSNORM:
+    case K_SOFTMAX: {
+      RowArgs a;
+      memset(&a, 0, sizeof(a));
+      a.tuples = plan->d_tuples;
+      a.goff = plan->d_goff;
+      a.blk_x = plan->d_blk[0];
+      a.x = (const char*)in[0]->data;
+      a.dt_x = in[0]->dtype;
+      if (plan->kind == K_RMSNORM) {
+        a.blk_w = plan->d_blk[1];
+        a.w = (const char*)in[1]->data;
+        a.dt_w = in[1]->dtype;
+        a.eps = params->eps;
+      }
+      a.blk_y = plan->d_blk[n_in];
+      a.y = (char*)out->data;
+      a.dt_y = out->dtype;
+      a.rows = (const int32_t*)plan->d_work;
+      a.n_rowtasks = (int32_t)plan->n_work;
+      a.tuple_stride = n_in + 1;
+      a.rank = out->rank;
+      a.causal = oi.causal;
+      a.row_len = plan->row_len;
+      a.vec = plan->row_vec;
+      EA_HIP_TRY(plan->kind == K_RMSNORM ? launch_rmsnorm(a, s) : launch_softmax(a, s));
+      break;
+    }
+    case K_ATTENTION: {
+      AttnArgs a;
+      memset(&a, 0, sizeof(a));
+      a.tuples = plan->d_tuples;
+      a.goff = plan->d_goff;
+      a.blk_q = plan->d_blk[0];
+      a.blk_k = plan->d_blk[1];
+      a.blk_v = plan->d_blk[2];
+      a.blk_o = plan->d_blk[3];
+      a.q = (const char*)in[0]->data;
+      a.k = (const char*)in[1]->data;
+      a.v = (const char*)in[2]->data;
+      a.o = (char*)out->data;
+      a.units = (const AttnUnit*)plan->d_work;
+      a.n_units = (int32_t)plan->n_work;
+      a.causal = oi.causal;
+      a.q_dim = oi.q_dim;
+      a.k_dim = oi.k_dim;
+      a.scale = params->scale;
+      a.part_o = plan->part_o;
+      a.part_ml = plan->part_ml;
+      a.counters = plan->counters;
+      a.dt_o = out->dtype;
+      EA_HIP_TRY(launch_attention(a, s));
+      break;
+    }
+    default:
+      return fail(EA_ERR_UNSUPPORTED, "internal: plan kind %d", (int)plan->kind);
+  }
+  return ok();
+}
+
+int ea_repartition(const ea_relation* src, ea_relation* dst, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  if (!src || !dst) return fail(EA_ERR_ARG, "NULL relation");
+  if (!src->data || !dst->data) return fail(EA_ERR_ARG, "relation has no data");
+  if (src->rank != dst->rank || src->dtype != dst->dtype)
+    return fail(EA_ERR_ARG, "source and destination differ in rank or dtype");
+  for (int d = 0; d < src->rank; ++d)
+    if (src->shape[d] != dst->shape[d]) return fail(EA_ERR_ARG, "source and destination differ in shape");
+  {
+    const char* a0 = (const char*)src->data;
+    const char* b0 = (const char*)dst->data;
+    if (a0 < b0 + dst->nbytes && b0 < a0 + src->nbytes)
+      return fail(EA_ERR_ARG, "source and destination memory overlap");
+  }
+  int dev = 0;
+  EA_HIP_TRY(hipGetDevice(&dev));
+  std::ostringstream k;
+  k << "R|" << dev;
+  key_rel(k, src);
+  key_rel(k, dst);
+  const std::string key = k.str();
+  Plan* plan = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_cache_mu);
+    auto it = cache().find(key);
+    if (it != cache().end()) plan = it->second.get();
+    if (!plan) {
+      // Overlay (Section 5.3): cut every dim at the union of both partitions'
+      // split points.  A box = the intersection of one source block and one
+      // destination block = a union of overlay atoms; it is copied row by row.
+      const int R = src->rank;
+      const int es = dtype_size(src->dtype);
+      std::vector<RepTask> tasks;
+      int32_t cd[kMaxRank];
+      std::vector<DevBlk> sb = dev_blocks(src);
+      for (int64_t b = 0; b < dst->nblocks; ++b) {
+        block_coords(dst, b, cd);
+        // source blocks overlapping destination block b: per dim, the source
+        // intervals that meet [dlo, dhi)
+        std::vector<int32_t> lo_i(R), hi_i(R);
+        for (int d = 0; d < R; ++d) {
+          const int64_t dlo = dst->splits[d][cd[d]], dhi = dst->splits[d][cd[d] + 1];
+          const auto& ss = src->splits[d];
+          int first = (int)(std::upper_bound(ss.begin(), ss.end(), dlo) - ss.begin()) - 1;
+          int last = (int)(std::lower_bound(ss.begin(), ss.end(), dhi) - ss.begin()) - 1;
+          lo_i[d] = first;
+          hi_i[d] = last + 1;
+        }
+        std::vector<int32_t> cs(lo_i);
+        while (true) {
+          int64_t sbi = 0;
+          for (int d = 0; d < R; ++d) sbi = sbi * src->nb[d] + cs[d];
+          const DevBlk& S = sb[(size_t)sbi];
+          int64_t blo[kMaxRank], bext[kMaxRank];
+          for (int d = 0; d < R; ++d) {
+            const int64_t dlo = dst->splits[d][cd[d]], dhi = dst->splits[d][cd[d] + 1];
+            const int64_t slo = S.lo[d], shi = S.lo[d] + S.ext[d];
+            blo[d] = std::max(dlo, slo);
+            bext[d] = std::min(dhi, shi) - blo[d];
+          }
+          // row-major strides (elements) inside each block
+          int64_t sst[kMaxRank], dst_st[kMaxRank];
+          sst[R - 1] = dst_st[R - 1] = 1;
+          for (int d = R - 2; d >= 0; --d) {
+            sst[d] = sst[d + 1] * S.ext[d + 1];
+            dst_st[d] = dst_st[d + 1] * (dst->splits[d + 1][cd[d + 1] + 1] - dst->splits[d + 1][cd[d + 1]]);
+          }
+          RepTask t;
+          memset(&t, 0, sizeof(t));
+          int64_t so = 0, dofs = 0;
+          for (int d = 0; d < R; ++d) {
+            so += (blo[d] - S.lo[d]) * sst[d];
+            dofs += (blo[d] - dst->splits[d][cd[d]]) * dst_st[d];
+          }
+          t.src_off = S.off + so * es;
+          t.dst_off = dst->off[(size_t)b] + dofs * es;
+          // merge trailing dims that are contiguous in both blocks into the row
+          int last = R - 1;
+          int64_t row_elems = bext[R - 1];
+          while (last > 0 && bext[last] == S.ext[last] &&
+                 bext[last] == dst->splits[last][cd[last] + 1] - dst->splits[last][cd[last]]) {
+            row_elems *= bext[last - 1];
+            --last;
+          }
+          t.n_outer = last;
+          int64_t rows = 1;
+          for (int d = 0; d < last; ++d) {
+            t.outer_ext[d] = (int32_t)bext[d];
+            t.src_stride[d] = sst[d] * es;
+            t.dst_stride[d] = dst_st[d] * es;
+            rows *= bext[d];
+          }
+          const int64_t rb = row_elems * es;
+          if (rb > INT32_MAX || rows > INT32_MAX) return fail(EA_ERR_UNSUPPORTED, "repartition box too large");
+          if (rows * rb > INT32_MAX) return fail(EA_ERR_UNSUPPORTED, "repartition box too large");
+          t.row_bytes = (int32_t)rb;
+          int vec = 16;
+          auto fits = [&](int64_t v) { return v % vec == 0; };
+          while (vec > 1) {
+            bool good = fits(t.row_bytes) && fits(t.src_off) && fits(t.dst_off);
+            for (int d = 0; d < last; ++d) good = good && fits(t.src_stride[d]) && fits(t.dst_stride[d]);
+            if (good) break;
+            vec /= 2;
+          }
+          t.vec = vec;
+          // 16 KiB of the box per workgroup task (one pass of 256 lanes x 4 x 16 B)
+          const int64_t total = rows * rb, per = 16384;
+          for (int64_t b0 = 0; b0 < total; b0 += per) {
+            RepTask u = t;
+            u.begin = (int32_t)b0;
+            u.end = (int32_t)std::min(total, b0 + per);
+            tasks.push_back(u);
+          }
+          int d = R - 1;
+          while (d >= 0) {
+            if (++cs[d] < hi_i[d]) break;
+            cs[d] = lo_i[d];
+            --d;
+          }
+          if (d < 0) break;
+        }
+      }
+      Image img;
+      const size_t toff = img.put_vec(tasks);
+      auto p = std::make_unique<Plan>();
+      p->kind = K_REPART;
+      int e = plan_upload(p.get(), img, 0, nullptr, s);
+      if (e) return e;
+      EA_HIP_TRY(hipStreamSynchronize(s));
+      p->d_work = p->dmem + toff;
+      p->n_work = (int64_t)tasks.size();
+      plan = p.get();
+      cache()[key] = std::move(p);
+    }
+  }
+  EA_HIP_TRY(launch_repartition((const RepTask*)plan->d_work, plan->n_work, (const char*)src->data,
+                                (char*)dst->data, s));
+  return ok();
+}
+
+int64_t ea_plan_cache_size(void) {
+  std::lock_guard<std::mutex> lk(g_cache_mu);
+  return (int64_t)cache().size();
+}
+
+int ea_plan_cache_clear(void) {
+  std::lock_guard<std::mutex> lk(g_cache_mu);
+  cache().clear();
+  return ok();
+}
+
+}  // extern "C"

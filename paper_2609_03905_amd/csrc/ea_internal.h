@@ -1,0 +1,219 @@
+// ea_internal.h -- structures shared by libea's host code and its HIP kernels.
+//
+// A plan is one library-owned device buffer holding everything a join-agg or
+// repartition needs besides the relations' data: the enumerator description,
+// the split points, per-operand block tables, the GPU-built tuple table with
+// its CSR group offsets, the kernel's work list and any scratch space.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "ea.h"
+
+namespace ea {
+
+constexpr int kMaxRank = EA_MAX_RANK;
+constexpr int kMaxIn = EA_MAX_INPUTS;
+constexpr int kMaxOps = EA_MAX_INPUTS + 1;  // inputs, then the output
+constexpr int kMaxLetters = 16;
+
+// One block of a relation: byte offset from the relation base, and its
+// sub-tensor type as (lo, extent) per dim.
+struct DevBlk {
+  int64_t off;
+  int32_t lo[kMaxRank];
+  int32_t ext[kMaxRank];
+};
+
+// ---------------------------------------------------------------------------
+// Join enumerator.  Candidates are the points of the letter-block space,
+// ordered group letters first (row-major), then the remaining letters in
+// order of first appearance; the last letter varies fastest.  A candidate
+// becomes a tuple when, for every operand, a block with exactly the
+// candidate's intervals on that operand's letters is found (integer key
+// matching by binary search on the operand's split points) and the optional
+// causal predicate holds.
+// ---------------------------------------------------------------------------
+struct EnumDesc {
+  int32_t n_in;
+  int32_t n_letters;
+  int32_t n_group_letters;
+  int32_t causal;
+  int32_t cq, ck;           // letter indices of the causal pair
+  int64_t per_group;        // candidates per group
+  int64_t n_groups;
+  int64_t n_cand;
+  int32_t letter_nb[kMaxLetters];
+  int32_t letter_split[kMaxLetters];  // offset of the letter's driving split list
+  int32_t op_rank[kMaxOps];
+  int32_t op_letter[kMaxOps][kMaxRank];
+  int32_t op_nb[kMaxOps][kMaxRank];
+  int32_t op_split[kMaxOps][kMaxRank];  // offset of the operand's own split list
+};
+
+hipError_t launch_enumerate(const EnumDesc* d_desc, const int32_t* d_splits, int32_t* d_tuples,
+                            int32_t* d_goff, int32_t* d_count, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Generic einsum join-agg: one thread per output element, the group's tuples
+// and their contracted index ranges walked in canonical order.
+// ---------------------------------------------------------------------------
+struct GenDesc {
+  int32_t n_in, join, agg, has_res;
+  int32_t out_rank, dt_out, dt_res, n_contr;
+  int32_t out_letter[kMaxRank];
+  int32_t in_rank[kMaxIn];
+  int32_t dt_in[kMaxIn];
+  int32_t in_letter[kMaxIn][kMaxRank];
+  int32_t contr_letter[kMaxLetters];
+  int32_t contr_op[kMaxLetters];   // input whose block gives the letter's interval
+  int32_t contr_dim[kMaxLetters];
+};
+
+struct GenWork {  // one workgroup: up to 256 consecutive elements of one output block
+  int32_t block;
+  int32_t start;
+};
+
+struct GenArgs {
+  const GenDesc* desc;
+  const int32_t* tuples;
+  const int32_t* goff;
+  const DevBlk* blk[kMaxOps];  // inputs, then output
+  const char* in[kMaxIn];
+  char* out;
+  const char* res;
+  const GenWork* work;
+  int64_t n_work;
+};
+
+hipError_t launch_generic(const GenArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Repartition: the overlay of the source and destination partitions cuts the
+// tensor into boxes, each inside exactly one source block and one destination
+// block; a task copies a range of a box's rows (rows run along the last dim).
+// ---------------------------------------------------------------------------
+struct RepTask {
+  int64_t src_off, dst_off;         // bytes from the bases to the box origin
+  int64_t src_stride[kMaxRank - 1]; // bytes per step of each outer dim
+  int64_t dst_stride[kMaxRank - 1];
+  int32_t outer_ext[kMaxRank - 1];  // extents of the outer dims
+  int32_t n_outer;
+  int32_t row_bytes;
+  int32_t vec;                      // bytes per vector access: 16, 8, 4, 2 or 1
+  int32_t begin, end;               // byte range of the box (rows x row_bytes) copied
+};
+
+hipError_t launch_repartition(const RepTask* d_tasks, int64_t n_tasks, const char* src, char* dst,
+                              hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Block GEMM on the matrix cores: out = sum over the group's tuples of
+// A_blk * B_blk (+ residual), bf16/f16 inputs, fp32 accumulation.
+// ---------------------------------------------------------------------------
+constexpr int kGemmTM = 128, kGemmTN = 128;  // output tile of one workgroup
+
+struct GemmTile {  // one workgroup: a tile of one output block
+  int32_t block;   // output block == group index
+  int32_t m0, n0;
+};
+
+struct GemmArgs {
+  const int32_t* tuples;
+  const int32_t* goff;
+  const DevBlk* blk_a;
+  const DevBlk* blk_b;
+  const DevBlk* blk_b2;  // second right operand (SwiGLU), else null
+  const DevBlk* blk_c;
+  const char* a;
+  const char* b;
+  const char* b2;
+  char* c;
+  const char* res;       // residual relation data (same layout as c) or null
+  const GemmTile* tiles;
+  int32_t n_tiles;
+  int32_t tuple_stride;  // 1 + n_in
+  int32_t b_kmajor;      // 1: B blocks are [n][k] ("ab,cb->ac"); 0: [k][n]
+  int32_t dt_in;         // EA_BF16 or EA_F16
+  int32_t dt_out;        // EA_F32, EA_BF16 or EA_F16
+  int32_t dt_res;
+  int32_t swiglu;        // 1: out = silu(A B) * (A B2)
+};
+
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Row reductions.  A row is the concatenation of its segments, one per tuple
+// of its group (RMSNorm: column blocks of x with the matching w blocks;
+// softmax: key blocks).
+// ---------------------------------------------------------------------------
+struct RowArgs {
+  const int32_t* tuples;
+  const int32_t* goff;
+  const DevBlk* blk_x;
+  const DevBlk* blk_w;   // RMSNorm weight blocks, or null
+  const DevBlk* blk_y;
+  const char* x;
+  const char* w;
+  char* y;
+  const int32_t* rows;   // per workgroup row range: (group, first row, n rows, -)
+  int32_t n_rowtasks;
+  int32_t tuple_stride;
+  int32_t rank;          // rank of x / y
+  int32_t dt_x, dt_w, dt_y;
+  int32_t causal;        // softmax: mask keys beyond the row's query position
+  int32_t row_len;       // full extent of the normalised letter
+  int32_t vec;           // 1: register path (see rows_vec_ok)
+  float eps;
+};
+
+bool rows_vec_ok(int64_t row_len, int64_t max_segments, bool seg_aligned, int es);
+
+hipError_t launch_rmsnorm(const RowArgs& a, hipStream_t s);
+hipError_t launch_softmax(const RowArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Causal attention with key-split online-softmax aggregation.
+// A unit is (group, query tile of 128 rows, a run of the group's tuples).
+// Units of one (group, tile) that split its tuples write partial (m, l, O)
+// to scratch; the last unit to finish merges them in tuple order.
+// ---------------------------------------------------------------------------
+struct AttnUnit {
+  int32_t group;
+  int32_t q0;          // first query row inside the q block
+  int32_t part;        // this unit takes tuples [part*n/n_parts, (part+1)*n/n_parts)
+  int32_t n_parts;     //   of its group's n tuples
+  int32_t slot;        // partial slot of this unit, -1 when the unit is alone
+  int32_t first_slot;  // first slot of the (group, tile), for the merge
+  int32_t counter;     // arrival counter index of the (group, tile)
+  int32_t weight;      // expected tuple count (host-side ordering only)
+};
+
+struct AttnArgs {
+  const int32_t* tuples;
+  const int32_t* goff;
+  const DevBlk* blk_q;
+  const DevBlk* blk_k;
+  const DevBlk* blk_v;
+  const DevBlk* blk_o;
+  const char* q;
+  const char* k;
+  const char* v;
+  char* o;
+  const AttnUnit* units;
+  int32_t n_units;
+  int32_t causal;
+  int32_t q_dim, k_dim;  // dim index of q (in Q/O) and k (in K/V)
+  float scale;
+  float* part_o;         // [slots][128 rows][128] fp32
+  float* part_ml;        // [slots][128 rows][2]
+  int32_t* counters;     // one per split (group, tile); zero between calls
+  int32_t dt_o;
+};
+
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+
+}  // namespace ea

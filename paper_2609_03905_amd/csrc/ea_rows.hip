@@ -1,0 +1,297 @@
+// ea_rows.hip -- row-reduction join-aggs: RMSNorm and softmax.
+//
+// The normalised letter (the last one) is split into blocks, so a row is the
+// concatenation of one segment per tuple of its group (Section 3.2,
+// Definition "Implementation": the per-tuple partials -- a sum of squares, or
+// a max and a sum of exponentials -- are aggregated across the group's
+// blocks).  One wavefront owns one row: it loads every segment of the row
+// into registers (16-byte vector loads, lanes interleaved across the row),
+// forms its local partials, aggregates them across lanes (the aggregation
+// across blocks, in a fixed order), and writes the normalised row from the
+// registers.  HBM traffic: one read of the visible inputs, one write.
+//
+// Causal softmax skips the loads of keys after the row's query position and
+// stores zeros there.  Rows too long for registers, or segments that are not
+// 16-byte multiples, take a scalar path that re-reads the row.
+#include "ea_device.h"
+
+namespace ea {
+
+namespace {
+
+constexpr int kThreads = 256;  // 4 rows per workgroup, one per wavefront
+constexpr int kMaxSeg = 64;    // segments per row on the register path
+constexpr int kMaxK = 16;      // 16-byte chunks per lane on the register path
+
+struct SegTable {
+  int32_t start[kMaxSeg];  // first chunk of the segment within the row
+  int64_t xoff[kMaxSeg];   // byte offset of the row's segment in x
+  int64_t yoff[kMaxSeg];   // element index base in y's block (by offset)
+  int64_t woff[kMaxSeg];   // byte offset of the w block (RMSNorm)
+  int32_t klo[kMaxSeg];    // position of the segment's first element
+  int32_t len[kMaxSeg];    // elements in the segment
+};
+
+struct RowInfo {
+  int32_t t0, nseg;
+  int32_t row;     // row index inside the group's blocks
+  int32_t qpos;    // query position of the row (softmax causal)
+};
+
+__device__ __forceinline__ RowInfo row_info(const RowArgs& a, int task_row) {
+  const int32_t* task = a.rows + 4 * blockIdx.x;
+  RowInfo ri;
+  const int g = task[0];
+  ri.row = task[1] + task_row;
+  ri.t0 = a.goff[g];
+  ri.nseg = a.goff[g + 1] - ri.t0;
+  ri.qpos = 0;
+  if (a.causal && ri.nseg > 0) {
+    const DevBlk& xb = a.blk_x[a.tuples[(int64_t)ri.t0 * a.tuple_stride + 1]];
+    const int qd = a.rank - 2;
+    ri.qpos = xb.lo[qd] + ri.row % xb.ext[qd];
+  }
+  return ri;
+}
+
+// Fill the wave's segment table (lane s describes segment s).  Returns the
+// row's total chunk count.
+__device__ __forceinline__ int fill_segments(const RowArgs& a, const RowInfo& ri, SegTable& st, int lane,
+                                             int es) {
+  const int d_last = a.rank - 1;
+  int chunks = 0;
+  if (lane < ri.nseg) {
+    const int32_t* tp = a.tuples + (int64_t)(ri.t0 + lane) * a.tuple_stride;
+    const DevBlk& xb = a.blk_x[tp[1]];
+    const DevBlk& yb = a.blk_y[tp[0]];
+    const int L = xb.ext[d_last];
+    chunks = L * es / 16;
+    st.xoff[lane] = xb.off + (int64_t)ri.row * L * es;
+    st.yoff[lane] = yb.off;
+    st.woff[lane] = a.blk_w ? a.blk_w[tp[2]].off : 0;
+    st.klo[lane] = xb.lo[d_last];
+    st.len[lane] = L;
+  }
+  // exclusive prefix sum of chunk counts across lanes
+  int incl = chunks;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += v;
+  }
+  if (lane < ri.nseg) st.start[lane] = incl - chunks;
+  return __shfl(incl, 63, 64);
+}
+
+__device__ __forceinline__ int seg_of(const SegTable& st, int nseg, int chunk) {
+  int s = 0;
+  for (int j = 1; j < nseg; ++j) s = chunk >= st.start[j] ? j : s;
+  return s;
+}
+
+template <typename T>
+__device__ __forceinline__ void unpack(const uint4& v, float (&f)[8]);
+
+template <>
+__device__ __forceinline__ void unpack<uint16_t>(const uint4& v, float (&f)[8]) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+
+template <>
+__device__ __forceinline__ void unpack<float>(const uint4& v, float (&f)[8]) {
+  f[0] = __uint_as_float(v.x);
+  f[1] = __uint_as_float(v.y);
+  f[2] = __uint_as_float(v.z);
+  f[3] = __uint_as_float(v.w);
+}
+
+// ---------------------------------------------------------------------------
+// register path; XT: uint16_t for bf16 rows, float for f32 rows
+// ---------------------------------------------------------------------------
+template <typename XT, bool SOFTMAX>
+__global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
+  __shared__ SegTable tabs[kThreads / 64];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int32_t* task = a.rows + 4 * blockIdx.x;
+  if (wid >= task[2]) return;  // whole wavefront leaves together
+  SegTable& st = tabs[wid];
+  const RowInfo ri = row_info(a, wid);
+  constexpr int ES = sizeof(XT), EPC = 16 / ES;
+  const int total = fill_segments(a, ri, st, lane, ES);
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+  uint4 v[kMaxK];
+  int seg[kMaxK];
+  bool vis[kMaxK];
+  float part = SOFTMAX ? -INFINITY : 0.0f;
+#pragma unroll
+  for (int k = 0; k < kMaxK; ++k) {
+    const int c = k * 64 + lane;
+    vis[k] = false;
+    seg[k] = 0;
+    v[k] = make_uint4(0, 0, 0, 0);
+    if (c < total) {
+      const int s = seg_of(st, ri.nseg, c);
+      seg[k] = s;
+      const int e0 = (c - st.start[s]) * EPC;  // element index inside the segment
+      vis[k] = !(SOFTMAX && a.causal) || st.klo[s] + e0 <= ri.qpos;
+      if (vis[k]) v[k] = *reinterpret_cast<const uint4*>(a.x + st.xoff[s] + (int64_t)e0 * ES);
+    }
+  }
+  // local partials, then the aggregation across lanes
+#pragma unroll
+  for (int k = 0; k < kMaxK; ++k) {
+    if (!vis[k]) continue;
+    float f[8];
+    unpack<XT>(v[k], f);
+    const int s = seg[k];
+    const int e0 = (k * 64 + lane - st.start[s]) * EPC;
+#pragma unroll
+    for (int i = 0; i < EPC; ++i) {
+      if constexpr (SOFTMAX) {
+        const bool ok = !a.causal || st.klo[s] + e0 + i <= ri.qpos;
+        part = ok ? fmaxf(part, f[i]) : part;
+      } else {
+        part += f[i] * f[i];
+      }
+    }
+  }
+  float scale = 0.0f, m = 0.0f;
+  if constexpr (SOFTMAX) {
+    m = wave_max(part);
+    float l = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kMaxK; ++k) {
+      if (!vis[k]) continue;
+      float f[8];
+      unpack<XT>(v[k], f);
+      const int s = seg[k];
+      const int e0 = (k * 64 + lane - st.start[s]) * EPC;
+#pragma unroll
+      for (int i = 0; i < EPC; ++i) {
+        const bool ok = !a.causal || st.klo[s] + e0 + i <= ri.qpos;
+        l += ok ? __expf(f[i] - m) : 0.0f;
+      }
+    }
+    l = wave_sum(l);
+    scale = m == -INFINITY ? 0.0f : 1.0f / l;
+  } else {
+    const float ss = wave_sum(part);
+    scale = 1.0f / sqrtf(ss / (float)a.row_len + a.eps);
+  }
+  // write the row
+#pragma unroll
+  for (int k = 0; k < kMaxK; ++k) {
+    const int c = k * 64 + lane;
+    if (c >= total) continue;
+    const int s = seg[k];
+    const int e0 = (c - st.start[s]) * EPC;
+    float f[8];
+    unpack<XT>(v[k], f);
+    float o[8];
+#pragma unroll
+    for (int i = 0; i < EPC; ++i) {
+      if constexpr (SOFTMAX) {
+        const bool ok = vis[k] && (!a.causal || st.klo[s] + e0 + i <= ri.qpos);
+        o[i] = ok ? __expf(f[i] - m) * scale : 0.0f;
+      } else {
+        const float w = ld_elem(a.w + st.woff[s], e0 + i, a.dt_w);
+        o[i] = w * (f[i] * scale);
+      }
+    }
+    const int64_t yidx = (int64_t)ri.row * st.len[s] + e0;
+    char* ybase = a.y + st.yoff[s];
+    if (a.dt_y == EA_BF16 && ES == 2) {
+      uint4 pk;
+      uint32_t* w = reinterpret_cast<uint32_t*>(&pk);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f32_to_bf16(o[2 * i]) | ((uint32_t)f32_to_bf16(o[2 * i + 1]) << 16);
+      *reinterpret_cast<uint4*>(ybase + yidx * 2) = pk;
+    } else if (a.dt_y == EA_F32 && ES == 4) {
+      *reinterpret_cast<uint4*>(ybase + yidx * 4) =
+          make_uint4(__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]), __float_as_uint(o[3]));
+    } else {
+#pragma unroll
+      for (int i = 0; i < EPC; ++i) st_elem(ybase, yidx + i, a.dt_y, o[i]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// scalar path: any segment lengths, any row length; re-reads the row
+// ---------------------------------------------------------------------------
+template <bool SOFTMAX>
+__global__ __launch_bounds__(kThreads) void rows_scalar_kernel(RowArgs a) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int32_t* task = a.rows + 4 * blockIdx.x;
+  if (wid >= task[2]) return;
+  const RowInfo ri = row_info(a, wid);
+  const int d_last = a.rank - 1;
+  auto visit = [&](auto&& fn) {
+    for (int s = 0; s < ri.nseg; ++s) {
+      const int32_t* tp = a.tuples + (int64_t)(ri.t0 + s) * a.tuple_stride;
+      const DevBlk& xb = a.blk_x[tp[1]];
+      const int L = xb.ext[d_last];
+      const char* xbase = a.x + xb.off;
+      for (int e = lane; e < L; e += 64) {
+        const int64_t idx = (int64_t)ri.row * L + e;
+        const bool ok = !(SOFTMAX && a.causal) || xb.lo[d_last] + e <= ri.qpos;
+        fn(tp, idx, e, ok, ok ? ld_elem(xbase, idx, a.dt_x) : 0.0f);
+      }
+    }
+  };
+  if constexpr (SOFTMAX) {
+    float m = -INFINITY;
+    visit([&](const int32_t*, int64_t, int, bool ok, float x) { m = ok ? fmaxf(m, x) : m; });
+    m = wave_max(m);
+    float l = 0.0f;
+    visit([&](const int32_t*, int64_t, int, bool ok, float x) { l += ok ? __expf(x - m) : 0.0f; });
+    l = wave_sum(l);
+    const float inv = m == -INFINITY ? 0.0f : 1.0f / l;
+    visit([&](const int32_t* tp, int64_t idx, int, bool ok, float x) {
+      st_elem(a.y + a.blk_y[tp[0]].off, idx, a.dt_y, ok ? __expf(x - m) * inv : 0.0f);
+    });
+  } else {
+    float ss = 0.0f;
+    visit([&](const int32_t*, int64_t, int, bool, float x) { ss += x * x; });
+    ss = wave_sum(ss);
+    const float inv = 1.0f / sqrtf(ss / (float)a.row_len + a.eps);
+    visit([&](const int32_t* tp, int64_t idx, int e, bool, float x) {
+      const float w = ld_elem(a.w + a.blk_w[tp[2]].off, e, a.dt_w);
+      st_elem(a.y + a.blk_y[tp[0]].off, idx, a.dt_y, w * (x * inv));
+    });
+  }
+}
+
+template <bool SOFTMAX>
+hipError_t launch_rows(const RowArgs& a, hipStream_t s) {
+  if (a.n_rowtasks == 0) return hipSuccess;
+  const dim3 grid((uint32_t)a.n_rowtasks), block(kThreads);
+  if (a.vec) {
+    if (a.dt_x == EA_BF16) hipLaunchKernelGGL((rows_vec_kernel<uint16_t, SOFTMAX>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((rows_vec_kernel<float, SOFTMAX>), grid, block, 0, s, a);
+  } else {
+    hipLaunchKernelGGL((rows_scalar_kernel<SOFTMAX>), grid, block, 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_rmsnorm(const RowArgs& a, hipStream_t s) { return launch_rows<false>(a, s); }
+hipError_t launch_softmax(const RowArgs& a, hipStream_t s) { return launch_rows<true>(a, s); }
+
+// Whether a row layout fits the register path: every segment a multiple of
+// 16 bytes, at most kMaxSeg segments and kMaxK chunks per lane.
+bool rows_vec_ok(int64_t row_len, int64_t max_segments, bool seg_aligned, int es) {
+  return seg_aligned && max_segments <= kMaxSeg && row_len * es <= (int64_t)kMaxK * 64 * 16;
+}
+
+}  // namespace ea

@@ -1,0 +1,69 @@
+"""Shared helpers of the GPU parity tests.
+
+Inputs are packed into block layout with the oracle's own layout code (test
+side), uploaded, run through the C ABI, downloaded and unpacked with the
+oracle again, so the product's layout is checked independently on every test.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+import synth
+from paper_2609_03905_amd import ea
+
+NP_STORAGE = {"f32": np.float32, "bf16": np.uint16, "f16": np.uint16}
+
+# Tolerance of the floating-point comparisons (relative Frobenius error and
+# max |diff| relative to max |ref|).
+REL_FRO = 1e-3
+MAX_ABS_REL = 2e-2
+
+
+def upload(stored: np.ndarray, dtype: str, partition) -> ea.Relation:
+    """A device relation holding ``stored`` (dense, storage dtype) under ``partition``."""
+    blocked = oracle.pack(np.ascontiguousarray(stored), partition)
+    t = torch.from_numpy(blocked).to("cuda")
+    return ea.Relation(stored.shape, dtype, partition, data=t)
+
+
+def empty(shape, dtype: str, partition) -> ea.Relation:
+    r = ea.Relation(shape, dtype, partition)
+    r.data.fill_(0xFF)  # NaN-ish garbage: anything not written shows up
+    return r
+
+
+def download(rel: ea.Relation) -> np.ndarray:
+    """Dense stored values of a device relation."""
+    torch.cuda.synchronize()
+    raw = rel.bytes().cpu().numpy()
+    return oracle.unpack(raw, rel.partition, NP_STORAGE[rel.dtype])
+
+
+def values(rel: ea.Relation) -> np.ndarray:
+    return synth.to_f64(download(rel), rel.dtype)
+
+
+def expected(ref64: np.ndarray, dtype: str) -> np.ndarray:
+    """The oracle's fp64 result as the output dtype would store it (bf16 via
+    the oracle's round-to-nearest-even; f32 by the fp64->fp32 cast)."""
+    if dtype == "bf16":
+        return oracle.rne_bf16(ref64)
+    if dtype == "f32":
+        return ref64.astype(np.float32).astype(np.float64)
+    return ref64.astype(np.float16).astype(np.float64)
+
+
+def assert_close(got: np.ndarray, ref: np.ndarray, rel_fro: float = REL_FRO, max_abs_rel: float = MAX_ABS_REL,
+                 what: str = ""):
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    diff = got - ref
+    nref = np.linalg.norm(ref)
+    fro = np.linalg.norm(diff) / nref if nref > 0 else np.linalg.norm(diff)
+    mx = np.max(np.abs(diff)) if diff.size else 0.0
+    scale = np.max(np.abs(ref)) if ref.size else 0.0
+    assert fro <= rel_fro, f"{what}: relative Frobenius error {fro:.3e} > {rel_fro:.1e}"
+    assert mx <= max_abs_rel * scale + 1e-30, f"{what}: max |diff| {mx:.3e} > {max_abs_rel} * {scale:.3e}"
+    return fro, mx
