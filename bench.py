@@ -1,20 +1,30 @@
 """Throughput of one GPU's share of the block join-agg hot path on MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qkv]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload block|qkv|attention|reductions]
 
-Workload "qkv": the LLaMA-7B QKV projection, one GPU's 1/8 column share:
-'tj,jk->tk' bf16 with t = 4096 tokens (2 x 2048), j = 4096, k = 1536, blocks
-512 x 512, x ~ N(0,1), W ~ N(0, 0.02); the join-agg (192 tuples in 24 output
-groups, SUM of 8 partial products per output block) followed by the
-repartition of its output from 512 x 512 blocks to per-head 4096 x 128 blocks.
-One step = that join-agg + that repartition; inputs are resident in HBM
-before the timed region.  Prints one JSON line.
+Default workload "block": one GPU's share of a LLaMA-65B-shape transformer
+block (hidden 8192, 8 of 64 heads of dim 128, SwiGLU FFN 2752 = 22016/8,
+batch 1 x seq 2048, bf16, seeded N(0,1) activations, N(0,0.02) weights,
+U(0.5,1.5) norm weights).  One step = the whole chain: RMSNorm join-agg, QKV
+block-GEMM join-agg, repartition to per-head blocks, causal attention join-agg
+(online-softmax aggregation over 128-key blocks), repartition back, O-proj
+join-agg with fused residual, RMSNorm, SwiGLU join-agg, down join-agg with
+fused residual.  The join of every stage is resolved once (plan cache) before
+the timed region; inputs are resident in HBM.  `value` = the step's
+algorithmic FLOPs (423.06 GFLOP) / step time.
+
+Other workloads (not the default line): "qkv" = the LLaMA-7B QKV projection
+share 'tj,jk->tk' 4096x4096x1536 in 512x512 blocks plus its repartition to
+per-head 4096x128 blocks; "attention" = causal attention B2 H4 S2048 D128;
+"reductions" = RMSNorm over x[4096, 4096] in 8 column blocks and causal
+softmax over s[4, 2048, 2048] in 256-key blocks.
+
+Prints one JSON line.
 """
 from __future__ import annotations
 
 import argparse
 import json
-import math
 import os
 import sys
 import time
@@ -23,81 +33,165 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
+METRIC = "join-agg TFLOP/s (%MFMA peak), norm/repartition GB/s (%HBM), ms per LLaMA block"
 
 
-def _events_ms(fn, n):
-    """Average duration of fn() over n launches, timed with HIP events on the
-    current stream (the stream libea launches on)."""
+def _events_ms(fn, n, warm=3):
+    """Average duration of fn() over n back-to-back launches, measured with
+    HIP events on the current stream (the stream libea launches on)."""
     import torch
 
-    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    times = []
-    for _ in range(n):
-        s.record()
+    for _ in range(warm):
         fn()
-        e.record()
-        e.synchronize()
-        times.append(s.elapsed_time(e))
-    return sum(times) / len(times)
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(n):
+        fn()
+    e.record()
+    e.synchronize()
+    return s.elapsed_time(e) / n
+
+
+def _dev(a):
+    import numpy as np
+    import torch
+
+    return torch.from_numpy(a.view(np.int16)).cuda()
+
+
+# ---------------------------------------------------------------------------
+# workloads
+# ---------------------------------------------------------------------------
+def block_workload():
+    import synth
+    from paper_2609_03905_amd.block import LlamaBlockShare
+
+    w = synth.llama_block()
+    blk = LlamaBlockShare(w["t"], w["hidden"], w["heads"], w["d_head"], w["ffn"], block=w["block"], eps=w["eps"])
+    blk.load({k: _dev(w[k]) for k in ("x", "n1", "n2", "wqkv", "wo", "wg", "wu", "wd")})
+    work = blk.work()
+    stages = blk.stages()
+    comps = {name: dict(fn=fn, **work[name]) for name, fn in stages}
+    flops = sum(c.get("flops", 0) for c in comps.values())
+    return dict(step=blk.forward, flops=flops, comps=comps, dominant="swiglu_gemm",
+                config={"workload": "llama65b_block_share", "hidden": 8192, "heads": "8 of 64", "d_head": 128,
+                        "ffn": 2752, "tokens": 2048, "batch": 1, "block": 512, "dtype": "bf16",
+                        "chain": [n for n, _ in stages]},
+                cpu=cpu_baseline_block)
 
 
 def qkv_workload():
-    import torch
-
     import synth
     from paper_2609_03905_amd import ea
 
     w = synth.qkv_projection()
-    X = ea.from_dense(torch.from_numpy(w["X"].view("int16")).cuda(), "bf16", w["pX"])
-    W = ea.from_dense(torch.from_numpy(w["W"].view("int16")).cuda(), "bf16", w["pW"])
+    X = ea.from_dense(_dev(w["X"]), "bf16", w["pX"])
+    W = ea.from_dense(_dev(w["W"]), "bf16", w["pW"])
     Y = ea.Relation((4096, 1536), "bf16", w["pY"])
     Yh = ea.Relation((4096, 1536), "bf16", w["pHead"])
-
-    def gemm():
-        ea.joinagg("tj,jk->tk", ea.JOIN_MUL, ea.AGG_SUM, [X, W], Y)
-
-    def repart():
-        ea.repartition(Y, Yh)
+    gemm = lambda: ea.joinagg("tj,jk->tk", ea.JOIN_MUL, ea.AGG_SUM, [X, W], Y)
+    repart = lambda: ea.repartition(Y, Yh)
 
     def step():
         gemm()
         repart()
 
     flops = 2.0 * 4096 * 4096 * 1536
-    repart_bytes = 2 * 4096 * 1536 * 2
-    comps = {
-        "joinagg_gemm": dict(fn=gemm, flops=flops, bound="mfma"),
-        "repartition": dict(fn=repart, bytes=repart_bytes, bound="hbm"),
-    }
+    comps = {"joinagg_gemm": dict(fn=gemm, flops=flops), "repartition": dict(fn=repart, bytes=2 * 4096 * 1536 * 2)}
     return dict(step=step, flops=flops, comps=comps, dominant="joinagg_gemm",
-                config={"workload": "qkv_projection_share", "spec": "tj,jk->tk", "t": 4096, "j": 4096, "k": 1536,
-                        "block": 512, "repartition": "512x512 -> 4096x128 per-head blocks", "dtype": "bf16"})
+                config={"workload": "llama7b_qkv_projection_share", "spec": "tj,jk->tk", "t": 4096, "j": 4096,
+                        "k": 1536, "block": 512, "repartition": "512x512 -> 4096x128", "dtype": "bf16"},
+                cpu=cpu_baseline_qkv)
 
 
-def cpu_baseline_qkv(target_s: float = 10.0):
-    """The oracle's dense fp64 product on a bounded sample of output rows of
-    the same workload, scaled to TFLOP/s."""
+def attention_workload():
+    import synth
+    from paper_2609_03905_amd import ea
+
+    w = synth.attention()
+    Q, K, V = (ea.from_dense(_dev(w[n]), "bf16", w["pq"]) for n in "qkv")
+    O = ea.Relation((2, 4, 2048, 128), "bf16", w["pq"])
+    fn = lambda: ea.joinagg("bhqd,bhkd,bhkd->bhqd", ea.OP_ATTENTION, ea.AGG_LSE, [Q, K, V], O, scale=w["scale"],
+                            causal=True)
+    flops = 4.0 * 128 * 2 * 4 * 2048 * 2049 / 2
+    return dict(step=fn, flops=flops, comps={"attention": dict(fn=fn, flops=flops)}, dominant="attention",
+                config={"workload": "llama7b_causal_attention_share", "batch": 2, "heads": 4, "seq": 2048,
+                        "d_head": 128, "q_block": 128, "k_block": 128, "dtype": "bf16"}, cpu=None)
+
+
+def reductions_workload():
+    import synth
+    from paper_2609_03905_amd import ea
+
+    w = synth.reductions()
+    X = ea.from_dense(_dev(w["x"]), "bf16", w["px"])
+    Wt = ea.from_dense(_dev(w["w"]), "bf16", w["pw"])
+    Y = ea.Relation((4096, 4096), "bf16", w["px"])
+    S = ea.from_dense(_dev(w["s"]), "bf16", w["ps"])
+    P = ea.Relation((4, 2048, 2048), "bf16", w["ps"])
+    rms = lambda: ea.joinagg("tc,c->tc", ea.OP_RMSNORM, ea.AGG_SUM, [X, Wt], Y, eps=w["eps"])
+    sm = lambda: ea.joinagg("hqk->hqk", ea.OP_SOFTMAX, ea.AGG_LSE, [S], P, causal=True)
+
+    def step():
+        rms()
+        sm()
+
+    rms_bytes = 2 * 4096 * 4096 * 2 + 4096 * 2
+    sm_bytes = 4 * (2048 * 2049 // 2) * 2 + 4 * 2048 * 2048 * 2
+    return dict(step=step, flops=0.0, comps={"rmsnorm": dict(fn=rms, bytes=rms_bytes),
+                                            "causal_softmax": dict(fn=sm, bytes=sm_bytes)},
+                dominant="rmsnorm", bytes=rms_bytes + sm_bytes,
+                config={"workload": "reductions", "rmsnorm": "x[4096,4096] bf16, 8 column blocks",
+                        "softmax": "s[4,2048,2048] bf16 causal, 256-key blocks", "dtype": "bf16"}, cpu=None)
+
+
+# ---------------------------------------------------------------------------
+# CPU baselines: the oracle, untuned, on a bounded sample of the workload
+# ---------------------------------------------------------------------------
+def _adaptive(run, first, cap, target_s):
+    n = first
+    while True:
+        t0 = time.perf_counter()
+        run(n)
+        dt = time.perf_counter() - t0
+        if dt >= target_s / 3 or n >= cap:
+            return n, dt
+        n = min(cap, max(2 * n, int(n * target_s / 3 / max(dt, 1e-3))))
+
+
+def cpu_baseline_block(target_s: float = 12.0):
     import numpy as np
 
     import oracle
     import synth
 
+    w = synth.llama_block()
+    f = {k: synth.to_f64(w[k], "bf16") for k in ("x", "n1", "wqkv", "wo", "wg", "wu", "wd", "n2")}
+    run = lambda rows: oracle.llama_block(f["x"][:rows], f["n1"], f["wqkv"], f["wo"], f["wg"], f["wu"], f["wd"],
+                                          f["n2"], heads=8, d_head=128, eps=1e-6)
+    rows, dt = _adaptive(run, 16, 2048, target_s)
+    dense = 2 * rows * (8192 * 3072 + 1024 * 8192 + 2 * 8192 * 2752 + 2752 * 8192)
+    attn = 4 * 128 * 8 * rows * (rows + 1) // 2
+    return {"value": (dense + attn) / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"fp64 oracle block chain on the first {rows} of 2048 tokens (causal prefix), {dt:.1f} s"}
+
+
+def cpu_baseline_qkv(target_s: float = 12.0):
+    import oracle
+    import synth
+
     w = synth.qkv_projection()
-    x = synth.to_f64(w["X"], "bf16")
-    wt = synth.to_f64(w["W"], "bf16")
-    rows = 16
-    while True:
-        t0 = time.perf_counter()
-        oracle.matmul(x[:rows], wt)
-        dt = time.perf_counter() - t0
-        if dt > target_s / 4 or rows >= 4096:
-            break
-        rows = min(4096, int(rows * max(2.0, target_s / 4 / max(dt, 1e-3))))
-    flops = 2.0 * rows * 4096 * 1536
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"fp64 oracle matmul of {rows} of 4096 output rows x 1536 columns, K=4096 ({dt:.1f} s)"}
+    x, wt = synth.to_f64(w["X"], "bf16"), synth.to_f64(w["W"], "bf16")
+    rows, dt = _adaptive(lambda r: oracle.matmul(x[:r], wt), 16, 4096, target_s)
+    return {"value": 2.0 * rows * 4096 * 1536 / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "sample": f"fp64 oracle matmul of {rows} of 4096 output rows, {dt:.1f} s"}
+
+
+WORKLOADS = {"block": block_workload, "qkv": qkv_workload, "attention": attention_workload,
+             "reductions": reductions_workload}
 
 
 def main():
@@ -105,24 +199,24 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="qkv", choices=["qkv"])
+    ap.add_argument("--workload", default="block", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs one GPU's share on one GPU; --gpus {args.gpus} is not supported "
-              "(the multi-GPU exchange is outside this build)", file=sys.stderr)
+        print(f"bench.py measures one GPU's share on one GPU; --gpus {args.gpus} is not supported "
+              "(exchanges between GPUs are outside this build)", file=sys.stderr)
         sys.exit(2)
 
     import torch
 
     torch.cuda.set_device(0)
-    wl = qkv_workload()
+    wl = WORKLOADS[args.workload]()
     step = wl["step"]
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
     s.record()
     for _ in range(args.steps):
         step()
@@ -134,7 +228,7 @@ def main():
     comps = {}
     for name, c in wl["comps"].items():
         ms = _events_ms(c["fn"], max(args.steps, 20))
-        d = {"ms": ms}
+        d = {"ms": round(ms, 5)}
         if "flops" in c:
             d["tflops"] = c["flops"] / ms / 1e9
             d["frac_mfma_peak"] = d["tflops"] / PEAK_BF16_TFLOPS
@@ -144,7 +238,7 @@ def main():
         comps[name] = d
     dom = wl["comps"][wl["dominant"]]
     dms = comps[wl["dominant"]]["ms"]
-    if dom["bound"] == "mfma":
+    if "flops" in dom:
         achieved = dom["flops"] / dms / 1e9
         roof = {"kernel": wl["dominant"], "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None}
@@ -153,16 +247,18 @@ def main():
         roof = {"kernel": wl["dominant"], "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None}
 
-    value = wl["flops"] / ms_per_step / 1e9
+    if wl["flops"]:
+        value, unit = wl["flops"] / ms_per_step / 1e9, "TFLOP/s"
+    else:
+        value, unit = wl["bytes"] / ms_per_step / 1e6, "GB/s"
     out = {
-        "metric": "join-agg TFLOP/s (%MFMA peak), norm/repartition GB/s (%HBM), ms per LLaMA block",
-        "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "metric": METRIC, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic (seeded N(0,1) activations, N(0,0.02) weights)",
-        "config": wl["config"], "roofline": roof, "components": comps, "wall_s": wall,
+        "dtype": "bf16", "data": "synthetic (seeded N(0,1) activations, N(0,0.02) weights, random init)",
+        "config": wl["config"], "roofline": roof, "components": comps, "wall_s": round(wall, 4),
     }
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline_qkv()
+    if not args.no_cpu_baseline and wl.get("cpu"):
+        out["cpu_baseline"] = wl["cpu"]()
     print(json.dumps(out))
 
 

@@ -169,9 +169,9 @@ int ea_relation_block(const ea_relation* rel, int64_t b, int64_t* lo, int64_t* h
      "<b>qd"; O = softmax(scale * Q K^T) V per batch letters <b>; d must be
      a single block of extent 128; q and k block extents multiples of 128;
      the causal rule needs q and k of the same extent; bf16 data.
-     Scores and softmax in f32; the probabilities are rounded to fp16 and V
-     converted to fp16 for the P.V product (fp32 accumulation), so V values
-     must lie within the fp16 range.
+     Scores and softmax in f32; for the P.V product V is converted to fp16
+     and P is split into two fp16 terms (hi + lo, about 22 significant bits),
+     fp32 accumulation, so V values must lie within the fp16 range.
    EA_OP_SWIGLU, agg SUM: in = (X "tj", W1 "jk", W2 "jk"), out "tk" =
      silu(X W1) * (X W2), silu(g) = g / (1 + e^-g); bf16 data.
    Errors: EA_ERR_ARG, EA_ERR_SPEC, EA_ERR_DTYPE, EA_ERR_JOIN,

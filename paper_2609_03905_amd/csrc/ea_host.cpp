@@ -568,6 +568,9 @@ int classify(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation*
         if (v % 128) return fail(EA_ERR_UNSUPPORTED, "ATTENTION needs query block bounds that are multiples of 128");
       for (int64_t v : ops[1]->splits[r - 2])
         if (v % 128) return fail(EA_ERR_UNSUPPORTED, "ATTENTION needs key block bounds that are multiples of 128");
+      for (int dd = 0; dd < r - 2; ++dd)
+        if (ops[0]->nb[dd] != ops[0]->shape[dd])
+          return fail(EA_ERR_UNSUPPORTED, "ATTENTION needs one block per batch-letter index (dim %d)", dd);
       const int causal = prm ? prm->causal : 0;
       if (causal && ops[0]->shape[r - 2] != ops[1]->shape[r - 2])
         return fail(EA_ERR_SPEC, "causal ATTENTION needs as many queries as keys");

@@ -1,0 +1,74 @@
+"""GPU parity of the composite: one GPU's share of a LLaMA-shaped block run as
+a chain of join-aggs and repartitions, against the oracle's chain with bf16
+rounding at the same relation boundaries."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from helpers import assert_close, values
+from paper_2609_03905_amd.block import LlamaBlockShare
+
+pytestmark = pytest.mark.gpu
+
+# Tolerance of the chain.  Every relation boundary of the chain rounds to
+# bf16, and the softmax and the SwiGLU product amplify any 1-ulp difference in
+# an upstream relation; an fp32 evaluation of this chain composed of torch
+# library routines (CPU, same rounding points) differs from the fp64 oracle's
+# chain by 2.98e-3 (relative Frobenius) at y on the full-size workload.  The
+# chain is therefore held to 5e-3; each join-agg alone is held to 1e-3 in the
+# other tests, and a well-conditioned chain below is held to 1e-3 too.
+CHAIN_REL_FRO = 5e-3
+
+
+def _device(w):
+    return {k: torch.from_numpy(w[k].view(np.int16)).cuda() for k in ("x", "n1", "n2", "wqkv", "wo", "wg", "wu", "wd")}
+
+
+def _oracle(w, rows=None):
+    f = {k: synth.to_f64(w[k], "bf16") for k in ("x", "n1", "wqkv", "wo", "wg", "wu", "wd", "n2")}
+    x = f["x"] if rows is None else f["x"][:rows]
+    return oracle.llama_block(x, f["n1"], f["wqkv"], f["wo"], f["wg"], f["wu"], f["wd"], f["n2"],
+                              heads=w["heads"], d_head=w["d_head"], eps=w["eps"])
+
+
+def _run(w):
+    blk = LlamaBlockShare(w["t"], w["hidden"], w["heads"], w["d_head"], w["ffn"], block=w["block"], eps=w["eps"])
+    blk.load(_device(w))
+    blk.forward()
+    torch.cuda.synchronize()
+    return blk
+
+
+def test_block_small_all_boundaries():
+    w = synth.llama_block(t=256, hidden=512, heads=2, d_head=128, ffn=344, block=128)
+    blk = _run(w)
+    ref = _oracle(w)
+    for name in ("h1", "qkv", "attn", "x2", "h2", "a", "y"):
+        assert_close(values(getattr(blk, name)), ref[name], rel_fro=CHAIN_REL_FRO, what=name)
+
+
+def test_block_well_conditioned_chain_strict():
+    """Small weights keep the softmax flat and the SwiGLU product small, so
+    rounding flips do not cascade: the whole chain meets 1e-3."""
+    w = synth.llama_block(t=256, hidden=512, heads=2, d_head=128, ffn=344, block=128)
+    for k in ("wqkv", "wo", "wg", "wu", "wd"):
+        w[k] = synth.store(synth.to_f64(w[k], "bf16") * 0.1, "bf16")
+    blk = _run(w)
+    ref = _oracle(w)
+    for name in ("h1", "qkv", "attn", "x2", "h2", "a", "y"):
+        assert_close(values(getattr(blk, name)), ref[name], what=name)
+
+
+def test_block_full_size():
+    w = synth.llama_block()
+    blk = _run(w)
+    ref = _oracle(w)
+    for name in ("h1", "qkv", "attn", "x2", "h2", "a", "y"):
+        assert_close(values(getattr(blk, name)), ref[name], rel_fro=CHAIN_REL_FRO, what=name)
+    # a second forward pass reproduces the same bytes (fixed aggregation order)
+    y1 = blk.y.bytes().clone()
+    blk.forward()
+    torch.cuda.synchronize()
+    assert torch.equal(y1, blk.y.bytes())
