@@ -650,10 +650,27 @@ int build_generic(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_rela
   return EA_OK;
 }
 
-// Tiles of every output block, ordered so that the tiles one XCD receives
-// (workgroup ids congruent mod 8) come from one contiguous stretch of the
-// natural order and so share operand blocks in that XCD's L2.
-std::vector<GemmTile> gemm_tiles(const ea_relation* c) {
+// Work units of a block-GEMM plan: every output block is cut into tiles of
+// kGemmTM x tn; a tile whose group has many tuples may be split into n_parts
+// runs of tuples (the SUM over the runs is merged by the kernel).  The split
+// count minimises a simple time model on 256 CUs (one workgroup per CU):
+//   waves(units) * ceil(iterations / parts) * t_step + merge traffic / BW
+// with t_step ~ 1 us per 64-deep K step of a full tile and the merge writing
+// and reading one 256 KiB fp32 partial per unit at ~4 TB/s.
+// Units are then ordered so that the workgroups one XCD receives (ids
+// congruent mod 8) come from one contiguous stretch of the natural order and
+// share operand blocks in that XCD's L2.
+struct GemmPlanInfo {
+  std::vector<GemmTile> units;
+  int32_t slots = 0, counters = 0;
+};
+
+GemmPlanInfo gemm_units(const ea_relation* a, const ea_relation* c, int tn) {
+  const int kCUs = 256;
+  // K steps of a group: every group has the same contracted blocks (a's column blocks)
+  int64_t steps = 0;
+  const int n_t = a->nb[1];
+  for (int b = 0; b < n_t; ++b) steps += (a->splits[1][b + 1] - a->splits[1][b] + 63) / 64;
   std::vector<GemmTile> nat;
   int32_t co[kMaxRank];
   for (int64_t b = 0; b < c->nblocks; ++b) {
@@ -661,25 +678,66 @@ std::vector<GemmTile> gemm_tiles(const ea_relation* c) {
     const int64_t me = c->splits[0][co[0] + 1] - c->splits[0][co[0]];
     const int64_t ne = c->splits[1][co[1] + 1] - c->splits[1][co[1]];
     for (int64_t m0 = 0; m0 < me; m0 += kGemmTM)
-      for (int64_t n0 = 0; n0 < ne; n0 += kGemmTN) nat.push_back(GemmTile{(int32_t)b, (int32_t)m0, (int32_t)n0});
+      for (int64_t n0 = 0; n0 < ne; n0 += tn) {
+        GemmTile t;
+        memset(&t, 0, sizeof(t));
+        t.block = (int32_t)b;
+        t.m0 = (int32_t)m0;
+        t.n0 = (int32_t)n0;
+        t.n_parts = 1;
+        t.slot = t.first_slot = t.counter = -1;
+        nat.push_back(t);
+      }
   }
-  const size_t n = nat.size();
-  const size_t nx = 8;
+  const int64_t tiles = (int64_t)nat.size();
+  int best_p = 1;
+  double best_t = 1e300;
+  for (int P = 1; P <= std::min(n_t, 16); ++P) {
+    const int64_t units = tiles * P;
+    const double waves = (double)((units + kCUs - 1) / kCUs);
+    const double t = waves * (double)((steps + P - 1) / P) * 1.0 + (P > 1 ? units * 2.0 * 262144.0 / 4.0e6 : 0.0);
+    if (t < best_t - 1e-9) {
+      best_t = t;
+      best_p = P;
+    }
+  }
+  GemmPlanInfo info;
+  std::vector<GemmTile> all;
+  for (const GemmTile& t0 : nat) {
+    for (int p = 0; p < best_p; ++p) {
+      GemmTile t = t0;
+      t.part = p;
+      t.n_parts = best_p;
+      if (best_p > 1) {
+        t.slot = info.slots + p;
+        t.first_slot = info.slots;
+        t.counter = info.counters;
+      }
+      all.push_back(t);
+    }
+    if (best_p > 1) {  // the next tile's slots and counter
+      info.slots += best_p;
+      info.counters += 1;
+    }
+  }
+  const size_t n = all.size(), nx = 8;
   std::vector<std::vector<GemmTile>> q(nx);
-  for (size_t i = 0; i < n; ++i) q[std::min(nx - 1, i * nx / std::max<size_t>(n, 1))].push_back(nat[i]);
+  for (size_t i = 0; i < n; ++i) q[std::min(nx - 1, i * nx / std::max<size_t>(n, 1))].push_back(all[i]);
   std::vector<size_t> head(nx, 0);
-  std::vector<GemmTile> out;
-  out.reserve(n);
-  for (size_t p = 0; out.size() < n; ++p) {
-    size_t x = p % nx;
+  info.units.reserve(n);
+  for (size_t p = 0; info.units.size() < n; ++p) {
+    const size_t x = p % nx;
     if (head[x] < q[x].size()) {
-      out.push_back(q[x][head[x]++]);
+      info.units.push_back(q[x][head[x]++]);
       continue;
     }
     for (size_t y = 0; y < nx; ++y)
-      if (head[y] < q[y].size()) { out.push_back(q[y][head[y]++]); break; }
+      if (head[y] < q[y].size()) {
+        info.units.push_back(q[y][head[y]++]);
+        break;
+      }
   }
-  return out;
+  return info;
 }
 
 int build_rows(const Spec& sp, const ea_relation* const* ops, const OpInfo& oi, Image* img, Extra* ex,
@@ -816,9 +874,12 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
   switch (oi.kind) {
     case K_GENERIC: e = build_generic(sp, join_op, agg_op, ops, ji, res, &img, &ex); break;
     case K_GEMM: {
-      auto tiles = gemm_tiles(ops[sp.n_in]);
-      ex.work = img.put_vec(tiles);
-      ex.n_work = (int64_t)tiles.size();
+      const GemmPlanInfo gi = gemm_units(ops[0], ops[sp.n_in], join_op == EA_OP_SWIGLU ? kGemmTNSwiglu : kGemmTN);
+      ex.work = img.put_vec(gi.units);
+      ex.n_work = (int64_t)gi.units.size();
+      ex.part_o = 0;  // partial sums of split tiles, then their counters
+      ex.counters = (size_t)gi.slots * kGemmTM * kGemmTN * sizeof(float);
+      ex.scratch_bytes = gi.slots ? ex.counters + (size_t)gi.counters * sizeof(int32_t) : 0;
       break;
     }
     case K_RMSNORM:
@@ -833,6 +894,10 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
   p->d_desc = ex.desc ? p->dmem + ex.desc : nullptr;
   p->d_work = p->dmem + ex.work;
   p->n_work = ex.n_work;
+  if (oi.kind == K_GEMM && ex.scratch_bytes) {
+    p->part_o = (float*)(p->dmem + scratch_base + ex.part_o);
+    p->counters = (int32_t*)(p->dmem + scratch_base + ex.counters);
+  }
   if (oi.kind == K_ATTENTION) {
     p->part_o = (float*)(p->dmem + scratch_base + ex.part_o);
     p->part_ml = (float*)(p->dmem + scratch_base + ex.part_ml);
@@ -1107,6 +1172,8 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
       a.b_kmajor = plan->b_kmajor;
       a.dt_in = in[0]->dtype;
       a.dt_out = out->dtype;
+      a.partials = plan->part_o;
+      a.counters = plan->counters;
       EA_HIP_TRY(launch_gemm(a, s));
       break;
     }

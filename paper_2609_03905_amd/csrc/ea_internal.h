@@ -114,11 +114,18 @@ hipError_t launch_repartition(const RepTask* d_tasks, int64_t n_tasks, const cha
 // Block GEMM on the matrix cores: out = sum over the group's tuples of
 // A_blk * B_blk (+ residual), bf16/f16 inputs, fp32 accumulation.
 // ---------------------------------------------------------------------------
-constexpr int kGemmTM = 128, kGemmTN = 128;  // output tile of one workgroup
+constexpr int kGemmTM = 256;          // output tile rows of one workgroup
+constexpr int kGemmTN = 256;          // output tile columns (128 for SwiGLU)
+constexpr int kGemmTNSwiglu = 128;
 
-struct GemmTile {  // one workgroup: a tile of one output block
-  int32_t block;   // output block == group index
+struct GemmTile {      // one workgroup: a tile of one output block and a run of its tuples
+  int32_t block;       // output block == group index
   int32_t m0, n0;
+  int32_t part;        // tuples [part*n/n_parts, (part+1)*n/n_parts) of the group's n
+  int32_t n_parts;
+  int32_t slot;        // partial-sum slot (split tiles only)
+  int32_t first_slot;  // first slot of the tile's parts
+  int32_t counter;     // arrival counter of the tile (split tiles only)
 };
 
 struct GemmArgs {
@@ -141,6 +148,8 @@ struct GemmArgs {
   int32_t dt_out;        // EA_F32, EA_BF16 or EA_F16
   int32_t dt_res;
   int32_t swiglu;        // 1: out = silu(A B) * (A B2)
+  float* partials;       // [slots][256 x 256] fp32 partial sums of split tiles
+  int32_t* counters;     // one per split tile; zero between calls
 };
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
