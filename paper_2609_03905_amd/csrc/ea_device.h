@@ -34,6 +34,18 @@ __device__ __forceinline__ uint16_t f32_to_f16(float f) {
   return h;
 }
 
+// Wavefront-uniform read-only metadata (tuple table, block tables) through
+// the constant address space: scalar loads, waited on with lgkmcnt, so they
+// never force a wait on in-flight vector loads.
+template <class T>
+__device__ __forceinline__ T ld_uniform(const T* p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return *(const __attribute__((address_space(4))) T*)(p);
+#else
+  return *p;  // host pass: parsed, never executed
+#endif
+}
+
 // Load/store one element of a relation given its dtype.
 __device__ __forceinline__ float ld_elem(const char* base, int64_t idx, int dt) {
   if (dt == EA_F32) return reinterpret_cast<const float*>(base)[idx];

@@ -11,13 +11,14 @@
 // recompose step is the store into the output block.
 //
 // Inputs bf16 or f16, fp32 accumulation (v_mfma_f32_32x32x16_{bf16,f16}).
-// 256 threads = 4 waves in a 2x2 grid.  Tile 256 x 256 (each wave 128 x 128,
-// 4 x 4 MFMA tiles, accumulators in AGPRs), or for SwiGLU 256 x 128 with two
-// right operands (each wave 128 x 64 per operand).  K step 64, LDS
-// double-buffered (2 x 72 KiB, rows padded to 72 elements: conflict-free
-// fragment reads), global loads for the next step staged in registers during
-// the current step's MFMAs.  A right operand stored [k][n] is transposed in
-// registers (4 k x 8 n per thread) before the LDS write, so both operands
+// 512 threads = 8 waves in a 2 (rows) x 4 (columns) grid, two waves per SIMD
+// so that one wave's LDS reads overlap the other's MFMAs.  Tile 256 x 256
+// (each wave 128 x 64: 4 x 2 MFMA tiles, 128 accumulators), or for SwiGLU
+// 256 x 128 with two right operands (each wave 128 x 32 per operand).  K step
+// 64, LDS double-buffered (2 x 72 KiB, rows padded to 72 elements:
+// conflict-free fragment reads); global loads run two K steps ahead of the
+// MFMAs (two register stages).  A right operand stored [k][n] is transposed
+// in registers (4 k x 8 n per thread) before the LDS write, so both operands
 // read 16 contiguous bytes per lane.
 //
 // Epilogues: residual relation added before the store; SwiGLU stores
@@ -35,7 +36,6 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 constexpr int TM = kGemmTM;  // 256
 constexpr int TK = 64;
 constexpr int PITCH = TK + 8;  // LDS row pitch in elements (144 bytes)
-constexpr int kThreads = 256;
 
 template <bool BF16>
 __device__ __forceinline__ f32x16_t mfma(const uint4& a, const uint4& b, const f32x16_t& c) {
@@ -59,37 +59,53 @@ __device__ __forceinline__ uint32_t word(const uint4& v, int w) {
   return w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
 }
 
-// ---- A tile: 256 rows x 64 k, k contiguous; 2048 16-byte pieces, 8 per thread
-__device__ __forceinline__ void load_a(uint4 (&r)[8], const char* base, const DevBlk& ab, int m0, int k0,
-                                       int tid) {
-  const int mext = ab.ext[0], kext = ab.ext[1];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int c = tid + kThreads * i;
-    const int gm = m0 + (c >> 3), gk = k0 + (c & 7) * 8;
-    const bool ok = gm < mext && gk < kext;
-    r[i] = masked_load(base, ok ? ((int64_t)gm * kext + gk) * 2 : 0, ok);
-  }
+// Uniform copy of a block's byte offset and 2-d extents (scalar loads).
+struct BlkInfo {
+  int64_t off;
+  int e0, e1;
+};
+
+__device__ __forceinline__ BlkInfo blk_info(const DevBlk* tab, int32_t idx) {
+  const DevBlk* b = tab + idx;
+  return BlkInfo{ld_uniform(&b->off), ld_uniform(&b->ext[0]), ld_uniform(&b->ext[1])};
 }
 
-__device__ __forceinline__ void store_a(const uint4 (&r)[8], uint16_t* s, int tid) {
+// ---- A tile: 256 rows x 64 k, k contiguous; 2048 16-byte pieces, NPA per thread
+template <int T>
+struct ATile {
+  static constexpr int NPA = TM * TK / 8 / T;
+  __device__ __forceinline__ static void load(uint4 (&r)[NPA], const char* base, const BlkInfo& ab, int m0, int k0,
+                                              int tid) {
+    const int mext = ab.e0, kext = ab.e1;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int c = tid + kThreads * i;
-    *reinterpret_cast<uint4*>(s + (c >> 3) * PITCH + (c & 7) * 8) = r[i];
+    for (int i = 0; i < NPA; ++i) {
+      const int c = tid + T * i;
+      const int gm = m0 + (c >> 3), gk = k0 + (c & 7) * 8;
+      const bool ok = gm < mext && gk < kext;
+      r[i] = masked_load(base, ok ? ((int64_t)gm * kext + gk) * 2 : 0, ok);
+    }
   }
-}
+  __device__ __forceinline__ static void store(const uint4 (&r)[NPA], uint16_t* s, int tid) {
+#pragma unroll
+    for (int i = 0; i < NPA; ++i) {
+      const int c = tid + T * i;
+      *reinterpret_cast<uint4*>(s + (c >> 3) * PITCH + (c & 7) * 8) = r[i];
+    }
+  }
+};
 
-// ---- B tile: BN columns x 64 k, stored in LDS as [n][k]; NP 16-byte pieces
-// per thread (BN = 256 -> 8, BN = 128 -> 4).
-template <bool KMAJOR, int BN>
+// ---- B tile: BN columns x 64 k, stored in LDS as [n][k].  [n][k] storage:
+// NP = BN*64/8/T 16-byte pieces per thread.  [k][n] storage: blocks of
+// 4 k x 8 n (block q: kg = q % 16, nc = q / 16), BN*64/32/T blocks per
+// thread, rounded up (threads past the last block take none).
+template <bool KMAJOR, int BN, int kThreads>
 struct BTile {
-  static constexpr int NP = BN * TK / 8 / kThreads;
-  // [k][n] storage: blocks of 4 k x 8 n; block q = tid + 256 b, kg = q % 16, nc = q / 16
-  __device__ __forceinline__ static void load(uint4 (&r)[NP], const char* base, const DevBlk& bb, int n0, int k0,
+  static constexpr int NBLK = BN * TK / 32;  // 4x8 blocks of the tile
+  static constexpr int NP = KMAJOR ? BN * TK / 8 / kThreads : 4 * ((NBLK + kThreads - 1) / kThreads);
+  __device__ __forceinline__ static void load(uint4 (&r)[NP], const char* base, const BlkInfo& bb, int n0, int k0,
                                               int tid) {
     if constexpr (!KMAJOR) {
-      const int kext = bb.ext[0], next = bb.ext[1];
+      const int kext = bb.e0, next = bb.e1;
 #pragma unroll
       for (int b = 0; b < NP / 4; ++b) {
         const int q = tid + kThreads * b;
@@ -98,12 +114,12 @@ struct BTile {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int gk = k0 + kg * 4 + i;
-          const bool ok = gk < kext && gn < next;
+          const bool ok = q < NBLK && gk < kext && gn < next;
           r[4 * b + i] = masked_load(base, ok ? ((int64_t)gk * next + gn) * 2 : 0, ok);
         }
       }
     } else {
-      const int next = bb.ext[0], kext = bb.ext[1];
+      const int next = bb.e0, kext = bb.e1;
 #pragma unroll
       for (int i = 0; i < NP; ++i) {
         const int c = tid + kThreads * i;
@@ -118,6 +134,7 @@ struct BTile {
 #pragma unroll
       for (int b = 0; b < NP / 4; ++b) {
         const int q = tid + kThreads * b;
+        if (NBLK % kThreads != 0 && q >= NBLK) break;
         const int kg = q & 15, nc = q >> 4;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -182,118 +199,24 @@ __device__ __forceinline__ void epilogue(const f32x16_t (&acc)[NB][4][WN], const
       }
 }
 
-template <bool BF16, bool KMAJOR, bool SWIGLU>
-__global__ __launch_bounds__(kThreads, 1) void gemm_kernel(const GemmArgs p) {
-  constexpr int NB = SWIGLU ? 2 : 1;      // right operands
-  constexpr int BN = SWIGLU ? 128 : 256;  // columns per right operand
-  constexpr int WN = BN / 2 / 32;         // MFMA tiles per wave along n, per operand
-  using BT = BTile<KMAJOR, BN>;
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2][TM * PITCH];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[2][NB * BN * PITCH];
+// Position of a K step: tuple index and offset inside its contracted block.
+struct KStep {
+  int t, k0;
+};
+
+// Split output keys: every unit writes its partial sums, the last unit of
+// the key (device-scope arrival counter, no waiting) adds all partials in part
+// order -- a fixed order, so results are deterministic -- and stores.
+// Partials are laid out in accumulator order (lane-contiguous float4s).
+// Then the epilogue, with dtype and residual decided outside its unrolled loops.
+template <bool SWIGLU, int NB, int WN, int W>
+__device__ __forceinline__ void finish_tile(f32x16_t (&acc)[NB][4][WN], const GemmArgs& p, const GemmTile& tile,
+                                            int wid, int lane, int row0, int col0) {
   __shared__ int s_last;
-
-  // kernel arguments into registers (no address of the argument block is taken)
-  const int32_t* __restrict__ tuples = p.tuples;
-  const DevBlk* __restrict__ blk_a = p.blk_a;
-  const DevBlk* __restrict__ blk_b = p.blk_b;
-  const DevBlk* __restrict__ blk_b2 = p.blk_b2;
-  const char* __restrict__ pa = p.a;
-  const char* __restrict__ pb = p.b;
-  const char* __restrict__ pb2 = p.b2;
-  const int ts = p.tuple_stride;
-
-  const GemmTile tile = p.tiles[blockIdx.x];
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
-  const int g = lane >> 5, lq = lane & 31;
-  const int32_t gb = p.goff[tile.block], ge = p.goff[tile.block + 1];
-  const int n_t = ge - gb;
-  const int t_begin = gb + (int)(((int64_t)tile.part * n_t) / tile.n_parts);
-  const int t_end = gb + (int)(((int64_t)(tile.part + 1) * n_t) / tile.n_parts);
-
-  f32x16_t acc[NB][4][WN];
-#pragma unroll
-  for (int o = 0; o < NB; ++o)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < WN; ++j) acc[o][i][j] = f32x16_t{};
-
-  uint4 ra[8], rb[NB][BT::NP];
-  int t = t_begin, k0 = 0;
-  bool have = t < t_end;
-  if (have) {
-    const int32_t* tp = tuples + (int64_t)t * ts;
-    const DevBlk& ab = blk_a[tp[1]];
-    load_a(ra, pa + ab.off, ab, tile.m0, 0, tid);
-    const DevBlk& bb = blk_b[tp[2]];
-    BT::load(rb[0], pb + bb.off, bb, tile.n0, 0, tid);
-    if constexpr (SWIGLU) {
-      const DevBlk& bb2 = blk_b2[tp[3]];
-      BT::load(rb[NB - 1], pb2 + bb2.off, bb2, tile.n0, 0, tid);
-    }
-    store_a(ra, sA[0], tid);
-#pragma unroll
-    for (int o = 0; o < NB; ++o) BT::store(rb[o], sB[0] + o * BN * PITCH, tid);
-  }
-  __syncthreads();
-  int buf = 0;
-  while (have) {
-    int nt = t, nk = k0 + TK;
-    if (nk >= blk_a[tuples[(int64_t)t * ts + 1]].ext[1]) {
-      nt = t + 1;
-      nk = 0;
-    }
-    const bool next = nt < t_end;
-    if (next) {  // prefetch the next K step into registers
-      const int32_t* tp = tuples + (int64_t)nt * ts;
-      const DevBlk& ab = blk_a[tp[1]];
-      load_a(ra, pa + ab.off, ab, tile.m0, nk, tid);
-      const DevBlk& bb = blk_b[tp[2]];
-      BT::load(rb[0], pb + bb.off, bb, tile.n0, nk, tid);
-      if constexpr (SWIGLU) {
-        const DevBlk& bb2 = blk_b2[tp[3]];
-        BT::load(rb[NB - 1], pb2 + bb2.off, bb2, tile.n0, nk, tid);
-      }
-    }
-    const uint16_t* a_s = sA[buf] + (wm * 128 + lq) * PITCH + 8 * g;
-    const uint16_t* b_s = sB[buf] + (wn * (BN / 2) + lq) * PITCH + 8 * g;
-#pragma unroll
-    for (int s = 0; s < TK / 16; ++s) {
-      uint4 af[4], bf[NB][WN];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const uint4*>(a_s + i * 32 * PITCH + s * 16);
-#pragma unroll
-      for (int o = 0; o < NB; ++o)
-#pragma unroll
-        for (int j = 0; j < WN; ++j)
-          bf[o][j] = *reinterpret_cast<const uint4*>(b_s + (o * BN + j * 32) * PITCH + s * 16);
-#pragma unroll
-      for (int o = 0; o < NB; ++o)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < WN; ++j) acc[o][i][j] = mfma<BF16>(af[i], bf[o][j], acc[o][i][j]);
-      __builtin_amdgcn_sched_barrier(0);  // bound the live fragment registers to one k16 step
-    }
-    if (next) {
-      store_a(ra, sA[buf ^ 1], tid);
-#pragma unroll
-      for (int o = 0; o < NB; ++o) BT::store(rb[o], sB[buf ^ 1] + o * BN * PITCH, tid);
-    }
-    __syncthreads();
-    buf ^= 1;
-    t = nt;
-    k0 = nk;
-    have = next;
-  }
-
-  // ---- split output key: write this unit's partial sums; the last unit of
-  // the key adds all partials in part order.  Partials are laid out in
-  // accumulator order (lane-contiguous float4s), so the accesses coalesce.
+  const int tid = wid * 64 + lane;
   if (tile.n_parts > 1) {
     constexpr int PER_WAVE = NB * 4 * WN * 16;  // floats per lane
-    float* mine = p.partials + ((int64_t)tile.slot * 4 + wid) * PER_WAVE * 64;
+    float* mine = p.partials + ((int64_t)tile.slot * W + wid) * PER_WAVE * 64;
 #pragma unroll
     for (int o = 0; o < NB; ++o)
 #pragma unroll
@@ -320,7 +243,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(const GemmArgs p) {
 #pragma unroll
         for (int j = 0; j < WN; ++j) acc[o][i][j] = f32x16_t{};
     for (int part = 0; part < tile.n_parts; ++part) {
-      const float* src = p.partials + ((int64_t)(tile.first_slot + part) * 4 + wid) * PER_WAVE * 64;
+      const float* src = p.partials + ((int64_t)(tile.first_slot + part) * W + wid) * PER_WAVE * 64;
 #pragma unroll
       for (int o = 0; o < NB; ++o)
 #pragma unroll
@@ -339,22 +262,418 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(const GemmArgs p) {
     }
     if (tid == 0) p.counters[tile.counter] = 0;  // ready for the next call (stream-ordered)
   }
-
-  // ---- epilogue (dtype and residual decided once, outside the unrolled loops)
   const DevBlk& cb = p.blk_c[tile.block];
-  const EpiArgs ea_{p.c + cb.off, p.res ? p.res + cb.off : nullptr, cb.ext[0], cb.ext[1],
-                    tile.m0 + wm * 128 + 4 * g, tile.n0 + wn * (BN / 2) + lq};
-  if (!ea_.res && p.dt_out == EA_BF16) epilogue<SWIGLU, NB, WN, EA_BF16, false>(acc, ea_);
-  else if (!ea_.res && p.dt_out == EA_F32) epilogue<SWIGLU, NB, WN, EA_F32, false>(acc, ea_);
-  else if (p.dt_out == EA_BF16) epilogue<SWIGLU, NB, WN, EA_BF16, true>(acc, ea_);
-  else if (p.dt_out == EA_F32) epilogue<SWIGLU, NB, WN, EA_F32, true>(acc, ea_);
-  else if (!ea_.res) epilogue<SWIGLU, NB, WN, EA_F16, false>(acc, ea_);
-  else epilogue<SWIGLU, NB, WN, EA_F16, true>(acc, ea_);
+  const EpiArgs e{p.c + cb.off, p.res ? p.res + cb.off : nullptr, cb.ext[0], cb.ext[1], row0, col0};
+  if (!e.res && p.dt_out == EA_BF16) epilogue<SWIGLU, NB, WN, EA_BF16, false>(acc, e);
+  else if (!e.res && p.dt_out == EA_F32) epilogue<SWIGLU, NB, WN, EA_F32, false>(acc, e);
+  else if (p.dt_out == EA_BF16) epilogue<SWIGLU, NB, WN, EA_BF16, true>(acc, e);
+  else if (p.dt_out == EA_F32) epilogue<SWIGLU, NB, WN, EA_F32, true>(acc, e);
+  else if (!e.res) epilogue<SWIGLU, NB, WN, EA_F16, false>(acc, e);
+  else epilogue<SWIGLU, NB, WN, EA_F16, true>(acc, e);
+}
+
+template <bool BF16, bool KMAJOR, bool SWIGLU, int W>
+__global__ __launch_bounds__(W * 64, 1) void gemm_kernel(const GemmArgs p) {
+  constexpr int kThreads = W * 64;
+  constexpr int NB = SWIGLU ? 2 : 1;      // right operands
+  constexpr int BN = SWIGLU ? 128 : 256;  // columns per right operand
+  constexpr int WGN = W / 2;              // waves along n (2 along m)
+  constexpr int WCOLS = BN / WGN;         // columns per wave, per operand
+  constexpr int WN = WCOLS / 32;          // MFMA tiles per wave along n, per operand
+  using BT = BTile<KMAJOR, BN, kThreads>;
+  using AT = ATile<kThreads>;
+  constexpr int NPA = AT::NPA;
+  __shared__ __attribute__((aligned(16))) uint16_t sA[2][TM * PITCH];
+  __shared__ __attribute__((aligned(16))) uint16_t sB[2][NB * BN * PITCH];
+
+  // kernel arguments into registers (no address of the argument block is taken)
+  const int32_t* __restrict__ tuples = p.tuples;
+  const DevBlk* __restrict__ blk_a = p.blk_a;
+  const DevBlk* __restrict__ blk_b = p.blk_b;
+  const DevBlk* __restrict__ blk_b2 = p.blk_b2;
+  const char* __restrict__ pa = p.a;
+  const char* __restrict__ pb = p.b;
+  const char* __restrict__ pb2 = p.b2;
+  const int ts = p.tuple_stride;
+
+  const GemmTile tile = ld_uniform(p.tiles + blockIdx.x);
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid / WGN, wn = wid % WGN;
+  const int g = lane >> 5, lq = lane & 31;
+  const int32_t gb = ld_uniform(p.goff + tile.block), ge = ld_uniform(p.goff + tile.block + 1);
+  const int n_t = ge - gb;
+  const int t_begin = gb + (int)(((int64_t)tile.part * n_t) / tile.n_parts);
+  const int t_end = gb + (int)(((int64_t)(tile.part + 1) * n_t) / tile.n_parts);
+
+  f32x16_t acc[NB][4][WN];
+#pragma unroll
+  for (int o = 0; o < NB; ++o)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j) acc[o][i][j] = f32x16_t{};
+
+  auto advance = [&](KStep st) -> KStep {
+    st.k0 += TK;
+    if (st.k0 >= ld_uniform(&blk_a[ld_uniform(tuples + (int64_t)st.t * ts + 1)].ext[1])) {
+      st.t += 1;
+      st.k0 = 0;
+    }
+    return st;
+  };
+  // two register stages of prefetched operands
+  uint4 ra[2][NPA], rb[2][NB][BT::NP];
+  auto load_step = [&](int set, KStep st) {
+    const int32_t* tp = tuples + (int64_t)st.t * ts;
+    const BlkInfo ab = blk_info(blk_a, ld_uniform(tp + 1));
+    AT::load(ra[set], pa + ab.off, ab, tile.m0, st.k0, tid);
+    const BlkInfo bb = blk_info(blk_b, ld_uniform(tp + 2));
+    BT::load(rb[set][0], pb + bb.off, bb, tile.n0, st.k0, tid);
+    if constexpr (SWIGLU) {
+      const BlkInfo bb2 = blk_info(blk_b2, ld_uniform(tp + 3));
+      BT::load(rb[set][NB - 1], pb2 + bb2.off, bb2, tile.n0, st.k0, tid);
+    }
+  };
+  auto store_step = [&](int set, int buf) {
+    AT::store(ra[set], sA[buf], tid);
+#pragma unroll
+    for (int o = 0; o < NB; ++o) BT::store(rb[set][o], sB[buf] + o * BN * PITCH, tid);
+  };
+  auto compute = [&](int buf) {
+    const uint16_t* a_s = sA[buf] + (wm * 128 + lq) * PITCH + 8 * g;
+    const uint16_t* b_s = sB[buf] + (wn * WCOLS + lq) * PITCH + 8 * g;
+#pragma unroll
+    for (int s = 0; s < TK / 16; ++s) {
+      uint4 af[4], bf[NB][WN];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const uint4*>(a_s + i * 32 * PITCH + s * 16);
+#pragma unroll
+      for (int o = 0; o < NB; ++o)
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+          bf[o][j] = *reinterpret_cast<const uint4*>(b_s + (o * BN + j * 32) * PITCH + s * 16);
+#pragma unroll
+      for (int o = 0; o < NB; ++o)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < WN; ++j) acc[o][i][j] = mfma<BF16>(af[i], bf[o][j], acc[o][i][j]);
+    }
+  };
+
+  // Pipeline: step s is computed from LDS buffer s%2; its operands were
+  // stored there at the end of step s-1 from register set s%2, which was
+  // loaded during step s-2.
+  KStep cur{t_begin, 0};
+  if (cur.t < t_end) {
+    load_step(0, cur);
+    KStep nx = advance(cur);
+    if (nx.t < t_end) load_step(1, nx);
+    store_step(0, 0);
+  }
+  __syncthreads();
+  // unrolled by two so that register sets are indexed statically
+  while (cur.t < t_end) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (cur.t >= t_end) break;
+      const KStep n1 = advance(cur);
+      const KStep n2 = n1.t < t_end ? advance(n1) : n1;
+      if (n2.t < t_end) load_step(h, n2);      // two steps ahead, into the set just consumed
+      compute(h);
+      if (n1.t < t_end) store_step(h ^ 1, h ^ 1);
+      __syncthreads();
+      cur = n1;
+    }
+  }
+
+  finish_tile<SWIGLU, NB, WN, W>(acc, p, tile, wid, lane, tile.m0 + wm * 128 + 4 * g, tile.n0 + wn * WCOLS + lq);
+}
+
+// ===========================================================================
+// Direct-to-LDS pipeline (fast path): operands go from global memory straight
+// into LDS (global_load_lds, 16 bytes per lane, lane-linear placement), with
+// no staging registers and no LDS write instructions.  Four stages of 32-deep
+// K steps (4 x 32 KiB) keep three steps of loads in flight while one is
+// computed.  LDS layouts, 16-byte chunks XOR-swizzled so that the fragment
+// reads spread over all banks (for 16-lane groups over 64 banks and for
+// 8-lane groups over 32 banks alike):
+//   A, and B stored [n][k]: row r (64 bytes = 4 chunks), logical chunk c at
+//     physical chunk c ^ swz_row(r);
+//   B stored [k][n]: row k (BN*2 bytes), logical chunk c at physical chunk
+//     c ^ swz_k(k); the MFMA operand (8 consecutive k of one column) is
+//     read with two ds_read_b64_tr_b16: in each 16-lane group, lane 4k'+r
+//     reads 4 columns N0+4r.. of row K0+k', and lane i receives rows K0..K0+3
+//     of column N0+i.
+// Rows or columns past a block's edge load from the block base instead (their
+// products land only in accumulator rows/columns that are never stored); the
+// K extent of every contracted block must be a multiple of 32.
+// ===========================================================================
+constexpr int DK = 32;  // K per stage
+constexpr int NSTAGE = 4;
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// 64-byte rows: the 16 rows read by 16 consecutive lanes fall on 4 row
+// positions mod 256 bytes, each taking 4 distinct chunks.
+__device__ __forceinline__ int swz_row(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+// [k][n] rows (a multiple of 256 bytes): the 4 k rows of one transposed read
+// take disjoint chunk sets, for each half of the 32 lanes and for all 32.
+__device__ __forceinline__ int swz_k(int k) { return (2 * (k & 3)) ^ (8 * (k & 1)); }
+
+// One direct global->LDS load: each lane fetches 16 bytes at gptr and the
+// wave's 64 pieces land contiguously at lds_wave_base (lane-linear).  Issued
+// through inline asm so that the compiler does not track the LDS write: the
+// kernel orders it explicitly (vmcnt wait for the stage, then a barrier),
+// and the compiler's own in-order vmcnt waits stay correct (later loads only
+// make them more conservative).
+__device__ __forceinline__ void dl_load16(const char* gptr, uint16_t* lds_wave_base) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t*)lds_wave_base);  // wave-uniform
+  // M0 is listed as clobbered; nothing else in these kernels reads M0 (no
+  // LDS-parameter, message or relative-move instructions), so the warning
+  // that clang gives for a reserved register is silenced here.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds) : "memory", "m0");
+#pragma clang diagnostic pop
+}
+
+__device__ __forceinline__ uint2 tr_read(const uint16_t* p) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
+  return __builtin_bit_cast(uint2, v);
+}
+
+// vmcnt waits (gfx9 encoding: vmcnt bits [3:0] and [15:14], expcnt [6:4] and
+// lgkmcnt [11:8] left at their maxima)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Per-tuple operand metadata of one unit, staged in LDS before the pipeline
+// starts, so that the loop reads it with LDS reads and never has to wait on
+// the vector-memory counter that also tracks the in-flight operand loads.
+struct TupleMeta {
+  int64_t aoff, boff, b2off;
+  int32_t am, ak, b0, b1, b20, b21, pad0, pad1;
+};
+
+// Workgroup barrier for the direct-load pipeline.  __syncthreads() carries a
+// workgroup-scope fence that waits for every outstanding LDS-DMA load, which
+// would drain the prefetch; here the stage's own loads are already waited for
+// (vmcnt), so only this wave's LDS reads must finish (lgkmcnt) before the
+// barrier.  The empty asm statements keep the compiler from moving memory
+// operations across it.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <bool BF16, bool KMAJOR, bool SWIGLU, int W>
+__global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
+  constexpr int WGN = W / 2;              // waves along n (2 along m)
+  constexpr int NB = SWIGLU ? 2 : 1;      // right operands
+  constexpr int BN = SWIGLU ? 128 : 256;  // columns per right operand
+  constexpr int WCOLS = BN / WGN;         // columns per wave, per operand
+  constexpr int WN = WCOLS / 32;          // MFMA tiles per wave along n, per operand
+  constexpr int A_BYTES = TM * DK * 2;    // 16 KiB per stage
+  constexpr int B_BYTES = NB * BN * DK * 2;
+  constexpr int ROWB = BN * 2;            // bytes per k row of a [k][n] B stage
+  constexpr int LA = A_BYTES / 1024 / W;  // direct-load instructions per wave per stage
+  constexpr int LB = B_BYTES / 1024 / W;
+  constexpr int LS = LA + LB;
+  __shared__ __attribute__((aligned(1024))) uint16_t sA0[TM * DK], sA1[TM * DK], sA2[TM * DK], sA3[TM * DK];
+  __shared__ __attribute__((aligned(1024))) uint16_t sB0[NB * BN * DK], sB1[NB * BN * DK], sB2[NB * BN * DK],
+      sB3[NB * BN * DK];
+  __shared__ TupleMeta s_meta[kGemmMaxTuples];
+
+  const GemmTile tile = p.tiles[blockIdx.x];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid / WGN, wn = wid % WGN;
+  const int g = lane >> 5, lq = lane & 31;
+  const int32_t gb = p.goff[tile.block], ge = p.goff[tile.block + 1];
+  const int n_t = ge - gb;
+  const int t_begin = gb + (int)(((int64_t)tile.part * n_t) / tile.n_parts);
+  const int t_end = gb + (int)(((int64_t)(tile.part + 1) * n_t) / tile.n_parts);
+  const int nt = t_end - t_begin;  // <= kGemmMaxTuples (host guarantee)
+  for (int i = tid; i < nt; i += 64 * W) {
+    const int32_t* tp = p.tuples + (int64_t)(t_begin + i) * p.tuple_stride;
+    const DevBlk& ab = p.blk_a[tp[1]];
+    const DevBlk& bb = p.blk_b[tp[2]];
+    TupleMeta m;
+    m.aoff = ab.off;
+    m.am = ab.ext[0];
+    m.ak = ab.ext[1];
+    m.boff = bb.off;
+    m.b0 = bb.ext[0];
+    m.b1 = bb.ext[1];
+    if constexpr (SWIGLU) {
+      const DevBlk& b2 = p.blk_b2[tp[3]];
+      m.b2off = b2.off;
+      m.b20 = b2.ext[0];
+      m.b21 = b2.ext[1];
+    } else {
+      m.b2off = 0;
+      m.b20 = m.b21 = 0;
+    }
+    m.pad0 = m.pad1 = 0;
+    s_meta[i] = m;
+  }
+  __syncthreads();
+
+  f32x16_t acc[NB][4][WN];
+#pragma unroll
+  for (int o = 0; o < NB; ++o)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j) acc[o][i][j] = f32x16_t{};
+
+  // number of K steps of this unit (every contracted block extent is a multiple of DK)
+  int n_steps = 0;
+  for (int i = 0; i < nt; ++i) n_steps += s_meta[i].ak / DK;
+
+  const char* __restrict__ pa = p.a;
+  const char* __restrict__ pb = p.b;
+  const char* __restrict__ pb2 = p.b2;
+  // issue the direct loads of K step (tuple i of the unit, offset k0) into a stage
+  auto issue = [&](int i, int k0, uint16_t* sa, uint16_t* sb) {
+    const TupleMeta& m = s_meta[i];
+    {  // A: 256 rows x 32 k; wave instruction q covers 16 rows
+      const char* base = pa + m.aoff;
+      const int mext = m.am, kext = m.ak;
+#pragma unroll
+      for (int q = 0; q < LA; ++q) {
+        const int r = (wid * LA + q) * 16 + (lane >> 2);
+        const int c = (lane & 3) ^ swz_row(r);
+        const int gm = tile.m0 + r;
+        const int64_t off = gm < mext ? ((int64_t)gm * kext + k0 + 8 * c) * 2 : 0;
+        dl_load16(base + off, sa + (wid * LA + q) * 512);
+      }
+    }
+#pragma unroll
+    for (int o = 0; o < NB; ++o) {
+      const char* base = (o == 0 ? pb + m.boff : pb2 + m.b2off);
+      const int e0 = o == 0 ? m.b0 : m.b20, e1 = o == 0 ? m.b1 : m.b21;
+      uint16_t* sbo = sb + o * BN * DK;
+      if constexpr (KMAJOR) {  // [n][k]: like A, BN rows of 32 k
+#pragma unroll
+        for (int q = 0; q < LB / NB; ++q) {
+          const int r = (wid * (LB / NB) + q) * 16 + (lane >> 2);
+          const int c = (lane & 3) ^ swz_row(r);
+          const int gn = tile.n0 + r;
+          const int64_t off = gn < e0 ? ((int64_t)gn * e1 + k0 + 8 * c) * 2 : 0;
+          dl_load16(base + off, sbo + (wid * (LB / NB) + q) * 512);
+        }
+      } else {  // [k][n]: 32 rows of BN columns; wave instruction covers 1024 / ROWB rows
+        constexpr int RPI = 1024 / ROWB;
+        constexpr int CPR = ROWB / 16;  // chunks per row
+#pragma unroll
+        for (int q = 0; q < LB / NB; ++q) {
+          const int inst = wid * (LB / NB) + q;
+          const int k = inst * RPI + lane / CPR;
+          const int c = (lane % CPR) ^ swz_k(k);
+          const int gn = tile.n0 + 8 * c;
+          const int64_t off = gn < e1 ? ((int64_t)(k0 + k) * e1 + gn) * 2 : 0;
+          dl_load16(base + off, sbo + inst * 512);
+        }
+      }
+    }
+  };
+  // walk of the K steps: (tuple of the unit, offset) advanced by DK
+  int it_t = 0, it_k = 0;
+  auto next_step = [&]() {
+    it_k += DK;
+    if (it_k >= s_meta[it_t].ak) {
+      ++it_t;
+      it_k = 0;
+    }
+  };
+  uint16_t* const sAs[NSTAGE] = {sA0, sA1, sA2, sA3};
+  uint16_t* const sBs[NSTAGE] = {sB0, sB1, sB2, sB3};
+
+  auto compute = [&](const uint16_t* sa, const uint16_t* sb) {
+#pragma unroll
+    for (int s = 0; s < DK / 16; ++s) {
+      uint4 af[4], bf[NB][WN];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = wm * 128 + i * 32 + lq;
+        const int c = (2 * s + g) ^ swz_row(r);
+        af[i] = *reinterpret_cast<const uint4*>(sa + r * DK + 8 * c);
+      }
+#pragma unroll
+      for (int o = 0; o < NB; ++o)
+#pragma unroll
+        for (int j = 0; j < WN; ++j) {
+          const uint16_t* sbo = sb + o * BN * DK;
+          if constexpr (KMAJOR) {
+            const int r = wn * WCOLS + j * 32 + lq;
+            const int c = (2 * s + g) ^ swz_row(r);
+            bf[o][j] = *reinterpret_cast<const uint4*>(sbo + r * DK + 8 * c);
+          } else {
+            const int gq = lane >> 4, li = lane & 15;
+            const int n = wn * WCOLS + j * 32 + 16 * (gq & 1) + 4 * (li & 3);
+            uint2 h2[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const int k = 16 * s + 8 * (gq >> 1) + 4 * h + (li >> 2);
+              const int c = (n >> 3) ^ swz_k(k);
+              h2[h] = tr_read(sbo + k * BN + 8 * c + (n & 4));
+            }
+            bf[o][j] = make_uint4(h2[0].x, h2[0].y, h2[1].x, h2[1].y);
+          }
+        }
+#pragma unroll
+      for (int o = 0; o < NB; ++o)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < WN; ++j) acc[o][i][j] = mfma<BF16>(af[i], bf[o][j], acc[o][i][j]);
+    }
+  };
+
+  // prologue: steps 0..2 in flight
+#pragma unroll
+  for (int st = 0; st < NSTAGE - 1; ++st)
+    if (st < n_steps) {
+      issue(it_t, it_k, sAs[st], sBs[st]);
+      next_step();
+    }
+  // main loop, unrolled by the stage count so that stage buffers are static
+  for (int base = 0; base < n_steps; base += NSTAGE) {
+#pragma unroll
+    for (int u = 0; u < NSTAGE; ++u) {
+      const int st = base + u;
+      if (st < n_steps) {
+        // loads of step st are done once at most those of st+1, st+2 are pending
+        if (st + 2 < n_steps) wait_vmcnt<2 * LS>();
+        else if (st + 1 < n_steps) wait_vmcnt<LS>();
+        else wait_vmcnt<0>();
+        stage_barrier();
+        if (st + NSTAGE - 1 < n_steps) {  // refill the stage computed one step ago
+          issue(it_t, it_k, sAs[(u + NSTAGE - 1) % NSTAGE], sBs[(u + NSTAGE - 1) % NSTAGE]);
+          next_step();
+        }
+        compute(sAs[u], sBs[u]);
+      }
+    }
+  }
+  finish_tile<SWIGLU, NB, WN, W>(acc, p, tile, wid, lane, tile.m0 + wm * 128 + 4 * g, tile.n0 + wn * WCOLS + lq);
 }
 
 template <bool BF16, bool KMAJOR, bool SWIGLU>
 hipError_t launch3(const GemmArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((gemm_kernel<BF16, KMAJOR, SWIGLU>), dim3((uint32_t)a.n_tiles), dim3(kThreads), 0, s, a);
+  if (a.direct && a.waves == 4)
+    hipLaunchKernelGGL((gemm_dl_kernel<BF16, KMAJOR, SWIGLU, 4>), dim3((uint32_t)a.n_tiles), dim3(256), 0, s, a);
+  else if (a.direct)
+    hipLaunchKernelGGL((gemm_dl_kernel<BF16, KMAJOR, SWIGLU, 8>), dim3((uint32_t)a.n_tiles), dim3(512), 0, s, a);
+  else
+    hipLaunchKernelGGL((gemm_kernel<BF16, KMAJOR, SWIGLU, 8>), dim3((uint32_t)a.n_tiles), dim3(512), 0, s, a);
   return hipGetLastError();
 }
 

@@ -310,6 +310,7 @@ struct Plan {
   int64_t n_work = 0;
   // gemm
   int b_kmajor = 0;
+  int gemm_parts = 1;
   // rows
   int32_t row_len = 0;
   int32_t row_vec = 0;
@@ -663,6 +664,7 @@ int build_generic(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_rela
 struct GemmPlanInfo {
   std::vector<GemmTile> units;
   int32_t slots = 0, counters = 0;
+  int parts = 1;
 };
 
 GemmPlanInfo gemm_units(const ea_relation* a, const ea_relation* c, int tn) {
@@ -702,6 +704,7 @@ GemmPlanInfo gemm_units(const ea_relation* a, const ea_relation* c, int tn) {
     }
   }
   GemmPlanInfo info;
+  info.parts = best_p;
   std::vector<GemmTile> all;
   for (const GemmTile& t0 : nat) {
     for (int p = 0; p < best_p; ++p) {
@@ -877,6 +880,7 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
       const GemmPlanInfo gi = gemm_units(ops[0], ops[sp.n_in], join_op == EA_OP_SWIGLU ? kGemmTNSwiglu : kGemmTN);
       ex.work = img.put_vec(gi.units);
       ex.n_work = (int64_t)gi.units.size();
+      p->gemm_parts = gi.parts;
       ex.part_o = 0;  // partial sums of split tiles, then their counters
       ex.counters = (size_t)gi.slots * kGemmTM * kGemmTN * sizeof(float);
       ex.scratch_bytes = gi.slots ? ex.counters + (size_t)gi.counters * sizeof(int32_t) : 0;
@@ -1172,6 +1176,16 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
       a.b_kmajor = plan->b_kmajor;
       a.dt_in = in[0]->dtype;
       a.dt_out = out->dtype;
+      a.waves = getenv("EA_GEMM_WAVES") ? atoi(getenv("EA_GEMM_WAVES")) : 8;
+      {
+        // direct-to-LDS kernel: contracted block extents multiples of 32 and
+        // at most kGemmMaxTuples tuples per unit
+        bool k32 = true;
+        for (int64_t v : in[0]->splits[1]) k32 &= v % 32 == 0;
+        const int64_t per_unit = (in[0]->nb[1] + plan->gemm_parts - 1) / plan->gemm_parts;
+        a.direct = k32 && per_unit <= kGemmMaxTuples &&
+                   !(getenv("EA_GEMM_DIRECT") && atoi(getenv("EA_GEMM_DIRECT")) == 0);
+      }
       a.partials = plan->part_o;
       a.counters = plan->counters;
       EA_HIP_TRY(launch_gemm(a, s));

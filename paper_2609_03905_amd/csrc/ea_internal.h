@@ -117,6 +117,7 @@ hipError_t launch_repartition(const RepTask* d_tasks, int64_t n_tasks, const cha
 constexpr int kGemmTM = 256;          // output tile rows of one workgroup
 constexpr int kGemmTN = 256;          // output tile columns (128 for SwiGLU)
 constexpr int kGemmTNSwiglu = 128;
+constexpr int kGemmMaxTuples = 128;   // tuples per unit on the direct-to-LDS kernel
 
 struct GemmTile {      // one workgroup: a tile of one output block and a run of its tuples
   int32_t block;       // output block == group index
@@ -148,6 +149,8 @@ struct GemmArgs {
   int32_t dt_out;        // EA_F32, EA_BF16 or EA_F16
   int32_t dt_res;
   int32_t swiglu;        // 1: out = silu(A B) * (A B2)
+  int32_t waves;         // 4 or 8 waves per workgroup (register-staged kernel)
+  int32_t direct;        // 1: direct-to-LDS kernel (contracted block extents multiples of 32)
   float* partials;       // [slots][256 x 256] fp32 partial sums of split tiles
   int32_t* counters;     // one per split tile; zero between calls
 };
