@@ -422,14 +422,13 @@ __device__ __forceinline__ int swz_row(int r) { return ((r >> 1) ^ (r >> 3)) & 3
 __device__ __forceinline__ int swz_k(int k) { return (2 * (k & 3)) ^ (8 * (k & 1)); }
 
 // One direct global->LDS load: each lane fetches 16 bytes at gptr and the
-// wave's 64 pieces land contiguously at lds_wave_base (lane-linear).  Issued
+// wave's 64 pieces land contiguously at LDS byte address lds_addr (lane-linear).  Issued
 // through inline asm so that the compiler does not track the LDS write: the
 // kernel orders it explicitly (vmcnt wait for the stage, then a barrier),
 // and the compiler's own in-order vmcnt waits stay correct (later loads only
 // make them more conservative).
-__device__ __forceinline__ void dl_load16(const char* gptr, uint16_t* lds_wave_base) {
-  const uint32_t lds = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t*)lds_wave_base);  // wave-uniform
+__device__ __forceinline__ void dl_load16(const char* gptr, uint32_t lds_addr) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_addr);  // wave-uniform
   // M0 is listed as clobbered; nothing else in these kernels reads M0 (no
   // LDS-parameter, message or relative-move instructions), so the warning
   // that clang gives for a reserved register is silenced here.
@@ -453,8 +452,9 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 // Per-tuple operand metadata of one unit, staged in LDS before the pipeline
-// starts, so that the loop reads it with LDS reads and never has to wait on
-// the vector-memory counter that also tracks the in-flight operand loads.
+// starts, so that the K loop reads it (once per tuple) with LDS reads and
+// never with vector-memory loads, which share a counter with the in-flight
+// operand loads.
 struct TupleMeta {
   int64_t aoff, boff, b2off;
   int32_t am, ak, b0, b1, b20, b21, pad0, pad1;
@@ -464,35 +464,40 @@ struct TupleMeta {
 // workgroup-scope fence that waits for every outstanding LDS-DMA load, which
 // would drain the prefetch; here the stage's own loads are already waited for
 // (vmcnt), so only this wave's LDS reads must finish (lgkmcnt) before the
-// barrier.  The empty asm statements keep the compiler from moving memory
-// operations across it.
+// barrier.  The scheduling barriers keep the compiler from moving any
+// instruction (memory or MFMA) across it.
 __device__ __forceinline__ void stage_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 template <bool BF16, bool KMAJOR, bool SWIGLU, int W>
 __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
-  constexpr int WGN = W / 2;              // waves along n (2 along m)
-  constexpr int NB = SWIGLU ? 2 : 1;      // right operands
-  constexpr int BN = SWIGLU ? 128 : 256;  // columns per right operand
-  constexpr int WCOLS = BN / WGN;         // columns per wave, per operand
-  constexpr int WN = WCOLS / 32;          // MFMA tiles per wave along n, per operand
-  constexpr int A_BYTES = TM * DK * 2;    // 16 KiB per stage
-  constexpr int B_BYTES = NB * BN * DK * 2;
-  constexpr int ROWB = BN * 2;            // bytes per k row of a [k][n] B stage
-  constexpr int LA = A_BYTES / 1024 / W;  // direct-load instructions per wave per stage
-  constexpr int LB = B_BYTES / 1024 / W;
-  constexpr int LS = LA + LB;
-  __shared__ __attribute__((aligned(1024))) uint16_t sA0[TM * DK], sA1[TM * DK], sA2[TM * DK], sA3[TM * DK];
-  __shared__ __attribute__((aligned(1024))) uint16_t sB0[NB * BN * DK], sB1[NB * BN * DK], sB2[NB * BN * DK],
-      sB3[NB * BN * DK];
+  constexpr int WGN = W / 2;                   // waves along n (2 along m)
+  constexpr int NB = SWIGLU ? 2 : 1;           // right operands
+  constexpr int BN = SWIGLU ? 128 : 256;       // columns per right operand
+  constexpr int WCOLS = BN / WGN;              // columns per wave, per operand
+  constexpr int WN = WCOLS / 32;               // MFMA tiles per wave along n, per operand
+  constexpr int A_ELEMS = TM * DK;             // per stage
+  constexpr int B_ELEMS = BN * DK;             // per stage and right operand
+  constexpr int STAGE = A_ELEMS + NB * B_ELEMS;
+  constexpr int LA = A_ELEMS * 2 / 1024 / W;   // direct loads per wave and stage: A
+  constexpr int LBO = B_ELEMS * 2 / 1024 / W;  // ... and each right operand
+  constexpr int LS = LA + NB * LBO;
+  constexpr int ROWB = BN * 2;                 // bytes per k row of a [k][n] B stage
+  constexpr int RPI = 1024 / ROWB;             // [k][n] rows per load instruction
+  constexpr int CPR = ROWB / 16;               // 16-byte chunks per [k][n] row
+  static_assert(LA >= 1 && LBO >= 1 && 4 * LS < 64, "stage shape");
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[NSTAGE * STAGE];
   __shared__ TupleMeta s_meta[kGemmMaxTuples];
 
   const GemmTile tile = p.tiles[blockIdx.x];
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid / WGN, wn = wid % WGN;
   const int g = lane >> 5, lq = lane & 31;
   const int32_t gb = p.goff[tile.block], ge = p.goff[tile.block + 1];
@@ -537,131 +542,165 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
   int n_steps = 0;
   for (int i = 0; i < nt; ++i) n_steps += s_meta[i].ak / DK;
 
-  const char* __restrict__ pa = p.a;
-  const char* __restrict__ pb = p.b;
-  const char* __restrict__ pb2 = p.b2;
-  // issue the direct loads of K step (tuple i of the unit, offset k0) into a stage
-  auto issue = [&](int i, int k0, uint16_t* sa, uint16_t* sb) {
-    const TupleMeta& m = s_meta[i];
-    {  // A: 256 rows x 32 k; wave instruction q covers 16 rows
-      const char* base = pa + m.aoff;
-      const int mext = m.am, kext = m.ak;
+  // ---- direct-load walk over the unit's K steps.  Each lane keeps one source
+  // pointer per load instruction for the current tuple; a K step advances
+  // them by a uniform stride.  Rows (A, [n][k] B) or columns ([k][n] B) past a
+  // block's edge read row 0 / column 0 of the block instead, which stays in
+  // bounds for every K step of the block.
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t*)smem;
+  const char* ga[LA];
+  const char* gbp[NB][LBO];
+  int64_t bstep[NB];
+  int it_t = 0, left = 0;
+  auto set_tuple = [&](int t) {
+    const TupleMeta& m = s_meta[t];
 #pragma unroll
-      for (int q = 0; q < LA; ++q) {
-        const int r = (wid * LA + q) * 16 + (lane >> 2);
-        const int c = (lane & 3) ^ swz_row(r);
-        const int gm = tile.m0 + r;
-        const int64_t off = gm < mext ? ((int64_t)gm * kext + k0 + 8 * c) * 2 : 0;
-        dl_load16(base + off, sa + (wid * LA + q) * 512);
-      }
+    for (int q = 0; q < LA; ++q) {
+      const int r = (wid * LA + q) * 16 + (lane >> 2);
+      const int c = (lane & 3) ^ swz_row(r);
+      const int gm = tile.m0 + r;
+      ga[q] = p.a + m.aoff + ((gm < m.am ? (int64_t)gm * m.ak : 0) + 8 * c) * 2;
     }
 #pragma unroll
     for (int o = 0; o < NB; ++o) {
-      const char* base = (o == 0 ? pb + m.boff : pb2 + m.b2off);
+      const char* base = o == 0 ? p.b + m.boff : p.b2 + m.b2off;
       const int e0 = o == 0 ? m.b0 : m.b20, e1 = o == 0 ? m.b1 : m.b21;
-      uint16_t* sbo = sb + o * BN * DK;
-      if constexpr (KMAJOR) {  // [n][k]: like A, BN rows of 32 k
+      if constexpr (KMAJOR) {  // [n][k]: like A, BN rows of DK k
 #pragma unroll
-        for (int q = 0; q < LB / NB; ++q) {
-          const int r = (wid * (LB / NB) + q) * 16 + (lane >> 2);
+        for (int q = 0; q < LBO; ++q) {
+          const int r = (wid * LBO + q) * 16 + (lane >> 2);
           const int c = (lane & 3) ^ swz_row(r);
           const int gn = tile.n0 + r;
-          const int64_t off = gn < e0 ? ((int64_t)gn * e1 + k0 + 8 * c) * 2 : 0;
-          dl_load16(base + off, sbo + (wid * (LB / NB) + q) * 512);
+          gbp[o][q] = base + ((gn < e0 ? (int64_t)gn * e1 : 0) + 8 * c) * 2;
         }
-      } else {  // [k][n]: 32 rows of BN columns; wave instruction covers 1024 / ROWB rows
-        constexpr int RPI = 1024 / ROWB;
-        constexpr int CPR = ROWB / 16;  // chunks per row
+        bstep[o] = DK * 2;
+      } else {  // [k][n]: DK rows of BN columns
 #pragma unroll
-        for (int q = 0; q < LB / NB; ++q) {
-          const int inst = wid * (LB / NB) + q;
-          const int k = inst * RPI + lane / CPR;
+        for (int q = 0; q < LBO; ++q) {
+          const int k = (wid * LBO + q) * RPI + lane / CPR;
           const int c = (lane % CPR) ^ swz_k(k);
           const int gn = tile.n0 + 8 * c;
-          const int64_t off = gn < e1 ? ((int64_t)(k0 + k) * e1 + gn) * 2 : 0;
-          dl_load16(base + off, sbo + inst * 512);
+          gbp[o][q] = base + ((int64_t)k * e1 + (gn < e1 ? gn : 0)) * 2;
         }
+        bstep[o] = (int64_t)DK * e1 * 2;
       }
     }
+    left = m.ak / DK;
   };
-  // walk of the K steps: (tuple of the unit, offset) advanced by DK
-  int it_t = 0, it_k = 0;
-  auto next_step = [&]() {
-    it_k += DK;
-    if (it_k >= s_meta[it_t].ak) {
+  auto seek = [&]() {  // first tuple at or after it_t with a K step
+    while (it_t < nt && s_meta[it_t].ak < DK) ++it_t;
+    if (it_t < nt) set_tuple(it_t);
+  };
+  // issue the loads of the next K step of the walk into stage u
+  auto issue_next = [&](int u) {
+    const uint32_t sbase = lds_base + (uint32_t)(u * STAGE * 2);
+#pragma unroll
+    for (int q = 0; q < LA; ++q) {
+      dl_load16(ga[q], sbase + (uint32_t)((wid * LA + q) * 1024));
+      ga[q] += DK * 2;
+    }
+#pragma unroll
+    for (int o = 0; o < NB; ++o)
+#pragma unroll
+      for (int q = 0; q < LBO; ++q) {
+        dl_load16(gbp[o][q], sbase + (uint32_t)(A_ELEMS * 2 + o * B_ELEMS * 2 + (wid * LBO + q) * 1024));
+        gbp[o][q] += bstep[o];
+      }
+    if (--left == 0) {
       ++it_t;
-      it_k = 0;
+      seek();
     }
   };
-  uint16_t* const sAs[NSTAGE] = {sA0, sA1, sA2, sA3};
-  uint16_t* const sBs[NSTAGE] = {sB0, sB1, sB2, sB3};
 
-  auto compute = [&](const uint16_t* sa, const uint16_t* sb) {
+  // ---- MFMA operands of one 16-deep half of a stage
+  struct Frag {
+    uint4 a[4];
+    uint4 b[NB][WN];
+  };
+  auto load_frag = [&](Frag& f, int u, int s) {
+    const uint16_t* sa = smem + u * STAGE;
 #pragma unroll
-    for (int s = 0; s < DK / 16; ++s) {
-      uint4 af[4], bf[NB][WN];
+    for (int i = 0; i < 4; ++i) {
+      const int r = wm * 128 + i * 32 + lq;
+      const int c = (2 * s + g) ^ swz_row(r);
+      f.a[i] = *reinterpret_cast<const uint4*>(sa + r * DK + 8 * c);
+    }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = wm * 128 + i * 32 + lq;
-        const int c = (2 * s + g) ^ swz_row(r);
-        af[i] = *reinterpret_cast<const uint4*>(sa + r * DK + 8 * c);
-      }
+    for (int o = 0; o < NB; ++o)
 #pragma unroll
-      for (int o = 0; o < NB; ++o)
+      for (int j = 0; j < WN; ++j) {
+        const uint16_t* sbo = sa + A_ELEMS + o * B_ELEMS;
+        if constexpr (KMAJOR) {
+          const int r = wn * WCOLS + j * 32 + lq;
+          const int c = (2 * s + g) ^ swz_row(r);
+          f.b[o][j] = *reinterpret_cast<const uint4*>(sbo + r * DK + 8 * c);
+        } else {
+          const int gq = lane >> 4, li = lane & 15;
+          const int n = wn * WCOLS + j * 32 + 16 * (gq & 1) + 4 * (li & 3);
+          uint2 h2[2];
 #pragma unroll
-        for (int j = 0; j < WN; ++j) {
-          const uint16_t* sbo = sb + o * BN * DK;
-          if constexpr (KMAJOR) {
-            const int r = wn * WCOLS + j * 32 + lq;
-            const int c = (2 * s + g) ^ swz_row(r);
-            bf[o][j] = *reinterpret_cast<const uint4*>(sbo + r * DK + 8 * c);
-          } else {
-            const int gq = lane >> 4, li = lane & 15;
-            const int n = wn * WCOLS + j * 32 + 16 * (gq & 1) + 4 * (li & 3);
-            uint2 h2[2];
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-              const int k = 16 * s + 8 * (gq >> 1) + 4 * h + (li >> 2);
-              const int c = (n >> 3) ^ swz_k(k);
-              h2[h] = tr_read(sbo + k * BN + 8 * c + (n & 4));
-            }
-            bf[o][j] = make_uint4(h2[0].x, h2[0].y, h2[1].x, h2[1].y);
+          for (int h = 0; h < 2; ++h) {
+            const int k = 16 * s + 8 * (gq >> 1) + 4 * h + (li >> 2);
+            const int c = (n >> 3) ^ swz_k(k);
+            h2[h] = tr_read(sbo + k * BN + 8 * c + (n & 4));
           }
+          f.b[o][j] = make_uint4(h2[0].x, h2[0].y, h2[1].x, h2[1].y);
         }
+      }
+  };
+  auto mma = [&](const Frag& f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int o = 0; o < NB; ++o)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < WN; ++j) acc[o][i][j] = mfma<BF16>(af[i], bf[o][j], acc[o][i][j]);
-    }
+        for (int j = 0; j < WN; ++j) acc[o][i][j] = mfma<BF16>(f.a[i], f.b[o][j], acc[o][i][j]);
   };
 
-  // prologue: steps 0..2 in flight
+  // ---- pipeline: all four stages in flight at the start.  In step st the
+  // first half's MFMAs run while the second half's operands are read; then
+  // (after step st+1's loads have landed and every wave has read stage st)
+  // stage st is refilled with step st+4 and the next step's first half is
+  // read while the second half's MFMAs run.
+  seek();
 #pragma unroll
-  for (int st = 0; st < NSTAGE - 1; ++st)
-    if (st < n_steps) {
-      issue(it_t, it_k, sAs[st], sBs[st]);
-      next_step();
-    }
-  // main loop, unrolled by the stage count so that stage buffers are static
-  for (int base = 0; base < n_steps; base += NSTAGE) {
+  for (int st = 0; st < NSTAGE; ++st)
+    if (st < n_steps) issue_next(st);
+  Frag f0, f1;
+  if (n_steps > 0) {
+    if (n_steps > 3) wait_vmcnt<3 * LS>();
+    else if (n_steps == 3) wait_vmcnt<2 * LS>();
+    else if (n_steps == 2) wait_vmcnt<LS>();
+    else wait_vmcnt<0>();
+    stage_barrier();
+    load_frag(f0, 0, 0);
+  }
+  // every step but the last (peeled below, it has no successor to wait for)
+  const int last = n_steps - 1;
+  for (int base = 0; base < last; base += NSTAGE) {
 #pragma unroll
     for (int u = 0; u < NSTAGE; ++u) {
       const int st = base + u;
-      if (st < n_steps) {
-        // loads of step st are done once at most those of st+1, st+2 are pending
-        if (st + 2 < n_steps) wait_vmcnt<2 * LS>();
-        else if (st + 1 < n_steps) wait_vmcnt<LS>();
+      if (st < last) {
+        load_frag(f1, u, 1);
+        __builtin_amdgcn_sched_barrier(0);  // operand reads go out before the MFMAs
+        mma(f0);
+        // loads of step st+1 are done once at most those of st+2, st+3 are pending
+        if (st + 3 < n_steps) wait_vmcnt<2 * LS>();
+        else if (st + 2 < n_steps) wait_vmcnt<LS>();
         else wait_vmcnt<0>();
         stage_barrier();
-        if (st + NSTAGE - 1 < n_steps) {  // refill the stage computed one step ago
-          issue(it_t, it_k, sAs[(u + NSTAGE - 1) % NSTAGE], sBs[(u + NSTAGE - 1) % NSTAGE]);
-          next_step();
-        }
-        compute(sAs[u], sBs[u]);
+        if (st + NSTAGE < n_steps) issue_next(u);
+        load_frag(f0, (u + 1) % NSTAGE, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(f1);
       }
     }
+  }
+  if (n_steps > 0) {
+    load_frag(f1, last % NSTAGE, 1);
+    mma(f0);
+    mma(f1);
   }
   finish_tile<SWIGLU, NB, WN, W>(acc, p, tile, wid, lane, tile.m0 + wm * 128 + 4 * g, tile.n0 + wn * WCOLS + lq);
 }
