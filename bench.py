@@ -1,6 +1,6 @@
 """Throughput of one GPU's share of the block join-agg hot path on MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload block|qkv|attention|reductions]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload block|qkv|attention|reductions|repartition]
 
 Default workload "block": one GPU's share of a LLaMA-65B-shape transformer
 block (hidden 8192, 8 of 64 heads of dim 128, SwiGLU FFN 2752 = 22016/8,
@@ -17,7 +17,8 @@ Other workloads (not the default line): "qkv" = the LLaMA-7B QKV projection
 share 'tj,jk->tk' 4096x4096x1536 in 512x512 blocks plus its repartition to
 per-head 4096x128 blocks; "attention" = causal attention B2 H4 S2048 D128;
 "reductions" = RMSNorm over x[4096, 4096] in 8 column blocks and causal
-softmax over s[4, 2048, 2048] in 256-key blocks.
+softmax over s[4, 2048, 2048] in 256-key blocks; "repartition" = a 256 MiB
+bf16 relation re-blocked from 512x512 to 128-row blocks (a pure copy).
 
 Prints one JSON line.
 """
@@ -53,6 +54,30 @@ def _events_ms(fn, n, warm=3):
     e.record()
     e.synchronize()
     return s.elapsed_time(e) / n
+
+
+def _profiled_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from its committed counter summary
+    (profiles/<kernel>_traffic.txt: FETCH_SIZE and WRITE_SIZE per dispatch,
+    scaled by the readings of a copy of known size), or None when there is no
+    summary or the kernel's sources have changed since it was taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"{kernel}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for line in open(path):
+        k, sep, v = line.partition(":")
+        if sep and " " not in k.strip():
+            rec[k.strip()] = v.strip()
+    h = hashlib.sha256()
+    for src in ("ea_gemm.hip", "ea_host.cpp", "ea_internal.h"):
+        with open(os.path.join(ROOT, "paper_2609_03905_amd", "csrc", src), "rb") as f:
+            h.update(f.read())
+    if rec.get("kernel_source_sha256") != h.hexdigest() or "traffic_bytes" not in rec:
+        return None
+    return float(rec["traffic_bytes"])
 
 
 def _dev(a):
@@ -148,6 +173,31 @@ def reductions_workload():
                         "softmax": "s[4,2048,2048] bf16 causal, 256-key blocks", "dtype": "bf16"}, cpu=None)
 
 
+def repartition_workload():
+    """Local repartition at HBM scale: a [8192, 16384] bf16 relation (256 MiB,
+    larger than the 256 MB Infinity Cache) re-blocked from 512x512 blocks to
+    128-row blocks of full width.  A pure copy with a known byte count; its
+    FETCH_SIZE / WRITE_SIZE readings are the scale factor for counter-derived
+    traffic of the other kernels."""
+    import torch
+
+    import synth
+    from paper_2609_03905_amd import ea
+
+    shape = (8192, 16384)
+    src = ea.Relation(shape, "bf16", [synth.splits(8192, 512), synth.splits(16384, 512)])
+    dst = ea.Relation(shape, "bf16", [synth.splits(8192, 128), synth.whole(16384)])
+    g = torch.Generator(device="cuda")
+    g.manual_seed(601)
+    src.bytes().copy_(torch.randint(0, 256, (src.nbytes,), dtype=torch.uint8, device="cuda", generator=g))
+    fn = lambda: ea.repartition(src, dst)
+    nbytes = 2 * shape[0] * shape[1] * 2
+    return dict(step=fn, flops=0.0, bytes=nbytes, comps={"repartition": dict(fn=fn, bytes=nbytes)},
+                dominant="repartition",
+                config={"workload": "repartition_256MiB", "shape": list(shape), "dtype": "bf16",
+                        "from": "512x512 blocks", "to": "128 x 16384 blocks"}, cpu=None)
+
+
 # ---------------------------------------------------------------------------
 # CPU baselines: the oracle, untuned, on a bounded sample of the workload
 # ---------------------------------------------------------------------------
@@ -191,7 +241,7 @@ def cpu_baseline_qkv(target_s: float = 12.0):
 
 
 WORKLOADS = {"block": block_workload, "qkv": qkv_workload, "attention": attention_workload,
-             "reductions": reductions_workload}
+             "reductions": reductions_workload, "repartition": repartition_workload}
 
 
 def main():
@@ -241,7 +291,7 @@ def main():
     if "flops" in dom:
         achieved = dom["flops"] / dms / 1e9
         roof = {"kernel": wl["dominant"], "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None}
+                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": _profiled_traffic(wl["dominant"])}
     else:
         achieved = dom["bytes"] / dms / 1e6
         roof = {"kernel": wl["dominant"], "bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS,
