@@ -263,25 +263,24 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int d = 32 * dt + 8 * rr + 4 * g;
-        *reinterpret_cast<float4*>(po + rt * D + d) =
-            make_float4(acc_o[dt][4 * rr], acc_o[dt][4 * rr + 1], acc_o[dt][4 * rr + 2], acc_o[dt][4 * rr + 3]);
+        store_agent2(po + rt * D + d, acc_o[dt][4 * rr], acc_o[dt][4 * rr + 1]);
+        store_agent2(po + rt * D + d + 2, acc_o[dt][4 * rr + 2], acc_o[dt][4 * rr + 3]);
       }
-    if (g == 0) *reinterpret_cast<float2*>(p.part_ml + ((int64_t)u.slot * 128 + rt) * 2) = make_float2(m, l);
+    if (g == 0) store_agent2(p.part_ml + ((int64_t)u.slot * 128 + rt) * 2, m, l);
   }
-  __threadfence();
+  drain_vmem();
   __syncthreads();
-  if (tid == 0) s_last = atomicAdd(p.counters + u.counter, 1) == u.n_parts - 1;
+  if (tid == 0) s_last = arrive_agent(p.counters + u.counter) == u.n_parts - 1;
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
   {
     const int rt = tid >> 1, dlo = (tid & 1) * 64;
     float M = -INFINITY;
-    for (int q = 0; q < u.n_parts; ++q) M = fmaxf(M, p.part_ml[((int64_t)(u.first_slot + q) * 128 + rt) * 2]);
+    for (int q = 0; q < u.n_parts; ++q) M = fmaxf(M, load_agent(p.part_ml + ((int64_t)(u.first_slot + q) * 128 + rt) * 2));
     const float Mu = M == -INFINITY ? 0.0f : M;
     float L = 0.0f;
     for (int q = 0; q < u.n_parts; ++q) {
-      const float2 ml = *reinterpret_cast<const float2*>(p.part_ml + ((int64_t)(u.first_slot + q) * 128 + rt) * 2);
+      const float2 ml = load_agent2(p.part_ml + ((int64_t)(u.first_slot + q) * 128 + rt) * 2);
       L += ml.y * exp2f(ml.x - Mu);
     }
     const float inv = L > 0.0f ? 1.0f / L : 0.0f;
@@ -291,12 +290,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
       float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int q = 0; q < u.n_parts; ++q) {
         const int64_t sl = u.first_slot + q;
-        const float w = exp2f(p.part_ml[(sl * 128 + rt) * 2] - Mu);
-        const float4 v = *reinterpret_cast<const float4*>(p.part_o + (sl * 128 + rt) * D + d);
-        acc.x += v.x * w;
-        acc.y += v.y * w;
-        acc.z += v.z * w;
-        acc.w += v.w * w;
+        const float w = exp2f(load_agent(p.part_ml + (sl * 128 + rt) * 2) - Mu);
+        const float2 v0 = load_agent2(p.part_o + (sl * 128 + rt) * D + d);
+        const float2 v1 = load_agent2(p.part_o + (sl * 128 + rt) * D + d + 2);
+        acc.x += v0.x * w;
+        acc.y += v0.y * w;
+        acc.z += v1.x * w;
+        acc.w += v1.y * w;
       }
       const float o0 = acc.x * inv, o1 = acc.y * inv, o2 = acc.z * inv, o3 = acc.w * inv;
       if (p.dt_o == EA_BF16) {
@@ -309,7 +309,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
       }
     }
   }
-  if (tid == 0) p.counters[u.counter] = 0;  // ready for the next call (stream-ordered)
+  if (tid == 0) reset_agent(p.counters + u.counter);  // ready for the next call (stream-ordered)
 }
 
 }  // namespace

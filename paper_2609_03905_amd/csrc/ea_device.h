@@ -46,6 +46,41 @@ __device__ __forceinline__ T ld_uniform(const T* p) {
 #endif
 }
 
+// ---- hand-off between workgroups through global memory ------------------
+// The eight XCDs' L2 caches are not coherent with each other.  Agent-scope
+// relaxed atomic loads and stores are (they carry the coherence bits), so
+// partial results passed from one workgroup to another use them, and no
+// device-scope fence -- which would write back and invalidate the whole L2 of
+// the XCD, evicting every co-resident workgroup's operands -- is needed.  The
+// writer drains its stores (vmcnt 0) before it counts its arrival; the reader
+// issues its loads only after its own arrival count has returned.
+__device__ __forceinline__ void store_agent2(float* p, float a, float b) {
+  const uint64_t v = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ float2 load_agent2(const float* p) {
+  const uint64_t v =
+      __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
+}
+
+__device__ __forceinline__ float load_agent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// every outstanding vector-memory access of this wave completed (vmcnt 0)
+__device__ __forceinline__ void drain_vmem() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
+
+// arrival count of a split key; returns the count before this arrival
+__device__ __forceinline__ int arrive_agent(int32_t* counter) {
+  return __hip_atomic_fetch_add(counter, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void reset_agent(int32_t* counter) {
+  __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Load/store one element of a relation given its dtype.
 __device__ __forceinline__ float ld_elem(const char* base, int64_t idx, int dt) {
   if (dt == EA_F32) return reinterpret_cast<const float*>(base)[idx];

@@ -14,15 +14,21 @@
 // 512 threads = 8 waves in a 2 (rows) x 4 (columns) grid, two waves per SIMD
 // so that one wave's LDS reads overlap the other's MFMAs.  Tile 256 x 256
 // (each wave 128 x 64: 4 x 2 MFMA tiles, 128 accumulators), or for SwiGLU
-// 256 x 128 with two right operands (each wave 128 x 32 per operand).  K step
-// 64, LDS double-buffered (2 x 72 KiB, rows padded to 72 elements:
-// conflict-free fragment reads); global loads run two K steps ahead of the
-// MFMAs (two register stages).  A right operand stored [k][n] is transposed
-// in registers (4 k x 8 n per thread) before the LDS write, so both operands
-// read 16 contiguous bytes per lane.
+// 256 x 128 with two right operands (each wave 128 x 32 per operand).
 //
-// Epilogues: residual relation added before the store; SwiGLU stores
-// silu(g) * u from its two accumulators.
+// Two K pipelines share the tile layout and the epilogue:
+//   * gemm_dl_kernel (every contracted block extent a multiple of 32): operands
+//     go straight from global memory into LDS (global_load_lds_dwordx4), four
+//     stages of 32-deep K steps in flight, XOR-swizzled LDS chunks, [k][n]
+//     right operands read with transposing LDS reads (description below);
+//   * gemm_kernel (any 8-aligned extents): register-staged loads two K steps
+//     ahead, K step 64, LDS double-buffered with padded rows; a right operand
+//     stored [k][n] is transposed in registers before the LDS write.
+//
+// Epilogue: the tile is staged through LDS so that stores (and the residual
+// loads) are 16-byte row chunks; the residual is added in fp32 before the one
+// rounding to the output dtype; SwiGLU stores silu(g) * u of its two
+// accumulators.
 #include "ea_device.h"
 
 namespace ea {
@@ -166,37 +172,85 @@ struct EpiArgs {
   char* c;          // output block base
   const char* res;  // residual block base (same layout and dtype) or null
   int mext, next;   // output block extents
-  int row0, col0;   // this lane's first row and column
+  int m0, n0;       // tile origin inside the block
 };
 
-// Accumulator r of MFMA tile (i, j) in lane l holds row 8*(r/4) + 4*(l/32) +
-// r%4 and column l%32 of that 32x32 tile (row0/col0 carry the lane parts).
-template <bool SWIGLU, int NB, int WN, int DT, bool RES>
-__device__ __forceinline__ void epilogue(const f32x16_t (&acc)[NB][4][WN], const EpiArgs& e) {
-#pragma clang loop unroll(full)
-  for (int i = 0; i < 4; ++i)
-#pragma clang loop unroll(full)
+// Epilogue through LDS.  Accumulator r of MFMA tile (i, j) in lane l holds
+// row 8*(r/4) + 4*(l/32) + r%4 and column l%32 of that 32x32 tile, so a lane
+// owns scattered 2-byte outputs.  The tile's values (SwiGLU: silu(g) * u) are
+// therefore staged in LDS, in four passes of 64 rows (MFMA row-tile i of every
+// wave), fp32 with a row pitch of kEpiPitch floats; then each thread takes 8
+// consecutive columns of one row and stores them with one 16-byte access (two
+// for fp32), reading the residual the same way.  Block rows are multiples of
+// 8 elements on this path (host guarantee), so a chunk never straddles a row.
+constexpr int kEpiPitch = 264;  // 256 + 8: rows 4 apart land on opposite halves of the 64 banks
+
+template <bool SWIGLU, int NB, int WN, int W, int DT, bool RES>
+__device__ __forceinline__ void epilogue(const f32x16_t (&acc)[NB][4][WN], const EpiArgs& e, float* stage,
+                                         int wid, int lane) {
+  constexpr int WGN = W / 2;            // waves along n (2 along m)
+  constexpr int WCOLS = WN * 32;        // columns per wave
+  constexpr int CPR = WGN * WCOLS / 8;  // 8-column chunks per tile row
+  constexpr int CHUNKS = CPR / W;       // chunks per thread per pass (64 rows)
+  static_assert(CPR % W == 0, "epilogue chunking");
+  const int wm = wid / WGN, wn = wid % WGN, g = lane >> 5, lq = lane & 31;
+  const int tid = wid * 64 + lane;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    __syncthreads();  // the stage area is free (K loop or previous pass done)
+#pragma unroll
     for (int j = 0; j < WN; ++j)
-#pragma clang loop unroll(full)
+#pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int gm = e.row0 + i * 32 + 8 * (r >> 2) + (r & 3);
-        const int gn = e.col0 + j * 32;
-        if (gm < e.mext && gn < e.next) {
-          float v = acc[0][i][j][r];
-          if constexpr (SWIGLU) v = v / (1.0f + __expf(-v)) * acc[NB - 1][i][j][r];
-          const int64_t idx = (int64_t)gm * e.next + gn;
-          if constexpr (DT == EA_F32) {
-            if constexpr (RES) v += reinterpret_cast<const float*>(e.res)[idx];
-            reinterpret_cast<float*>(e.c)[idx] = v;
-          } else if constexpr (DT == EA_BF16) {
-            if constexpr (RES) v += bf16_to_f32(reinterpret_cast<const uint16_t*>(e.res)[idx]);
-            reinterpret_cast<uint16_t*>(e.c)[idx] = f32_to_bf16(v);
-          } else {
-            if constexpr (RES) v += f16_to_f32(reinterpret_cast<const uint16_t*>(e.res)[idx]);
-            reinterpret_cast<uint16_t*>(e.c)[idx] = f32_to_f16(v);
+        float v = acc[0][i][j][r];
+        if constexpr (SWIGLU) v = v / (1.0f + __expf(-v)) * acc[NB - 1][i][j][r];
+        const int row = wm * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+        stage[row * kEpiPitch + wn * WCOLS + 32 * j + lq] = v;
+      }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < CHUNKS; ++k) {
+      const int c = tid + 64 * W * k;
+      const int row = c / CPR, c8 = c % CPR;
+      const int gm = e.m0 + (row >> 5) * 128 + 32 * i + (row & 31);
+      const int gn = e.n0 + 8 * c8;
+      if (gm < e.mext && gn < e.next) {
+        const float4 lo = *reinterpret_cast<const float4*>(stage + row * kEpiPitch + 8 * c8);
+        const float4 hi = *reinterpret_cast<const float4*>(stage + row * kEpiPitch + 8 * c8 + 4);
+        float o[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        const int64_t idx = (int64_t)gm * e.next + gn;
+        if constexpr (DT == EA_F32) {
+          if constexpr (RES) {
+            const float4 r0 = *reinterpret_cast<const float4*>(e.res + idx * 4);
+            const float4 r1 = *reinterpret_cast<const float4*>(e.res + idx * 4 + 16);
+            o[0] += r0.x; o[1] += r0.y; o[2] += r0.z; o[3] += r0.w;
+            o[4] += r1.x; o[5] += r1.y; o[6] += r1.z; o[7] += r1.w;
           }
+          *reinterpret_cast<float4*>(e.c + idx * 4) = make_float4(o[0], o[1], o[2], o[3]);
+          *reinterpret_cast<float4*>(e.c + idx * 4 + 16) = make_float4(o[4], o[5], o[6], o[7]);
+        } else {
+          if constexpr (RES) {
+            const uint4 rv = *reinterpret_cast<const uint4*>(e.res + idx * 2);
+            const uint32_t w[4] = {rv.x, rv.y, rv.z, rv.w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const uint16_t h0 = (uint16_t)(w[q] & 0xffffu), h1 = (uint16_t)(w[q] >> 16);
+              o[2 * q] += DT == EA_BF16 ? bf16_to_f32(h0) : f16_to_f32(h0);
+              o[2 * q + 1] += DT == EA_BF16 ? bf16_to_f32(h1) : f16_to_f32(h1);
+            }
+          }
+          uint32_t w[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const uint32_t h0 = DT == EA_BF16 ? f32_to_bf16(o[2 * q]) : f32_to_f16(o[2 * q]);
+            const uint32_t h1 = DT == EA_BF16 ? f32_to_bf16(o[2 * q + 1]) : f32_to_f16(o[2 * q + 1]);
+            w[q] = h0 | (h1 << 16);
+          }
+          *reinterpret_cast<uint4*>(e.c + idx * 2) = make_uint4(w[0], w[1], w[2], w[3]);
         }
       }
+    }
+  }
 }
 
 // Position of a K step: tuple index and offset inside its contracted block.
@@ -211,7 +265,7 @@ struct KStep {
 // Then the epilogue, with dtype and residual decided outside its unrolled loops.
 template <bool SWIGLU, int NB, int WN, int W>
 __device__ __forceinline__ void finish_tile(f32x16_t (&acc)[NB][4][WN], const GemmArgs& p, const GemmTile& tile,
-                                            int wid, int lane, int row0, int col0) {
+                                            int wid, int lane, float* stage) {
   __shared__ int s_last;
   const int tid = wid * 64 + lane;
   if (tile.n_parts > 1) {
@@ -226,16 +280,15 @@ __device__ __forceinline__ void finish_tile(f32x16_t (&acc)[NB][4][WN], const Ge
 #pragma unroll
           for (int r4 = 0; r4 < 4; ++r4) {
             const int q = ((o * 4 + i) * WN + j) * 4 + r4;
-            *reinterpret_cast<float4*>(mine + ((int64_t)q * 64 + lane) * 4) =
-                make_float4(acc[o][i][j][4 * r4], acc[o][i][j][4 * r4 + 1], acc[o][i][j][4 * r4 + 2],
-                            acc[o][i][j][4 * r4 + 3]);
+            float* dst = mine + ((int64_t)q * 64 + lane) * 4;
+            store_agent2(dst, acc[o][i][j][4 * r4], acc[o][i][j][4 * r4 + 1]);
+            store_agent2(dst + 2, acc[o][i][j][4 * r4 + 2], acc[o][i][j][4 * r4 + 3]);
           }
-    __threadfence();
+    drain_vmem();
     __syncthreads();
-    if (tid == 0) s_last = atomicAdd(p.counters + tile.counter, 1) == tile.n_parts - 1;
+    if (tid == 0) s_last = arrive_agent(p.counters + tile.counter) == tile.n_parts - 1;
     __syncthreads();
     if (!s_last) return;
-    __threadfence();
 #pragma unroll
     for (int o = 0; o < NB; ++o)
 #pragma unroll
@@ -253,23 +306,24 @@ __device__ __forceinline__ void finish_tile(f32x16_t (&acc)[NB][4][WN], const Ge
 #pragma unroll
             for (int r4 = 0; r4 < 4; ++r4) {
               const int q = ((o * 4 + i) * WN + j) * 4 + r4;
-              const float4 v = *reinterpret_cast<const float4*>(src + ((int64_t)q * 64 + lane) * 4);
-              acc[o][i][j][4 * r4] += v.x;
-              acc[o][i][j][4 * r4 + 1] += v.y;
-              acc[o][i][j][4 * r4 + 2] += v.z;
-              acc[o][i][j][4 * r4 + 3] += v.w;
+              const float2 v0 = load_agent2(src + ((int64_t)q * 64 + lane) * 4);
+              const float2 v1 = load_agent2(src + ((int64_t)q * 64 + lane) * 4 + 2);
+              acc[o][i][j][4 * r4] += v0.x;
+              acc[o][i][j][4 * r4 + 1] += v0.y;
+              acc[o][i][j][4 * r4 + 2] += v1.x;
+              acc[o][i][j][4 * r4 + 3] += v1.y;
             }
     }
-    if (tid == 0) p.counters[tile.counter] = 0;  // ready for the next call (stream-ordered)
+    if (tid == 0) reset_agent(p.counters + tile.counter);  // ready for the next call (stream-ordered)
   }
   const DevBlk& cb = p.blk_c[tile.block];
-  const EpiArgs e{p.c + cb.off, p.res ? p.res + cb.off : nullptr, cb.ext[0], cb.ext[1], row0, col0};
-  if (!e.res && p.dt_out == EA_BF16) epilogue<SWIGLU, NB, WN, EA_BF16, false>(acc, e);
-  else if (!e.res && p.dt_out == EA_F32) epilogue<SWIGLU, NB, WN, EA_F32, false>(acc, e);
-  else if (p.dt_out == EA_BF16) epilogue<SWIGLU, NB, WN, EA_BF16, true>(acc, e);
-  else if (p.dt_out == EA_F32) epilogue<SWIGLU, NB, WN, EA_F32, true>(acc, e);
-  else if (!e.res) epilogue<SWIGLU, NB, WN, EA_F16, false>(acc, e);
-  else epilogue<SWIGLU, NB, WN, EA_F16, true>(acc, e);
+  const EpiArgs e{p.c + cb.off, p.res ? p.res + cb.off : nullptr, cb.ext[0], cb.ext[1], tile.m0, tile.n0};
+  if (!e.res && p.dt_out == EA_BF16) epilogue<SWIGLU, NB, WN, W, EA_BF16, false>(acc, e, stage, wid, lane);
+  else if (!e.res && p.dt_out == EA_F32) epilogue<SWIGLU, NB, WN, W, EA_F32, false>(acc, e, stage, wid, lane);
+  else if (p.dt_out == EA_BF16) epilogue<SWIGLU, NB, WN, W, EA_BF16, true>(acc, e, stage, wid, lane);
+  else if (p.dt_out == EA_F32) epilogue<SWIGLU, NB, WN, W, EA_F32, true>(acc, e, stage, wid, lane);
+  else if (!e.res) epilogue<SWIGLU, NB, WN, W, EA_F16, false>(acc, e, stage, wid, lane);
+  else epilogue<SWIGLU, NB, WN, W, EA_F16, true>(acc, e, stage, wid, lane);
 }
 
 template <bool BF16, bool KMAJOR, bool SWIGLU, int W>
@@ -387,7 +441,8 @@ __global__ __launch_bounds__(W * 64, 1) void gemm_kernel(const GemmArgs p) {
     }
   }
 
-  finish_tile<SWIGLU, NB, WN, W>(acc, p, tile, wid, lane, tile.m0 + wm * 128 + 4 * g, tile.n0 + wn * WCOLS + lq);
+  static_assert(sizeof(sA) >= 64 * kEpiPitch * sizeof(float), "epilogue stage");
+  finish_tile<SWIGLU, NB, WN, W>(acc, p, tile, wid, lane, reinterpret_cast<float*>(&sA[0][0]));
 }
 
 // ===========================================================================
@@ -702,14 +757,13 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
     mma(f0);
     mma(f1);
   }
-  finish_tile<SWIGLU, NB, WN, W>(acc, p, tile, wid, lane, tile.m0 + wm * 128 + 4 * g, tile.n0 + wn * WCOLS + lq);
+  static_assert(sizeof(smem) >= 64 * kEpiPitch * sizeof(float), "epilogue stage");
+  finish_tile<SWIGLU, NB, WN, W>(acc, p, tile, wid, lane, reinterpret_cast<float*>(smem));
 }
 
 template <bool BF16, bool KMAJOR, bool SWIGLU>
 hipError_t launch3(const GemmArgs& a, hipStream_t s) {
-  if (a.direct && a.waves == 4)
-    hipLaunchKernelGGL((gemm_dl_kernel<BF16, KMAJOR, SWIGLU, 4>), dim3((uint32_t)a.n_tiles), dim3(256), 0, s, a);
-  else if (a.direct)
+  if (a.direct)
     hipLaunchKernelGGL((gemm_dl_kernel<BF16, KMAJOR, SWIGLU, 8>), dim3((uint32_t)a.n_tiles), dim3(512), 0, s, a);
   else
     hipLaunchKernelGGL((gemm_kernel<BF16, KMAJOR, SWIGLU, 8>), dim3((uint32_t)a.n_tiles), dim3(512), 0, s, a);

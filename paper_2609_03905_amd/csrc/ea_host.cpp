@@ -314,6 +314,7 @@ struct Plan {
   // rows
   int32_t row_len = 0;
   int32_t row_vec = 0;
+  int32_t row_cps = 0;
   // attention scratch
   float* part_o = nullptr;
   float* part_ml = nullptr;
@@ -476,8 +477,11 @@ int classify(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation*
         if (L1[0] == b && L1[1] != a && L1[1] != b) { kmaj = 0; c = L1[1]; }
         else if (L1[1] == b && L1[0] != a && L1[0] != b) { kmaj = 1; c = L1[0]; }
         if (kmaj >= 0 && L2[0] == a && L2[1] == c) {
-          bool aligned = true;  // 16-byte vector loads need 8-element-aligned rows
+          // 16-byte vector loads and stores need 8-element-aligned block rows:
+          // the contracted letter in both operands and the output columns
+          bool aligned = true;
           for (int64_t v : ops[0]->splits[1]) aligned &= v % 8 == 0;
+          for (int64_t v : ops[1]->splits[0]) aligned &= v % 8 == 0;
           for (int64_t v : ops[1]->splits[1]) aligned &= v % 8 == 0;
           if (aligned) {
             oi->kind = K_GEMM;
@@ -744,7 +748,7 @@ GemmPlanInfo gemm_units(const ea_relation* a, const ea_relation* c, int tn) {
 }
 
 int build_rows(const Spec& sp, const ea_relation* const* ops, const OpInfo& oi, Image* img, Extra* ex,
-               int32_t* row_len, int32_t* vec) {
+               int32_t* row_len, int32_t* vec, int32_t* seg_chunks) {
   // rows of a group: points of the group letters' box; every group has the
   // same structure as block (g) of the output restricted to the group letters.
   const ea_relation* y = ops[sp.n_in];
@@ -773,6 +777,14 @@ int build_rows(const Spec& sp, const ea_relation* const* ops, const OpInfo& oi, 
   bool aligned = true;
   for (int b = 0; b < x->nb[r - 1]; ++b) aligned &= (x->splits[r - 1][b + 1] - x->splits[r - 1][b]) * es % 16 == 0;
   *vec = rows_vec_ok(y->shape[r - 1], x->nb[r - 1], aligned, es) ? 1 : 0;
+  // even segments (all but the last of one chunk count, the last no longer)
+  const int64_t first = (x->splits[r - 1][1] - x->splits[r - 1][0]) * es / 16;
+  bool even = aligned;
+  for (int b = 0; b < x->nb[r - 1]; ++b) {
+    const int64_t n = (x->splits[r - 1][b + 1] - x->splits[r - 1][b]) * es / 16;
+    even &= b + 1 < x->nb[r - 1] ? n == first : n <= first;
+  }
+  *seg_chunks = even ? (int32_t)first : 0;
   ex->work = img->put_vec(tasks);
   ex->n_work = (int64_t)tasks.size() / 4;
   (void)oi;
@@ -887,7 +899,7 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
       break;
     }
     case K_RMSNORM:
-    case K_SOFTMAX: e = build_rows(sp, ops, oi, &img, &ex, &p->row_len, &p->row_vec); break;
+    case K_SOFTMAX: e = build_rows(sp, ops, oi, &img, &ex, &p->row_len, &p->row_vec, &p->row_cps); break;
     case K_ATTENTION: e = build_attention(ops, oi, ji, oi.causal, &img, &ex); break;
     default: e = fail(EA_ERR_UNSUPPORTED, "internal: unknown plan kind");
   }
@@ -1176,15 +1188,13 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
       a.b_kmajor = plan->b_kmajor;
       a.dt_in = in[0]->dtype;
       a.dt_out = out->dtype;
-      a.waves = getenv("EA_GEMM_WAVES") ? atoi(getenv("EA_GEMM_WAVES")) : 8;
       {
         // direct-to-LDS kernel: contracted block extents multiples of 32 and
-        // at most kGemmMaxTuples tuples per unit
+        // at most kGemmMaxTuples tuples per unit; else the register-staged one
         bool k32 = true;
         for (int64_t v : in[0]->splits[1]) k32 &= v % 32 == 0;
         const int64_t per_unit = (in[0]->nb[1] + plan->gemm_parts - 1) / plan->gemm_parts;
-        a.direct = k32 && per_unit <= kGemmMaxTuples &&
-                   !(getenv("EA_GEMM_DIRECT") && atoi(getenv("EA_GEMM_DIRECT")) == 0);
+        a.direct = k32 && per_unit <= kGemmMaxTuples;
       }
       a.partials = plan->part_o;
       a.counters = plan->counters;
@@ -1216,6 +1226,7 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
       a.causal = oi.causal;
       a.row_len = plan->row_len;
       a.vec = plan->row_vec;
+      a.seg_chunks = plan->row_cps;
       EA_HIP_TRY(plan->kind == K_RMSNORM ? launch_rmsnorm(a, s) : launch_softmax(a, s));
       break;
     }

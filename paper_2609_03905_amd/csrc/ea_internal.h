@@ -149,7 +149,6 @@ struct GemmArgs {
   int32_t dt_out;        // EA_F32, EA_BF16 or EA_F16
   int32_t dt_res;
   int32_t swiglu;        // 1: out = silu(A B) * (A B2)
-  int32_t waves;         // 4 or 8 waves per workgroup (register-staged kernel)
   int32_t direct;        // 1: direct-to-LDS kernel (contracted block extents multiples of 32)
   float* partials;       // [slots][256 x 256] fp32 partial sums of split tiles
   int32_t* counters;     // one per split tile; zero between calls
@@ -179,6 +178,8 @@ struct RowArgs {
   int32_t causal;        // softmax: mask keys beyond the row's query position
   int32_t row_len;       // full extent of the normalised letter
   int32_t vec;           // 1: register path (see rows_vec_ok)
+  int32_t seg_chunks;    // register path: 16-byte chunks of every segment but the
+                         // last (which has at most as many), or 0 if uneven
   float eps;
 };
 

@@ -27,6 +27,22 @@ struct Vec<1> { using T = uint8_t; };
 
 constexpr int kThreads = 256;
 
+constexpr int kUnroll = 4;  // vectors per thread loaded before any is stored
+
+// Byte offsets (source, destination) of byte L of the task's box.
+__device__ __forceinline__ void box_offsets(const RepTask& t, int32_t L, int64_t& so, int64_t& dof) {
+  int32_t row = L / t.row_bytes;
+  const int32_t col = L - row * t.row_bytes;
+  so = col;
+  dof = col;
+  for (int d = t.n_outer - 1; d >= 0; --d) {
+    const int32_t c = row % t.outer_ext[d];
+    row /= t.outer_ext[d];
+    so += (int64_t)c * t.src_stride[d];
+    dof += (int64_t)c * t.dst_stride[d];
+  }
+}
+
 template <int VEC>
 __device__ __forceinline__ void copy_range(const RepTask* __restrict__ tp, const char* __restrict__ src,
                                            char* __restrict__ dst) {
@@ -34,18 +50,24 @@ __device__ __forceinline__ void copy_range(const RepTask* __restrict__ tp, const
   const RepTask& t = *tp;  // fields read from global memory, never copied to the stack
   const char* s0 = src + t.src_off;
   char* d0 = dst + t.dst_off;
-  const int32_t end = t.end, row_bytes = t.row_bytes, n_outer = t.n_outer;
-  for (int32_t L = t.begin + threadIdx.x * VEC; L < end; L += kThreads * VEC) {
-    int32_t row = L / row_bytes;
-    const int32_t col = L - row * row_bytes;
-    int64_t so = col, dof = col;
-    for (int d = n_outer - 1; d >= 0; --d) {
-      const int32_t c = row % t.outer_ext[d];
-      row /= t.outer_ext[d];
-      so += (int64_t)c * t.src_stride[d];
-      dof += (int64_t)c * t.dst_stride[d];
+  const int32_t end = t.end;
+  // kUnroll loads in flight per thread, then their stores.  A vector past the
+  // range is redirected to the range's first vector: it loads that vector and
+  // stores it to its own destination again (the same bytes that lane 0
+  // writes), so neither loads nor stores carry a condition and all the loads
+  // are issued before the first store.
+  for (int32_t L0 = t.begin + threadIdx.x * VEC; L0 < end; L0 += kThreads * VEC * kUnroll) {
+    int64_t sos[kUnroll], dofs[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int32_t L = L0 + u * kThreads * VEC;
+      box_offsets(t, L < end ? L : t.begin, sos[u], dofs[u]);
     }
-    *reinterpret_cast<T*>(d0 + dof) = *reinterpret_cast<const T*>(s0 + so);
+    T v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) v[u] = *reinterpret_cast<const T*>(s0 + sos[u]);
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) *reinterpret_cast<T*>(d0 + dofs[u]) = v[u];
   }
 }
 

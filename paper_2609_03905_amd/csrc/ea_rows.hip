@@ -127,8 +127,13 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-  uint4 v[kMaxK];
-  int seg[kMaxK];
+  // Segment of each of the lane's chunks: direct when every segment but the
+  // last has the same chunk count (the usual even split, ragged tail
+  // allowed), else a scan of the segment table.
+  const int cps = a.seg_chunks;
+  const bool wvec = !SOFTMAX && ES == 2 && a.dt_w == EA_BF16;
+  uint4 v[kMaxK], wv[kMaxK];
+  int seg[kMaxK], e0s[kMaxK];
   bool vis[kMaxK];
   float part = SOFTMAX ? -INFINITY : 0.0f;
 #pragma unroll
@@ -136,13 +141,17 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     const int c = k * 64 + lane;
     vis[k] = false;
     seg[k] = 0;
+    e0s[k] = 0;
     v[k] = make_uint4(0, 0, 0, 0);
+    wv[k] = make_uint4(0, 0, 0, 0);
     if (c < total) {
-      const int s = seg_of(st, ri.nseg, c);
+      const int s = cps > 0 ? min(c / cps, ri.nseg - 1) : seg_of(st, ri.nseg, c);
+      const int e0 = (c - (cps > 0 ? s * cps : st.start[s])) * EPC;  // element index inside the segment
       seg[k] = s;
-      const int e0 = (c - st.start[s]) * EPC;  // element index inside the segment
+      e0s[k] = e0;
       vis[k] = !(SOFTMAX && a.causal) || st.klo[s] + e0 <= ri.qpos;
       if (vis[k]) v[k] = *reinterpret_cast<const uint4*>(a.x + st.xoff[s] + (int64_t)e0 * ES);
+      if (wvec) wv[k] = *reinterpret_cast<const uint4*>(a.w + st.woff[s] + (int64_t)e0 * 2);
     }
   }
   // local partials, then the aggregation across lanes
@@ -152,7 +161,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     float f[8];
     unpack<XT>(v[k], f);
     const int s = seg[k];
-    const int e0 = (k * 64 + lane - st.start[s]) * EPC;
+    const int e0 = e0s[k];
 #pragma unroll
     for (int i = 0; i < EPC; ++i) {
       if constexpr (SOFTMAX) {
@@ -173,7 +182,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
       float f[8];
       unpack<XT>(v[k], f);
       const int s = seg[k];
-      const int e0 = (k * 64 + lane - st.start[s]) * EPC;
+      const int e0 = e0s[k];
 #pragma unroll
       for (int i = 0; i < EPC; ++i) {
         const bool ok = !a.causal || st.klo[s] + e0 + i <= ri.qpos;
@@ -192,19 +201,24 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     const int c = k * 64 + lane;
     if (c >= total) continue;
     const int s = seg[k];
-    const int e0 = (c - st.start[s]) * EPC;
+    const int e0 = e0s[k];
     float f[8];
     unpack<XT>(v[k], f);
     float o[8];
+    if constexpr (SOFTMAX) {
 #pragma unroll
-    for (int i = 0; i < EPC; ++i) {
-      if constexpr (SOFTMAX) {
+      for (int i = 0; i < EPC; ++i) {
         const bool ok = vis[k] && (!a.causal || st.klo[s] + e0 + i <= ri.qpos);
         o[i] = ok ? __expf(f[i] - m) * scale : 0.0f;
-      } else {
-        const float w = ld_elem(a.w + st.woff[s], e0 + i, a.dt_w);
-        o[i] = w * (f[i] * scale);
       }
+    } else if (wvec) {
+      float wf[8];
+      unpack<uint16_t>(wv[k], wf);
+#pragma unroll
+      for (int i = 0; i < EPC; ++i) o[i] = wf[i] * (f[i] * scale);
+    } else {
+#pragma unroll
+      for (int i = 0; i < EPC; ++i) o[i] = ld_elem(a.w + st.woff[s], e0 + i, a.dt_w) * (f[i] * scale);
     }
     const int64_t yidx = (int64_t)ri.row * st.len[s] + e0;
     char* ybase = a.y + st.yoff[s];
