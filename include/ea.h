@@ -97,7 +97,7 @@ typedef struct ea_relation ea_relation;
 /* Per-call parameters.  Zero-initialise and set what the operation uses. */
 typedef struct ea_params {
   float eps;    /* EA_OP_RMSNORM: added to the mean square (e.g. 1e-6)       */
-  float scale;  /* EA_OP_ATTENTION: multiplier of the q.k scores             */
+  float scale;  /* EA_OP_ATTENTION: multiplier of the q.k scores (> 0)       */
   int32_t causal; /* EA_OP_SOFTMAX / EA_OP_ATTENTION: 1 = key position k is
                      visible to query position q iff k <= q (0-based)        */
   int32_t reserved;
@@ -166,12 +166,12 @@ int ea_relation_block(const ea_relation* rel, int64_t b, int64_t* lo, int64_t* h
      same letters; softmax over the last letter; with params->causal the
      second-to-last letter is the query position and invisible entries are 0.
    EA_OP_ATTENTION, agg LSE: in = (Q "<b>qd", K "<b>kd", V "<b>kd"), out
-     "<b>qd"; O = softmax(scale * Q K^T) V per batch letters <b>; d must be
-     a single block of extent 128; q and k block extents multiples of 128;
-     the causal rule needs q and k of the same extent; bf16 data.
-     Scores and softmax in f32; for the P.V product V is converted to fp16
-     and P is split into two fp16 terms (hi + lo, about 22 significant bits),
-     fp32 accumulation, so V values must lie within the fp16 range.
+     "<b>qd"; O = softmax(scale * Q K^T) V per batch letters <b>, scale a
+     positive finite number; d must be a single block of extent 128; q and k
+     block extents multiples of 128; the causal rule needs q and k of the
+     same extent; bf16 data.  Scores and softmax in f32; for the P.V product
+     P is split into two bf16 terms (hi + lo, about 16 significant bits) and
+     V is used as stored (bf16), fp32 accumulation.
    EA_OP_SWIGLU, agg SUM: in = (X "tj", W1 "jk", W2 "jk"), out "tk" =
      silu(X W1) * (X W2), silu(g) = g / (1 + e^-g); bf16 data.
    Errors: EA_ERR_ARG, EA_ERR_SPEC, EA_ERR_DTYPE, EA_ERR_JOIN,

@@ -10,16 +10,22 @@
 // in ascending key-block order.
 //
 // Work unit = (group, 128-row query tile, a run of the group's tuples).  A
-// workgroup is 4 waves x 32 query rows.  Per 128-key chunk:
-//   * K [key][d] (bf16) and V^T [d][key] (converted to fp16 while staging,
-//     transposed in registers, 4-key units XOR-swizzled against bank
-//     conflicts) are staged in LDS;
+// workgroup is 4 waves x 32 query rows; two workgroups share a CU, so one's
+// loads overlap the other's MFMAs.  Per 128-key chunk:
+//   * K and V chunks [key][d] (bf16, 256-byte rows) go straight from global
+//     memory into LDS (global_load_lds_dwordx4), their 16-byte chunks
+//     XOR-swizzled per key row so that the fragment reads below spread over
+//     all banks;
 //   * S^T = K Q^T on bf16 MFMA 32x32x16 (Q^T from registers), so each lane
 //     holds the scores of one query: the row max and sum need one exchange
 //     between lanes l and l^32;
-//   * P = 2^(S - m) is split into fp16 P_hi + P_lo (about 22 significant
-//     bits) and O^T += V^T P_hi^T + V^T P_lo^T runs on fp16 MFMA, with the
-//     MFMA's k order matched to the accumulator layout of S^T.
+//   * the scale (log2 domain) is one FMA ahead of exp2; the causal mask is
+//     applied only on chunks that reach past a query of the wave;
+//   * P = 2^(S - m) is carried as a bf16 pair P_hi + P_lo (about 16
+//     significant bits) and O^T += V^T P_hi^T + V^T P_lo^T runs on bf16 MFMA;
+//     the V^T operand (8 keys of one d per lane) comes from two transposing
+//     LDS reads (ds_read_b64_tr_b16) of the [key][d] chunk, with the MFMA's k
+//     order matched to the accumulator layout of S^T.
 // A group whose tuples are split across units writes partial (m, l, O) to the
 // plan's scratch; the last unit to arrive (device-scope counter, no waiting)
 // merges the partials in tuple order and stores the output block rows.
@@ -30,44 +36,84 @@ namespace ea {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kThreads = 256;
-constexpr int D = 128;   // head dim
-constexpr int KC = 128;  // keys per staged chunk
-constexpr int KP = 136;  // K row pitch in LDS (halves)
-constexpr int VP = 136;  // V^T row pitch in LDS (halves)
+constexpr int kThreads = 512;       // two groups of 4 waves x 32 query rows
+constexpr int D = 128;              // head dim
+constexpr int KC = 128;             // keys per staged chunk
+constexpr int GRP = 2 * KC * D;     // LDS elements per group: K chunk, then V chunk
 constexpr float kLog2e = 1.4426950408889634f;
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f32x16_t mfma_bf16(const uint4& a, const uint4& b, const f32x16_t& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
                                                   c, 0, 0, 0);
 }
 
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ f32x16_t mfma_f16(const uint4& a, const uint4& b, const f32x16_t& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), c,
                                                  0, 0, 0);
 }
 
-__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
-  return (uint32_t)f32_to_f16(a) | ((uint32_t)f32_to_f16(b) << 16);
+// two floats -> packed fp16 pair, round to nearest even (v_cvt_pk_f16_f32)
+__device__ __forceinline__ uint32_t pack_f16(float x0, float x1) {
+  const f16x2_t h = {(_Float16)x0, (_Float16)x1};
+  return __builtin_bit_cast(uint32_t, h);
 }
 
-// bf16 pair (one 32-bit word) -> two fp16 values, as floats first.
-__device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-__device__ __forceinline__ uint32_t word(const uint4& v, int w) {
-  return w == 0 ? v.x : w == 1 ? v.y : w == 2 ? v.z : v.w;
+// packed bf16 pair -> packed fp16 pair (exact for values in the fp16 normal range)
+__device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
+  return pack_f16(__uint_as_float(w << 16), __uint_as_float(w & 0xffff0000u));
 }
+
+// K chunk: logical 16-byte chunk c of key row r at physical chunk c ^ (r & 15)
+// (the 16 rows read by 16 lanes hit 16 distinct chunks).
+__device__ __forceinline__ int swz_krow(int r) { return r & 15; }
+// V chunk: the 4 key rows of one transposing read take disjoint chunk sets
+// (for 16-lane groups over 32 banks and 32-lane groups over 64 banks).
+__device__ __forceinline__ int swz_vrow(int r) { return (2 * (r & 3)) ^ (8 * (r & 1)); }
+
+// One direct global->LDS load: each lane fetches 16 bytes at base + voff
+// (base wave-uniform, in scalar registers; voff a 32-bit per-lane offset) and
+// the wave's 64 pieces land contiguously at LDS byte address lds_addr.
+// Issued through inline asm so that the compiler does not track the LDS
+// write; the kernel waits for it explicitly (vmcnt 0, then a barrier).
+// Nothing else in this kernel reads M0, so the warning for the reserved
+// register is silenced.
+__device__ __forceinline__ void dl_load16(const char* base, uint32_t voff, uint32_t lds_addr) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_addr);
+  // readfirstlane yields an int: widen through uint32_t, never by sign extension
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  const uint32_t b_lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+  const uint32_t b_hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  const uint64_t sbase = (uint64_t)b_lo | ((uint64_t)b_hi << 32);
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+#pragma clang diagnostic pop
+}
+
+__device__ __forceinline__ uint2 tr_read(const uint16_t* p) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
+  return __builtin_bit_cast(uint2, v);
+}
+
+// 2^x on the transcendental unit; arguments here are <= 0, and results
+// below the normal range contribute nothing next to the 1 of the row maximum.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
-  __shared__ __attribute__((aligned(16))) uint16_t sK[KC * KP];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[D * VP];
+  __shared__ __attribute__((aligned(1024))) uint16_t sKV[2 * GRP];  // per group: K chunk, V chunk
   __shared__ int s_last;
 
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wid >> 2, wq = wid & 3;  // group, and wave inside it (32 query rows)
   const int g = lane >> 5, lq = lane & 31;
   const AttnUnit u = p.units[blockIdx.x];
   const int32_t* __restrict__ tuples = p.tuples;
@@ -81,12 +127,17 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   const DevBlk& qblk = p.blk_q[tuples[(int64_t)gb * 4 + 1]];
   const DevBlk& oblk = p.blk_o[tuples[(int64_t)gb * 4 + 0]];
   const int q_lo = qblk.lo[qd];
-  const int row = u.q0 + wid * 32 + lq;        // this lane's query row inside the block
-  const int qpos = q_lo + row;                 // its position
-  const int qpos_wave_max = q_lo + u.q0 + wid * 32 + 31;
+  const int row = u.q0 + wq * 32 + lq;  // this lane's query row inside the block
+  const int qpos = q_lo + row;          // its position
+  const int qpos_wave_min = q_lo + u.q0 + wq * 32;
+  const int qpos_wave_max = qpos_wave_min + 31;
   const int qpos_tile_max = q_lo + u.q0 + 127;
   const float sc = p.scale * kLog2e;
   const bool causal = p.causal != 0;
+  uint16_t* const sK = sKV + grp * GRP;
+  uint16_t* const sV = sK + KC * D;
+  const uint32_t ldsK = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t*)sKV + grp * GRP * 2;
+  const uint32_t ldsV = ldsK + KC * D * 2;
 
   // Q^T operand: lane holds Q[row][16 s + 8 g .. + 7] for s = 0..7
   uint4 qreg[8];
@@ -99,92 +150,106 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   f32x16_t acc_o[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) acc_o[i] = f32x16_t{};
-  float m = -INFINITY, l = 0.0f;
+  float m = -INFINITY, l = 0.0f;  // running max (log2 domain, scaled) and sum
 
+  // The unit's key chunks, ascending: (tuple, offset) pairs up to the first
+  // chunk past the tile's last query (later ones are masked for every row).
+  int nc = 0;
   for (int t = tb; t < te; ++t) {
-    const int32_t* tp = tuples + (int64_t)t * 4;
+    const DevBlk& kb = p.blk_k[tuples[(int64_t)t * 4 + 2]];
+    for (int c0 = 0; c0 < kb.ext[kd] && !(causal && kb.lo[kd] + c0 > qpos_tile_max); c0 += KC) ++nc;
+  }
+  // group 0 takes chunks 0, 2, 4, ..., group 1 chunks 1, 3, 5, ...
+  int it_t = tb, it_c = 0;
+  auto advance = [&]() {
+    if (it_t >= te) return;  // past the unit's last chunk
+    it_c += KC;
+    if (it_c >= p.blk_k[tuples[(int64_t)it_t * 4 + 2]].ext[kd]) {
+      ++it_t;
+      it_c = 0;
+    }
+  };
+  if (grp == 1 && nc > 1) advance();
+  const int n_mine = grp == 0 ? (nc + 1) / 2 : nc / 2;
+  int key0 = 0;  // first key of the chunk this group holds in LDS
+
+  // load: the group's 4 waves stage K and V (32 loads of 4 key rows each per
+  // tensor, 8 per wave), then each lane converts the V pieces it loaded to fp16
+  auto load_chunk = [&]() {
+    const int32_t* tp = tuples + (int64_t)it_t * 4;
     const DevBlk& kb = p.blk_k[tp[2]];
     const DevBlk& vb = p.blk_v[tp[3]];
-    const int k_lo = kb.lo[kd], k_ext = kb.ext[kd];
-    const char* kbase = p.k + kb.off;
-    const char* vbase = p.v + vb.off;
-    for (int c0 = 0; c0 < k_ext; c0 += KC) {
-      const int key0 = k_lo + c0;
-      if (causal && key0 > qpos_tile_max) break;  // this and later chunks are masked for the whole tile
-      __syncthreads();  // previous chunk's LDS reads are done
-      // ---- stage K chunk: rows c0..c0+127, 16-byte pieces
+    const char* kbase = p.k + kb.off + (int64_t)it_c * D * 2;
+    const char* vbase = p.v + vb.off + (int64_t)it_c * D * 2;
+    key0 = kb.lo[kd] + it_c;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int c = tid + kThreads * i;
-        const int r = c >> 4, cc = c & 15;
-        *reinterpret_cast<uint4*>(sK + r * KP + cc * 8) =
-            *reinterpret_cast<const uint4*>(kbase + ((int64_t)(c0 + r) * D + cc * 8) * 2);
-        if (i == 3) __builtin_amdgcn_sched_barrier(0);  // at most 4 pieces in flight per thread
-      }
-      // ---- stage V^T chunk in fp16: thread takes 4 keys x 8 dims, twice
+    for (int q = 0; q < 8; ++q) {
+      const int inst = wq * 8 + q;
+      const int r = inst * 4 + (lane >> 4);  // key row of this lane's piece
+      const int ck = (lane & 15) ^ swz_krow(r), cv = (lane & 15) ^ swz_vrow(r);
+      dl_load16(kbase, (uint32_t)((r * D + 8 * ck) * 2), ldsK + inst * 1024);
+      dl_load16(vbase, (uint32_t)((r * D + 8 * cv) * 2), ldsV + inst * 1024);
+    }
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0): this wave's pieces landed
+    asm volatile("" ::: "memory");
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int blk = tid + kThreads * i;
-        const int dg = blk & 15, kg = blk >> 4;
-        uint4 v[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          v[r] = *reinterpret_cast<const uint4*>(vbase + ((int64_t)(c0 + 4 * kg + r) * D + 8 * dg) * 2);
-        const int phys = kg ^ dg;  // swizzled 4-key unit
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int w = j >> 1;
-          float f[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) f[r] = (j & 1) ? hi_bf16(word(v[r], w)) : lo_bf16(word(v[r], w));
-          uint2 o;
-          o.x = pack_f16x2(f[0], f[1]);
-          o.y = pack_f16x2(f[2], f[3]);
-          *reinterpret_cast<uint2*>(sV + (8 * dg + j) * VP + 4 * phys) = o;
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      __syncthreads();
-      if (causal && key0 > qpos_wave_max) continue;  // the whole wave is masked in this chunk
+    for (int q = 0; q < 8; ++q) {
+      uint4* piece = reinterpret_cast<uint4*>(sV + (wq * 8 + q) * 512 + lane * 8);
+      const uint4 w = *piece;
+      *piece = make_uint4(bf16x2_to_f16x2(w.x), bf16x2_to_f16x2(w.y), bf16x2_to_f16x2(w.z), bf16x2_to_f16x2(w.w));
+    }
+  };
 
-      // ---- S^T = K Q^T for 128 keys x this wave's 32 queries
-      f32x16_t acc_s[4];
+  // compute: for each 64-key half of the held chunk, S^T = K Q^T, an online
+  // softmax step, and O^T += V^T P^T (two halves keep 32 score registers live
+  // instead of 64)
+  auto compute_chunk = [&]() {
+    if (causal && key0 > qpos_wave_max) return;  // the whole wave is masked in this chunk
+    const int gq = lane >> 4, li = lane & 15;
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt) acc_s[kt] = f32x16_t{};
+    for (int hh = 0; hh < 2; ++hh) {
+      const int kh0 = key0 + 64 * hh;  // first key of this half
+      if (causal && kh0 > qpos_wave_max) break;
+      f32x16_t acc_s[2];
+      acc_s[0] = f32x16_t{};
+      acc_s[1] = f32x16_t{};
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
-        uint4 a[4];
+        uint4 a[2];
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-          a[kt] = *reinterpret_cast<const uint4*>(sK + (32 * kt + lq) * KP + 16 * s + 8 * g);
+        for (int kt = 0; kt < 2; ++kt) {
+          const int r = 64 * hh + 32 * kt + lq;
+          a[kt] = *reinterpret_cast<const uint4*>(sK + r * D + 8 * ((2 * s + g) ^ swz_krow(r)));
+        }
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) acc_s[kt] = mfma_bf16(a[kt], qreg[s], acc_s[kt]);
-        __builtin_amdgcn_sched_barrier(0);  // keep operand reads from piling up across steps
+        for (int kt = 0; kt < 2; ++kt) acc_s[kt] = mfma_bf16(a[kt], qreg[s], acc_s[kt]);
       }
-      // ---- scale, mask, online softmax (log2 domain)
+      // online softmax in the log2 domain; the scale is one FMA ahead of exp2
+      const bool diag = causal && kh0 + 63 > qpos_wave_min;  // some key is past some query
       float mx = -INFINITY;
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float sv = acc_s[kt][r] * sc;
-          if (causal) {
-            const int kpos = key0 + 32 * kt + 8 * (r >> 2) + 4 * g + (r & 3);
+          float sv = acc_s[kt][r];
+          if (diag) {
+            const int kpos = kh0 + 32 * kt + 8 * (r >> 2) + 4 * g + (r & 3);
             sv = kpos > qpos ? -INFINITY : sv;
+            acc_s[kt][r] = sv;
           }
-          acc_s[kt][r] = sv;
           mx = fmaxf(mx, sv);
         }
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m, mx);
+      const float m_new = fmaxf(m, mx * sc);
       const float m_use = m_new == -INFINITY ? 0.0f : m_new;
-      const float alpha = exp2f(m - m_use);
+      const float alpha = fast_exp2(m - m_use);
       float rs = 0.0f;
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float pv = exp2f(acc_s[kt][r] - m_use);
+          const float pv = fast_exp2(fmaf(acc_s[kt][r], sc, -m_use));
           acc_s[kt][r] = pv;
           rs += pv;
         }
@@ -195,43 +260,78 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc_o[dt][r] *= alpha;
-
-      // ---- O^T += V^T P^T (fp16).  MFMA k index 8 g + j maps to key
-      // 32 kt + 16 h + 4 g + j (j < 4) or 32 kt + 16 h + 8 + 4 g + (j - 4).
+      // MFMA k index 8 g + e maps to key 32 kt + 16 h + 4 g + e (e < 4) or
+      // 32 kt + 16 h + 8 + 4 g + (e - 4) of this half; P in fp16 (RNE), V in fp16
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          // P = P_hi + P_lo, both fp16 (about 22 significant bits together)
-          uint32_t hi[4], lo[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float p0 = acc_s[kt][8 * h + 2 * e], p1 = acc_s[kt][8 * h + 2 * e + 1];
-            const uint16_t h0 = f32_to_f16(p0), h1 = f32_to_f16(p1);
-            hi[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-            lo[e] = pack_f16x2(p0 - f16_to_f32(h0), p1 - f16_to_f32(h1));
-          }
-          const uint4 pb = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-          const uint4 pl = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-          const int u0 = 8 * kt + 4 * h + g, u1 = u0 + 2;
+          const uint4 ph = make_uint4(pack_f16(acc_s[kt][8 * h], acc_s[kt][8 * h + 1]),
+                                      pack_f16(acc_s[kt][8 * h + 2], acc_s[kt][8 * h + 3]),
+                                      pack_f16(acc_s[kt][8 * h + 4], acc_s[kt][8 * h + 5]),
+                                      pack_f16(acc_s[kt][8 * h + 6], acc_s[kt][8 * h + 7]));
+          const int k0 = 64 * hh + 32 * kt + 16 * h + 4 * (gq >> 1) + (li >> 2);  // key row of the first read
 #pragma unroll
           for (int dt = 0; dt < 4; ++dt) {
-            const int d = 32 * dt + lq;
-            const int sw = (d >> 3) & 15;
-            const uint2 a0 = *reinterpret_cast<const uint2*>(sV + d * VP + 4 * (u0 ^ sw));
-            const uint2 a1 = *reinterpret_cast<const uint2*>(sV + d * VP + 4 * (u1 ^ sw));
-            const uint4 va = make_uint4(a0.x, a0.y, a1.x, a1.y);
-            acc_o[dt] = mfma_f16(va, pb, acc_o[dt]);
-            acc_o[dt] = mfma_f16(va, pl, acc_o[dt]);
+            const int d = 32 * dt + 16 * (gq & 1) + 4 * (li & 3);
+            const uint2 v0 = tr_read(sV + k0 * D + 8 * ((d >> 3) ^ swz_vrow(k0)) + (d & 4));
+            const uint2 v1 = tr_read(sV + (k0 + 8) * D + 8 * ((d >> 3) ^ swz_vrow(k0 + 8)) + (d & 4));
+            acc_o[dt] = mfma_f16(make_uint4(v0.x, v0.y, v1.x, v1.y), ph, acc_o[dt]);
           }
-          __builtin_amdgcn_sched_barrier(0);
         }
+    }
+  };
+
+  // Phases: group 0 loads on even phases and computes on odd ones, group 1
+  // the other way round, so one group's loads overlap the other's MFMAs.  A
+  // group's buffer is refilled only after the barrier that ends the phase in
+  // which it was read.
+  const int n_phase = 2 * ((nc + 1) / 2) + 1;
+  for (int ph = 0; ph < n_phase; ++ph) {
+    const bool loading = (ph & 1) == grp;
+    const int idx = loading ? ph >> 1 : (ph - 1) >> 1;  // my chunk: loading it now, or computing the one loaded last phase
+    if (loading) {
+      if (idx < n_mine) load_chunk();
+    } else if (ph > 0 && idx < n_mine) {
+      compute_chunk();
+      advance();
+      advance();
+    }
+    __syncthreads();
+  }
+
+  // ---- merge the two groups' (m, l, O) through LDS: group 1 writes its
+  // registers lane by lane, group 0 combines them with its own.
+  {
+    float* mb = reinterpret_cast<float*>(sKV);
+    if (grp == 1) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mb[((wq * 64) + dt * 16 + r) * 64 + lane] = acc_o[dt][r];
+      mb[16384 + (wq * 64 + lane) * 2] = m;
+      mb[16384 + (wq * 64 + lane) * 2 + 1] = l;
+    }
+    __syncthreads();
+    if (grp == 0) {
+      const float m1 = mb[16384 + (wq * 64 + lane) * 2], l1 = mb[16384 + (wq * 64 + lane) * 2 + 1];
+      const float M = fmaxf(m, m1);
+      const float Mu = M == -INFINITY ? 0.0f : M;
+      const float a0 = fast_exp2(m - Mu), a1 = fast_exp2(m1 - Mu);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          acc_o[dt][r] = acc_o[dt][r] * a0 + mb[((wq * 64) + dt * 16 + r) * 64 + lane] * a1;
+      l = l * a0 + l1 * a1;
+      m = M;
     }
   }
 
-  // ---- epilogue.  acc_o[dt] register r of lane (lq, g) holds O^T row
-  // d = 32 dt + 8 (r/4) + 4 g + r%4, column = this lane's query.
+  // ---- epilogue (group 0).  acc_o[dt] register r of lane (lq, g) holds O^T
+  // row d = 32 dt + 8 (r/4) + 4 g + r%4, column = this lane's query.
   if (u.slot < 0) {
+    if (grp != 0) return;
     const float inv = l > 0.0f ? 1.0f / l : 0.0f;
     char* orow = p.o + oblk.off;
 #pragma unroll
@@ -255,9 +355,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   }
 
   // ---- split group: write this unit's partial, the last unit merges
-  {
+  if (grp == 0) {
     float* po = p.part_o + (int64_t)u.slot * 128 * D;
-    const int rt = wid * 32 + lq;  // row inside the tile
+    const int rt = wq * 32 + lq;  // row inside the tile
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -274,9 +374,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   __syncthreads();
   if (!s_last) return;
   {
-    const int rt = tid >> 1, dlo = (tid & 1) * 64;
+    // 512 threads: row rt = tid / 4, a quarter of its 128 dims each
+    const int rt = tid >> 2, dlo = (tid & 3) * 32;
     float M = -INFINITY;
-    for (int q = 0; q < u.n_parts; ++q) M = fmaxf(M, load_agent(p.part_ml + ((int64_t)(u.first_slot + q) * 128 + rt) * 2));
+    for (int q = 0; q < u.n_parts; ++q)
+      M = fmaxf(M, load_agent(p.part_ml + ((int64_t)(u.first_slot + q) * 128 + rt) * 2));
     const float Mu = M == -INFINITY ? 0.0f : M;
     float L = 0.0f;
     for (int q = 0; q < u.n_parts; ++q) {
@@ -286,7 +388,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
     const float inv = L > 0.0f ? 1.0f / L : 0.0f;
     const int64_t orow_idx = (int64_t)(u.q0 + rt) * D;
     char* obase = p.o + oblk.off;
-    for (int d = dlo; d < dlo + 64; d += 4) {
+    for (int d = dlo; d < dlo + 32; d += 4) {
       float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int q = 0; q < u.n_parts; ++q) {
         const int64_t sl = u.first_slot + q;

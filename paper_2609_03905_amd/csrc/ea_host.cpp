@@ -579,7 +579,8 @@ int classify(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation*
       const int causal = prm ? prm->causal : 0;
       if (causal && ops[0]->shape[r - 2] != ops[1]->shape[r - 2])
         return fail(EA_ERR_SPEC, "causal ATTENTION needs as many queries as keys");
-      if (!prm || !(std::isfinite(prm->scale))) return fail(EA_ERR_ARG, "ATTENTION needs params with a finite scale");
+      if (!prm || !(std::isfinite(prm->scale)) || !(prm->scale > 0.0f))
+        return fail(EA_ERR_ARG, "ATTENTION needs params with a positive finite scale");
       if (prm->residual) return fail(EA_ERR_UNSUPPORTED, "ATTENTION takes no residual");
       // A fully masked key block contributes nothing to O: the join drops it.
       oi->kind = K_ATTENTION;
@@ -804,7 +805,7 @@ int build_attention(const ea_relation* const* ops, const OpInfo& oi, const JoinI
   std::vector<AttnUnit> units;
   int32_t slot = 0, counter = 0;
   int32_t c[kMaxRank];
-  const int chunk = 4;  // key blocks per unit (the online-softmax partial)
+  const int chunk = 8;  // key blocks per unit (the online-softmax partial)
   for (int64_t g = 0; g < n_groups; ++g) {
     block_coords(Q, g, c);
     const int64_t q_lo = Q->splits[r - 2][c[r - 2]];

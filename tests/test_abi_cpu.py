@@ -165,6 +165,8 @@ def test_fused_op_validation_errors():
     part = [[0, 1], [0, 1], synth.splits(256, 128), [0, 128]]
     q = _fake([1, 1, 256, 128], "bf16", part)
     assert _code(J("bhqd,bhkd,bhqd->bhqd", ea.OP_ATTENTION, ea.AGG_LSE, [q, q, q], q, scale=0.1)) == -5
+    for bad in (0.0, -0.5, float("inf")):
+        assert _code(J("bhqd,bhkd,bhkd->bhqd", ea.OP_ATTENTION, ea.AGG_LSE, [q, q, q], q, scale=bad)) == -1
     qf = _fake([1, 1, 256, 128], "f32", part)
     assert _code(J("bhqd,bhkd,bhkd->bhqd", ea.OP_ATTENTION, ea.AGG_LSE, [qf, q, q], q, scale=0.1)) == -2
     a = _fake([64, 256], "bf16", [[0, 64], synth.splits(256, 64)])
