@@ -40,8 +40,16 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 512;       // two groups of 4 waves x 32 query rows
 constexpr int D = 128;              // head dim
-constexpr int KC = 128;             // keys per staged chunk
-constexpr int GRP = 2 * KC * D;     // LDS elements per group: K chunk, then V chunk
+constexpr int KC = 64;              // keys per staged chunk
+constexpr int BUF = 2 * KC * D;     // LDS elements per chunk buffer: K chunk, then V chunk
+constexpr int NBUF = 4;             // two chunks computed while the next two load
+
+// Per-tuple K/V metadata of a unit, staged in LDS once so that the chunk walk
+// never waits on a chain of global table loads.
+struct KvMeta {
+  int64_t koff, voff;  // byte offsets of the K and V blocks
+  int32_t klo, kext;   // key interval of the block
+};
 constexpr float kLog2e = 1.4426950408889634f;
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -108,7 +116,8 @@ __device__ __forceinline__ uint2 tr_read(const uint16_t* p) {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
-  __shared__ __attribute__((aligned(1024))) uint16_t sKV[2 * GRP];  // per group: K chunk, V chunk
+  __shared__ __attribute__((aligned(1024))) uint16_t sKV[NBUF * BUF];  // chunk buffers: K, then V
+  __shared__ KvMeta s_tm[kAttnMaxUnitTuples];
   __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -134,10 +143,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   const int qpos_tile_max = q_lo + u.q0 + 127;
   const float sc = p.scale * kLog2e;
   const bool causal = p.causal != 0;
-  uint16_t* const sK = sKV + grp * GRP;
-  uint16_t* const sV = sK + KC * D;
-  const uint32_t ldsK = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t*)sKV + grp * GRP * 2;
-  const uint32_t ldsV = ldsK + KC * D * 2;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t*)sKV;
 
   // Q^T operand: lane holds Q[row][16 s + 8 g .. + 7] for s = 0..7
   uint4 qreg[8];
@@ -152,152 +158,172 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   for (int i = 0; i < 4; ++i) acc_o[i] = f32x16_t{};
   float m = -INFINITY, l = 0.0f;  // running max (log2 domain, scaled) and sum
 
-  // The unit's key chunks, ascending: (tuple, offset) pairs up to the first
-  // chunk past the tile's last query (later ones are masked for every row).
-  int nc = 0;
-  for (int t = tb; t < te; ++t) {
-    const DevBlk& kb = p.blk_k[tuples[(int64_t)t * 4 + 2]];
-    for (int c0 = 0; c0 < kb.ext[kd] && !(causal && kb.lo[kd] + c0 > qpos_tile_max); c0 += KC) ++nc;
-  }
-  // group 0 takes chunks 0, 2, 4, ..., group 1 chunks 1, 3, 5, ...
-  int it_t = tb, it_c = 0;
-  auto advance = [&]() {
-    if (it_t >= te) return;  // past the unit's last chunk
-    it_c += KC;
-    if (it_c >= p.blk_k[tuples[(int64_t)it_t * 4 + 2]].ext[kd]) {
-      ++it_t;
-      it_c = 0;
-    }
-  };
-  if (grp == 1 && nc > 1) advance();
-  const int n_mine = grp == 0 ? (nc + 1) / 2 : nc / 2;
-  int key0 = 0;  // first key of the chunk this group holds in LDS
-
-  // load: the group's 4 waves stage K and V (32 loads of 4 key rows each per
-  // tensor, 8 per wave), then each lane converts the V pieces it loaded to fp16
-  auto load_chunk = [&]() {
-    const int32_t* tp = tuples + (int64_t)it_t * 4;
+  // the unit's tuples' K/V metadata into LDS (nt <= kAttnMaxUnitTuples: host guarantee)
+  const int nt = te - tb;
+  if (tid < nt) {
+    const int32_t* tp = tuples + (int64_t)(tb + tid) * 4;
     const DevBlk& kb = p.blk_k[tp[2]];
     const DevBlk& vb = p.blk_v[tp[3]];
-    const char* kbase = p.k + kb.off + (int64_t)it_c * D * 2;
-    const char* vbase = p.v + vb.off + (int64_t)it_c * D * 2;
-    key0 = kb.lo[kd] + it_c;
+    KvMeta mt;
+    mt.koff = kb.off;
+    mt.voff = vb.off;
+    mt.klo = kb.lo[kd];
+    mt.kext = kb.ext[kd];
+    s_tm[tid] = mt;
+  }
+  __syncthreads();
+  // The unit's 64-key chunks, ascending: (tuple, offset) pairs up to the
+  // first chunk past the tile's last query (later ones are masked for every row).
+  int nc = 0;
+  for (int t = 0; t < nt; ++t)
+    for (int c0 = 0; c0 < s_tm[t].kext && !(causal && s_tm[t].klo + c0 > qpos_tile_max); c0 += KC) ++nc;
+  // walk of the chunks in load order; chunk j goes to buffer j % 4
+  int it_t = 0, it_c = 0;  // tuple (index into s_tm) and offset of the next chunk to load
+  int key0_buf[NBUF];  // first key of the chunk held in each buffer (constant indices only)
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int inst = wq * 8 + q;
+  for (int b = 0; b < NBUF; ++b) key0_buf[b] = 0;
+
+  // Load the next chunk of the walk into buffer b (a compile-time constant):
+  // all 8 waves take part, 2 K and 2 V loads of 4 key rows each per wave.
+  auto load_chunk = [&](int b) {
+    const KvMeta& mt = s_tm[it_t];
+    const char* kbase = p.k + mt.koff + (int64_t)it_c * D * 2;
+    const char* vbase = p.v + mt.voff + (int64_t)it_c * D * 2;
+    key0_buf[b] = mt.klo + it_c;
+    const uint32_t ldsK = lds0 + b * BUF * 2, ldsV = ldsK + KC * D * 2;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int inst = wid * 2 + q;
       const int r = inst * 4 + (lane >> 4);  // key row of this lane's piece
       const int ck = (lane & 15) ^ swz_krow(r), cv = (lane & 15) ^ swz_vrow(r);
       dl_load16(kbase, (uint32_t)((r * D + 8 * ck) * 2), ldsK + inst * 1024);
       dl_load16(vbase, (uint32_t)((r * D + 8 * cv) * 2), ldsV + inst * 1024);
     }
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0): this wave's pieces landed
-    asm volatile("" ::: "memory");
+    it_c += KC;
+    if (it_c >= mt.kext) {
+      ++it_t;
+      it_c = 0;
+    }
+  };
+  // after this wave's loads have landed: its V pieces of buffer b to fp16
+  auto convert_v = [&](int b) {
+    uint16_t* sVb = sKV + b * BUF + KC * D;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      uint4* piece = reinterpret_cast<uint4*>(sV + (wq * 8 + q) * 512 + lane * 8);
+    for (int q = 0; q < 2; ++q) {
+      uint4* piece = reinterpret_cast<uint4*>(sVb + (wid * 2 + q) * 512 + lane * 8);
       const uint4 w = *piece;
       *piece = make_uint4(bf16x2_to_f16x2(w.x), bf16x2_to_f16x2(w.y), bf16x2_to_f16x2(w.z), bf16x2_to_f16x2(w.w));
     }
   };
 
-  // compute: for each 64-key half of the held chunk, S^T = K Q^T, an online
-  // softmax step, and O^T += V^T P^T (two halves keep 32 score registers live
-  // instead of 64)
-  auto compute_chunk = [&]() {
+  // compute the 64-key chunk held in buffer b: S^T = K Q^T, an online
+  // softmax step, O^T += V^T P^T
+  auto compute_chunk = [&](int b) {
+    const uint16_t* sK = sKV + b * BUF;
+    const uint16_t* sV = sK + KC * D;
+    const int key0 = key0_buf[b];
     if (causal && key0 > qpos_wave_max) return;  // the whole wave is masked in this chunk
-    const int gq = lane >> 4, li = lane & 15;
+    f32x16_t acc_s[2];
+    acc_s[0] = f32x16_t{};
+    acc_s[1] = f32x16_t{};
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      const int kh0 = key0 + 64 * hh;  // first key of this half
-      if (causal && kh0 > qpos_wave_max) break;
-      f32x16_t acc_s[2];
-      acc_s[0] = f32x16_t{};
-      acc_s[1] = f32x16_t{};
+    for (int s = 0; s < 8; ++s) {
+      uint4 a[2];
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        uint4 a[2];
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-          const int r = 64 * hh + 32 * kt + lq;
-          a[kt] = *reinterpret_cast<const uint4*>(sK + r * D + 8 * ((2 * s + g) ^ swz_krow(r)));
-        }
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) acc_s[kt] = mfma_bf16(a[kt], qreg[s], acc_s[kt]);
+      for (int kt = 0; kt < 2; ++kt) {
+        const int r = 32 * kt + lq;
+        a[kt] = *reinterpret_cast<const uint4*>(sK + r * D + 8 * ((2 * s + g) ^ swz_krow(r)));
       }
-      // online softmax in the log2 domain; the scale is one FMA ahead of exp2
-      const bool diag = causal && kh0 + 63 > qpos_wave_min;  // some key is past some query
-      float mx = -INFINITY;
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < 2; ++kt) acc_s[kt] = mfma_bf16(a[kt], qreg[s], acc_s[kt]);
+    }
+    // online softmax in the log2 domain; the scale is one FMA ahead of exp2
+    const bool diag = causal && key0 + KC - 1 > qpos_wave_min;  // some key is past some query
+    float mx = -INFINITY;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float sv = acc_s[kt][r];
-          if (diag) {
-            const int kpos = kh0 + 32 * kt + 8 * (r >> 2) + 4 * g + (r & 3);
-            sv = kpos > qpos ? -INFINITY : sv;
-            acc_s[kt][r] = sv;
-          }
-          mx = fmaxf(mx, sv);
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float sv = acc_s[kt][r];
+        if (diag) {
+          const int kpos = key0 + 32 * kt + 8 * (r >> 2) + 4 * g + (r & 3);
+          sv = kpos > qpos ? -INFINITY : sv;
+          acc_s[kt][r] = sv;
         }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m, mx * sc);
-      const float m_use = m_new == -INFINITY ? 0.0f : m_new;
+        mx = fmaxf(mx, sv);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m, mx * sc);
+    const float m_use = m_new == -INFINITY ? 0.0f : m_new;
+    float rs = 0.0f;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float pv = fast_exp2(fmaf(acc_s[kt][r], sc, -m_use));
+        acc_s[kt][r] = pv;
+        rs += pv;
+      }
+    rs += __shfl_xor(rs, 32, 64);
+    if (__any(m_new != m)) {  // a running max moved: rescale (else alpha is 1 on every lane)
       const float alpha = fast_exp2(m - m_use);
-      float rs = 0.0f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float pv = fast_exp2(fmaf(acc_s[kt][r], sc, -m_use));
-          acc_s[kt][r] = pv;
-          rs += pv;
-        }
-      rs += __shfl_xor(rs, 32, 64);
-      l = l * alpha + rs;
-      m = m_new;
+      l *= alpha;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc_o[dt][r] *= alpha;
-      // MFMA k index 8 g + e maps to key 32 kt + 16 h + 4 g + e (e < 4) or
-      // 32 kt + 16 h + 8 + 4 g + (e - 4) of this half; P in fp16 (RNE), V in fp16
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const uint4 ph = make_uint4(pack_f16(acc_s[kt][8 * h], acc_s[kt][8 * h + 1]),
-                                      pack_f16(acc_s[kt][8 * h + 2], acc_s[kt][8 * h + 3]),
-                                      pack_f16(acc_s[kt][8 * h + 4], acc_s[kt][8 * h + 5]),
-                                      pack_f16(acc_s[kt][8 * h + 6], acc_s[kt][8 * h + 7]));
-          const int k0 = 64 * hh + 32 * kt + 16 * h + 4 * (gq >> 1) + (li >> 2);  // key row of the first read
-#pragma unroll
-          for (int dt = 0; dt < 4; ++dt) {
-            const int d = 32 * dt + 16 * (gq & 1) + 4 * (li & 3);
-            const uint2 v0 = tr_read(sV + k0 * D + 8 * ((d >> 3) ^ swz_vrow(k0)) + (d & 4));
-            const uint2 v1 = tr_read(sV + (k0 + 8) * D + 8 * ((d >> 3) ^ swz_vrow(k0 + 8)) + (d & 4));
-            acc_o[dt] = mfma_f16(make_uint4(v0.x, v0.y, v1.x, v1.y), ph, acc_o[dt]);
-          }
-        }
     }
+    l += rs;
+    m = m_new;
+    // MFMA k index 8 g + e maps to key 32 kt + 16 h + 4 g + e (e < 4) or
+    // 32 kt + 16 h + 8 + 4 g + (e - 4); P in fp16 (RNE), V in fp16
+    const int gq = lane >> 4, li = lane & 15;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint4 ph = make_uint4(pack_f16(acc_s[kt][8 * h], acc_s[kt][8 * h + 1]),
+                                    pack_f16(acc_s[kt][8 * h + 2], acc_s[kt][8 * h + 3]),
+                                    pack_f16(acc_s[kt][8 * h + 4], acc_s[kt][8 * h + 5]),
+                                    pack_f16(acc_s[kt][8 * h + 6], acc_s[kt][8 * h + 7]));
+        const int k0 = 32 * kt + 16 * h + 4 * (gq >> 1) + (li >> 2);  // key row of this lane's first read
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) {
+          const int d = 32 * dt + 16 * (gq & 1) + 4 * (li & 3);
+          const uint2 v0 = tr_read(sV + k0 * D + 8 * ((d >> 3) ^ swz_vrow(k0)) + (d & 4));
+          const uint2 v1 = tr_read(sV + (k0 + 8) * D + 8 * ((d >> 3) ^ swz_vrow(k0 + 8)) + (d & 4));
+          acc_o[dt] = mfma_f16(make_uint4(v0.x, v0.y, v1.x, v1.y), ph, acc_o[dt]);
+        }
+      }
   };
 
-  // Phases: group 0 loads on even phases and computes on odd ones, group 1
-  // the other way round, so one group's loads overlap the other's MFMAs.  A
-  // group's buffer is refilled only after the barrier that ends the phase in
-  // which it was read.
-  const int n_phase = 2 * ((nc + 1) / 2) + 1;
-  for (int ph = 0; ph < n_phase; ++ph) {
-    const bool loading = (ph & 1) == grp;
-    const int idx = loading ? ph >> 1 : (ph - 1) >> 1;  // my chunk: loading it now, or computing the one loaded last phase
-    if (loading) {
-      if (idx < n_mine) load_chunk();
-    } else if (ph > 0 && idx < n_mine) {
-      compute_chunk();
-      advance();
-      advance();
+  // Phases: in phase ph every wave issues its loads of chunks 2ph and 2ph+1
+  // (buffers 2ph % 4, 2ph % 4 + 1), group 0 computes chunk 2ph - 2 and group
+  // 1 chunk 2ph - 1 (the other two buffers) while those loads are in
+  // flight; then each wave waits for its own loads, converts its V pieces,
+  // and the workgroup meets at the barrier.  The loop runs two phases per
+  // iteration so that every buffer index is a compile-time constant.
+  const int n_phase = (nc + 1) / 2 + 1;
+  for (int ph0 = 0; ph0 < n_phase; ph0 += 2) {
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int ph = ph0 + e;
+      if (ph < n_phase) {
+        const int lb = 2 * e, cb = 2 * (1 - e);  // buffers loaded / computed in this phase
+        if (2 * ph < nc) load_chunk(lb);
+        if (2 * ph + 1 < nc) load_chunk(lb + 1);
+        const int cj = 2 * ph - 2 + grp;  // this group's chunk to compute
+        if (ph >= 1 && cj < nc) compute_chunk(cb + grp);
+        if (2 * ph < nc) {
+          asm volatile("" ::: "memory");
+          __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0): this wave's pieces landed
+          asm volatile("" ::: "memory");
+          convert_v(lb);
+          if (2 * ph + 1 < nc) convert_v(lb + 1);
+        }
+        __syncthreads();
+      }
     }
-    __syncthreads();
   }
 
   // ---- merge the two groups' (m, l, O) through LDS: group 1 writes its

@@ -805,7 +805,8 @@ int build_attention(const ea_relation* const* ops, const OpInfo& oi, const JoinI
   std::vector<AttnUnit> units;
   int32_t slot = 0, counter = 0;
   int32_t c[kMaxRank];
-  const int chunk = 8;  // key blocks per unit (the online-softmax partial)
+  constexpr int chunk = 8;  // key blocks per unit (the online-softmax partial)
+  static_assert(chunk <= kAttnMaxUnitTuples, "attention unit size");
   for (int64_t g = 0; g < n_groups; ++g) {
     block_coords(Q, g, c);
     const int64_t q_lo = Q->splits[r - 2][c[r - 2]];

@@ -205,6 +205,8 @@ struct AttnUnit {
   int32_t weight;      // expected tuple count (host-side ordering only)
 };
 
+constexpr int kAttnMaxUnitTuples = 32;  // key blocks per attention work unit (LDS table size)
+
 struct AttnArgs {
   const int32_t* tuples;
   const int32_t* goff;
