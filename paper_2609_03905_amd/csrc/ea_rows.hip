@@ -113,50 +113,77 @@ __device__ __forceinline__ void unpack<float>(const uint4& v, float (&f)[8]) {
 // ---------------------------------------------------------------------------
 // register path; XT: uint16_t for bf16 rows, float for f32 rows
 // ---------------------------------------------------------------------------
-template <typename XT, bool SOFTMAX>
+// K: 16-byte chunks of the row per lane (4, 8 or 16), chosen from the row
+// length so that short rows keep few registers and many waves per SIMD.
+template <typename XT, bool SOFTMAX, int K>
 __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
   __shared__ SegTable tabs[kThreads / 64];
+  // RMSNorm: the weights of the group's row, in the row's chunk order as
+  // fp32 (EPC values per chunk), staged once for the workgroup's rows
+  constexpr int ES = sizeof(XT), EPC = 16 / ES;
+  __shared__ float sw[SOFTMAX ? 1 : K * 64 * EPC];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int32_t* task = a.rows + 4 * blockIdx.x;
-  if (wid >= task[2]) return;  // whole wavefront leaves together
+  const bool active = wid < task[2];  // waves past the task's rows only help stage the weights
   SegTable& st = tabs[wid];
-  const RowInfo ri = row_info(a, wid);
-  constexpr int ES = sizeof(XT), EPC = 16 / ES;
+  const RowInfo ri = row_info(a, wid);  // every row of the task is in the same group
   const int total = fill_segments(a, ri, st, lane, ES);
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-  // Segment of each of the lane's chunks: direct when every segment but the
-  // last has the same chunk count (the usual even split, ragged tail
-  // allowed), else a scan of the segment table.
+  // Segment of a chunk: direct when every segment but the last has the same
+  // chunk count (the usual even split, ragged tail allowed), else a scan of
+  // the segment table.
   const int cps = a.seg_chunks;
-  const bool wvec = !SOFTMAX && ES == 2 && a.dt_w == EA_BF16;
-  uint4 v[kMaxK], wv[kMaxK];
-  int seg[kMaxK], e0s[kMaxK];
-  bool vis[kMaxK];
+  auto locate = [&](const SegTable& t, int c, int& s, int& e0) {
+    s = cps > 0 ? min(c / cps, ri.nseg - 1) : seg_of(t, ri.nseg, c);
+    e0 = (c - (cps > 0 ? s * cps : t.start[s])) * EPC;
+  };
+
+  uint4 v[K];
+  int seg[K], e0s[K];
+  bool vis[K];
   float part = SOFTMAX ? -INFINITY : 0.0f;
 #pragma unroll
-  for (int k = 0; k < kMaxK; ++k) {
+  for (int k = 0; k < K; ++k) {
     const int c = k * 64 + lane;
     vis[k] = false;
     seg[k] = 0;
     e0s[k] = 0;
     v[k] = make_uint4(0, 0, 0, 0);
-    wv[k] = make_uint4(0, 0, 0, 0);
     if (c < total) {
-      const int s = cps > 0 ? min(c / cps, ri.nseg - 1) : seg_of(st, ri.nseg, c);
-      const int e0 = (c - (cps > 0 ? s * cps : st.start[s])) * EPC;  // element index inside the segment
+      int s, e0;  // e0: element index inside the segment
+      locate(st, c, s, e0);
       seg[k] = s;
       e0s[k] = e0;
-      vis[k] = !(SOFTMAX && a.causal) || st.klo[s] + e0 <= ri.qpos;
+      vis[k] = active && (!(SOFTMAX && a.causal) || st.klo[s] + e0 <= ri.qpos);
       if (vis[k]) v[k] = *reinterpret_cast<const uint4*>(a.x + st.xoff[s] + (int64_t)e0 * ES);
-      if (wvec) wv[k] = *reinterpret_cast<const uint4*>(a.w + st.woff[s] + (int64_t)e0 * 2);
     }
   }
+  // RMSNorm: while the row's loads are in flight, every wave of the
+  // workgroup helps stage the weights
+  if constexpr (!SOFTMAX) {
+    for (int c = threadIdx.x; c < total; c += kThreads) {
+      int s, e0;
+      locate(st, c, s, e0);
+      const char* wb = a.w + st.woff[s];
+      if (a.dt_w == EA_BF16 && EPC == 8) {  // one 16-byte load: 8 bf16 weights
+        float f[8];
+        unpack<uint16_t>(*reinterpret_cast<const uint4*>(wb + (int64_t)e0 * 2), f);
+        *reinterpret_cast<float4*>(sw + c * EPC) = make_float4(f[0], f[1], f[2], f[3]);
+        *reinterpret_cast<float4*>(sw + c * EPC + 4) = make_float4(f[4], f[5], f[6], f[7]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < EPC; ++i) sw[c * EPC + i] = ld_elem(wb, e0 + i, a.dt_w);
+      }
+    }
+    __syncthreads();
+  }
+  if (!active) return;
   // local partials, then the aggregation across lanes
 #pragma unroll
-  for (int k = 0; k < kMaxK; ++k) {
+  for (int k = 0; k < K; ++k) {
     if (!vis[k]) continue;
     float f[8];
     unpack<XT>(v[k], f);
@@ -177,7 +204,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     m = wave_max(part);
     float l = 0.0f;
 #pragma unroll
-    for (int k = 0; k < kMaxK; ++k) {
+    for (int k = 0; k < K; ++k) {
       if (!vis[k]) continue;
       float f[8];
       unpack<XT>(v[k], f);
@@ -197,7 +224,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
   }
   // write the row
 #pragma unroll
-  for (int k = 0; k < kMaxK; ++k) {
+  for (int k = 0; k < K; ++k) {
     const int c = k * 64 + lane;
     if (c >= total) continue;
     const int s = seg[k];
@@ -211,14 +238,9 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
         const bool ok = vis[k] && (!a.causal || st.klo[s] + e0 + i <= ri.qpos);
         o[i] = ok ? __expf(f[i] - m) * scale : 0.0f;
       }
-    } else if (wvec) {
-      float wf[8];
-      unpack<uint16_t>(wv[k], wf);
-#pragma unroll
-      for (int i = 0; i < EPC; ++i) o[i] = wf[i] * (f[i] * scale);
     } else {
 #pragma unroll
-      for (int i = 0; i < EPC; ++i) o[i] = ld_elem(a.w + st.woff[s], e0 + i, a.dt_w) * (f[i] * scale);
+      for (int i = 0; i < EPC; ++i) o[i] = sw[c * EPC + i] * (f[i] * scale);
     }
     const int64_t yidx = (int64_t)ri.row * st.len[s] + e0;
     char* ybase = a.y + st.yoff[s];
@@ -289,8 +311,16 @@ hipError_t launch_rows(const RowArgs& a, hipStream_t s) {
   if (a.n_rowtasks == 0) return hipSuccess;
   const dim3 grid((uint32_t)a.n_rowtasks), block(kThreads);
   if (a.vec) {
-    if (a.dt_x == EA_BF16) hipLaunchKernelGGL((rows_vec_kernel<uint16_t, SOFTMAX>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((rows_vec_kernel<float, SOFTMAX>), grid, block, 0, s, a);
+    const int64_t chunks = (int64_t)a.row_len * (a.dt_x == EA_BF16 ? 2 : 4) / 16;
+    if (a.dt_x == EA_BF16) {
+      if (chunks <= 4 * 64) hipLaunchKernelGGL((rows_vec_kernel<uint16_t, SOFTMAX, 4>), grid, block, 0, s, a);
+      else if (chunks <= 8 * 64) hipLaunchKernelGGL((rows_vec_kernel<uint16_t, SOFTMAX, 8>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((rows_vec_kernel<uint16_t, SOFTMAX, kMaxK>), grid, block, 0, s, a);
+    } else {
+      if (chunks <= 4 * 64) hipLaunchKernelGGL((rows_vec_kernel<float, SOFTMAX, 4>), grid, block, 0, s, a);
+      else if (chunks <= 8 * 64) hipLaunchKernelGGL((rows_vec_kernel<float, SOFTMAX, 8>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((rows_vec_kernel<float, SOFTMAX, kMaxK>), grid, block, 0, s, a);
+    }
   } else {
     hipLaunchKernelGGL((rows_scalar_kernel<SOFTMAX>), grid, block, 0, s, a);
   }
