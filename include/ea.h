@@ -170,8 +170,8 @@ int ea_relation_block(const ea_relation* rel, int64_t b, int64_t* lo, int64_t* h
      positive finite number; d must be a single block of extent 128; q and k
      block extents multiples of 128; the causal rule needs q and k of the
      same extent; bf16 data.  Scores and softmax in f32; for the P.V product
-     P is split into two bf16 terms (hi + lo, about 16 significant bits) and
-     V is used as stored (bf16), fp32 accumulation.
+     P (in [0, 1]) is rounded to fp16 and V is converted to fp16, so V values
+     must lie within the fp16 range; fp32 accumulation.
    EA_OP_SWIGLU, agg SUM: in = (X "tj", W1 "jk", W2 "jk"), out "tk" =
      silu(X W1) * (X W2), silu(g) = g / (1 + e^-g); bf16 data.
    Errors: EA_ERR_ARG, EA_ERR_SPEC, EA_ERR_DTYPE, EA_ERR_JOIN,
