@@ -435,6 +435,17 @@ struct OpInfo {
   int q_dim = 0, k_dim = 0;
 };
 
+// largest block of a relation, in bytes
+int64_t max_block_bytes(const ea_relation* r) {
+  int64_t n = dtype_size(r->dtype);
+  for (int d = 0; d < r->rank; ++d) {
+    int64_t m = 0;
+    for (int b = 0; b < r->nb[d]; ++b) m = std::max<int64_t>(m, r->splits[d][b + 1] - r->splits[d][b]);
+    n *= m;
+  }
+  return n;
+}
+
 bool is_float_dtype(int32_t dt) { return dt == EA_F32 || dt == EA_BF16 || dt == EA_F16; }
 
 int classify(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation* const* ops,
@@ -1191,12 +1202,15 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
       a.dt_in = in[0]->dtype;
       a.dt_out = out->dtype;
       {
-        // direct-to-LDS kernel: contracted block extents multiples of 32 and
-        // at most kGemmMaxTuples tuples per unit; else the register-staged one
+        // direct-to-LDS kernel: contracted block extents multiples of 32, at
+        // most kGemmMaxTuples tuples per unit and operand blocks below 4 GiB
+        // (32-bit lane offsets); else the register-staged one
         bool k32 = true;
         for (int64_t v : in[0]->splits[1]) k32 &= v % 32 == 0;
         const int64_t per_unit = (in[0]->nb[1] + plan->gemm_parts - 1) / plan->gemm_parts;
-        a.direct = k32 && per_unit <= kGemmMaxTuples;
+        bool small = true;
+        for (int i = 0; i < n_in; ++i) small &= max_block_bytes(in[i]) < (int64_t(1) << 32);
+        a.direct = k32 && per_unit <= kGemmMaxTuples && small;
       }
       a.partials = plan->part_o;
       a.counters = plan->counters;

@@ -94,6 +94,43 @@ def test_gemm_ragged_blocks(kmajor, out_dtype):
     assert_close(values(Y), expected(ref, out_dtype), what=f"gemm kmajor={kmajor} {out_dtype}")
 
 
+@pytest.mark.parametrize("ragged", [False, True])
+@pytest.mark.parametrize("out_dtype", ["f16", "f32"])
+def test_gemm_f16_inputs(ragged, out_dtype):
+    """fp16 operands take the same matrix-core paths as bf16 (f16 MFMA):
+    32-aligned blocks the direct-to-LDS pipeline, ragged ones the register-
+    staged one."""
+    rng = np.random.default_rng(9)
+    T, J, K = 320, 384, 264
+    if ragged:
+        pt = synth.random_splits(T, 3, rng)
+        pj = synth.random_splits(J, 3, rng, quantum=8)
+        pk = synth.random_splits(K, 2, rng, quantum=8)
+    else:
+        pt, pj, pk = synth.splits(T, 128), synth.splits(J, 128), [0, 128, 264]
+    x = synth.normal((T, J), 35, dtype="f16")
+    w = synth.normal((K, J), 36, 0.05, dtype="f16")
+    X, W = upload(x, "f16", [pt, pj]), upload(w, "f16", [pk, pj])
+    Y = empty((T, K), out_dtype, [pt, pk])
+    ea.joinagg("tj,kj->tk", ea.JOIN_MUL, ea.AGG_SUM, [X, W], Y)
+    ref = oracle.matmul(synth.to_f64(x, "f16"), synth.to_f64(w, "f16").T)
+    assert_close(values(Y), expected(ref, out_dtype), what=f"f16 gemm ragged={ragged} -> {out_dtype}")
+
+
+def test_swiglu_f16_inputs():
+    T, H, F = 256, 384, 256
+    pt, ph, pf = synth.splits(T, 128), synth.splits(H, 128), synth.splits(F, 128)
+    x = synth.normal((T, H), 54, dtype="f16")
+    wg = synth.normal((H, F), 55, 0.05, dtype="f16")
+    wu = synth.normal((H, F), 56, 0.05, dtype="f16")
+    X, G, U = upload(x, "f16", [pt, ph]), upload(wg, "f16", [ph, pf]), upload(wu, "f16", [ph, pf])
+    A = empty((T, F), "f16", [pt, pf])
+    ea.joinagg("tj,jk,jk->tk", ea.OP_SWIGLU, ea.AGG_SUM, [X, G, U], A)
+    fx = synth.to_f64(x, "f16")
+    ref = oracle.silu_mul(oracle.matmul(fx, synth.to_f64(wg, "f16")), oracle.matmul(fx, synth.to_f64(wu, "f16")))
+    assert_close(values(A), expected(ref, "f16"), what="swiglu f16")
+
+
 def test_gemm_integer_data_bitexact_and_residual():
     T, J, K = 256, 512, 384
     pt, pj, pk = synth.splits(T, 128), synth.splits(J, 128), synth.splits(K, 128)
