@@ -675,8 +675,8 @@ int build_generic(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_rela
 // with t_step ~ 1 us per 64-deep K step of a full tile and the merge writing
 // and reading one 256 KiB fp32 partial per unit at ~4 TB/s.
 // Units are then ordered so that the workgroups one XCD receives (ids
-// congruent mod 8) come from one contiguous stretch of the natural order and
-// share operand blocks in that XCD's L2.
+// congruent mod 8) form a compact rectangle of the tile grid and share
+// operand panels in that XCD's L2.
 struct GemmPlanInfo {
   std::vector<GemmTile> units;
   int32_t slots = 0, counters = 0;
@@ -739,22 +739,61 @@ GemmPlanInfo gemm_units(const ea_relation* a, const ea_relation* c, int tn) {
       info.counters += 1;
     }
   }
-  const size_t n = all.size(), nx = 8;
-  std::vector<std::vector<GemmTile>> q(nx);
-  for (size_t i = 0; i < n; ++i) q[std::min(nx - 1, i * nx / std::max<size_t>(n, 1))].push_back(all[i]);
+  // XCD-aware order.  Workgroup i runs on XCD i % 8, and the eight XCDs have
+  // private L2 caches, so each XCD gets a compact rectangle of the tile grid
+  // (global tile rows mi x tile columns ni) of one part: its workgroups then
+  // share the fewest distinct A row panels and B column panels at every K
+  // step.  With P parts and P dividing 8, each part has 8 / P XCDs; else
+  // every part is spread over all eight.
+  std::vector<int> mrow(c->nb[0] + 1, 0), ncol(c->nb[1] + 1, 0);
+  for (int b = 0; b < c->nb[0]; ++b)
+    mrow[b + 1] = mrow[b] + (int)((c->splits[0][b + 1] - c->splits[0][b] + kGemmTM - 1) / kGemmTM);
+  for (int b = 0; b < c->nb[1]; ++b) ncol[b + 1] = ncol[b] + (int)((c->splits[1][b + 1] - c->splits[1][b] + tn - 1) / tn);
+  const int mt = mrow.back(), ntl = ncol.back();
+  const int nx = 8;
+  const bool split_parts = 8 % best_p == 0;
+  const int per_part = split_parts ? 8 / best_p : 8;
+  int gr = 1, gc = per_part;
+  double best_perim = 1e300;
+  for (int r = 1; r <= per_part; ++r) {
+    if (per_part % r) continue;
+    const int cc = per_part / r;
+    const double perim = (double)mt / r + (double)ntl / cc + (r > mt ? 1e6 : 0) + (cc > ntl ? 1e6 : 0);
+    if (perim < best_perim) {
+      best_perim = perim;
+      gr = r;
+      gc = cc;
+    }
+  }
+  struct Keyed {
+    int64_t key;
+    GemmTile t;
+  };
+  std::vector<std::vector<Keyed>> q(nx);
+  for (const GemmTile& t : all) {
+    block_coords(c, t.block, co);
+    const int mi = mrow[co[0]] + t.m0 / kGemmTM, ni = ncol[co[1]] + t.n0 / tn;
+    const int rb = (int)((int64_t)mi * gr / std::max(mt, 1)), cb = (int)((int64_t)ni * gc / std::max(ntl, 1));
+    const int region = rb * gc + cb;
+    const int x = split_parts ? (t.part * per_part + region) % nx : region % nx;
+    // inside a region: part, then 4-row stripes walked column by column
+    const int64_t key = (((int64_t)t.part * (mt / 4 + 1) + mi / 4) * (ntl + 1) + ni) * 4 + mi % 4;
+    q[x].push_back(Keyed{key, t});
+  }
+  for (auto& v : q) std::stable_sort(v.begin(), v.end(), [](const Keyed& x, const Keyed& y) { return x.key < y.key; });
+  const size_t n = all.size();
   std::vector<size_t> head(nx, 0);
   info.units.reserve(n);
   for (size_t p = 0; info.units.size() < n; ++p) {
     const size_t x = p % nx;
     if (head[x] < q[x].size()) {
-      info.units.push_back(q[x][head[x]++]);
+      info.units.push_back(q[x][head[x]++].t);
       continue;
     }
-    for (size_t y = 0; y < nx; ++y)
-      if (head[y] < q[y].size()) {
-        info.units.push_back(q[y][head[y]++]);
-        break;
-      }
+    size_t y_best = nx;  // this XCD has run out: take from the fullest queue
+    for (size_t y = 0; y < (size_t)nx; ++y)
+      if (head[y] < q[y].size() && (y_best == nx || q[y].size() - head[y] > q[y_best].size() - head[y_best])) y_best = y;
+    info.units.push_back(q[y_best][head[y_best]++].t);
   }
   return info;
 }
