@@ -292,6 +292,12 @@ struct Image {
 
 enum Kind { K_GENERIC = 1, K_GEMM, K_RMSNORM, K_SOFTMAX, K_ATTENTION, K_REPART };
 
+// row-reduction plan constants (see RowArgs)
+struct RowLayout {
+  int32_t row_len = 0, vec = 0, cps = 0, affine = 0, seg_len = 0, nseg = 0;
+  int64_t xs = 0, ys = 0, ws = 0, wbase = 0;
+};
+
 struct Plan {
   int device = 0;
   Kind kind = K_GENERIC;
@@ -312,9 +318,7 @@ struct Plan {
   int b_kmajor = 0;
   int gemm_parts = 1;
   // rows
-  int32_t row_len = 0;
-  int32_t row_vec = 0;
-  int32_t row_cps = 0;
+  RowLayout rows;
   // attention scratch
   float* part_o = nullptr;
   float* part_ml = nullptr;
@@ -799,46 +803,80 @@ GemmPlanInfo gemm_units(const ea_relation* a, const ea_relation* c, int tn) {
 }
 
 int build_rows(const Spec& sp, const ea_relation* const* ops, const OpInfo& oi, Image* img, Extra* ex,
-               int32_t* row_len, int32_t* vec, int32_t* seg_chunks) {
+               RowLayout* lay) {
   // rows of a group: points of the group letters' box; every group has the
   // same structure as block (g) of the output restricted to the group letters.
   const ea_relation* y = ops[sp.n_in];
-  const int r = y->rank;
-  std::vector<int32_t> tasks;  // (group, first row, n rows, 0)
+  const ea_relation* x = ops[0];
+  const ea_relation* w = oi.kind == K_RMSNORM ? ops[1] : nullptr;
+  const int r = y->rank, dl = r - 1;
+  const int es = dtype_size(x->dtype), esy = dtype_size(y->dtype);
+  lay->row_len = (int32_t)y->shape[dl];
+  bool aligned = true;
+  for (int b = 0; b < x->nb[dl]; ++b) aligned &= (x->splits[dl][b + 1] - x->splits[dl][b]) * es % 16 == 0;
+  lay->vec = rows_vec_ok(y->shape[dl], x->nb[dl], aligned, es) ? 1 : 0;
+  // even segments (all but the last of one chunk count, the last no longer)
+  const int64_t first = (x->splits[dl][1] - x->splits[dl][0]) * es / 16;
+  bool even = aligned;
+  for (int b = 0; b < x->nb[dl]; ++b) {
+    const int64_t n = (x->splits[dl][b + 1] - x->splits[dl][b]) * es / 16;
+    even &= b + 1 < x->nb[dl] ? n == first : n <= first;
+  }
+  lay->cps = even ? (int32_t)first : 0;
+  // affine layout: equal segments, x and y with one partition (w along the
+  // normalised letter too), and block offsets at fixed strides along it
+  const int nseg = x->nb[dl];
+  const int64_t L = x->splits[dl][1] - x->splits[dl][0];
+  bool aff = lay->vec && even && x->rank == r;
+  for (int b = 0; aff && b < nseg; ++b) aff &= x->splits[dl][b + 1] - x->splits[dl][b] == L;
+  for (int d = 0; aff && d < r; ++d) aff &= x->splits[d] == y->splits[d];
+  if (aff && w) aff &= w->rank == 1 && w->splits[0] == x->splits[dl];
+  const int64_t xs = nseg > 1 ? x->off[1] - x->off[0] : 0, ys = nseg > 1 ? y->off[1] - y->off[0] : 0;
+  const int64_t ws = w && nseg > 1 ? w->off[1] - w->off[0] : 0;
+  for (int64_t b = 0; aff && b < x->nblocks; ++b) {
+    const int64_t g = b / nseg, sg = b % nseg;
+    aff &= x->off[b] == x->off[g * nseg] + sg * xs && y->off[b] == y->off[g * nseg] + sg * ys;
+  }
+  for (int sg = 0; aff && w && sg < nseg; ++sg) aff &= w->off[sg] == w->off[0] + sg * ws;
+  lay->affine = aff ? 1 : 0;
+  lay->seg_len = (int32_t)L;
+  lay->nseg = nseg;
+  lay->xs = xs;
+  lay->ys = ys;
+  lay->ws = ws;
+  lay->wbase = w ? w->off[0] : 0;
+
+  std::vector<RowTask> tasks;
   // groups enumerate block coordinates of the first r-1 dims, row-major
   int64_t n_groups = 1;
   for (int d = 0; d < r - 1; ++d) n_groups *= y->nb[d];
   int32_t c[kMaxRank] = {};
   const int rows_per_task = 4;
+  const int qd = r - 2;
   for (int64_t g = 0; g < n_groups; ++g) {
     int64_t rem = g;
     for (int d = r - 2; d >= 0; --d) { c[d] = (int32_t)(rem % y->nb[d]); rem /= y->nb[d]; }
     int64_t rows = 1;
     for (int d = 0; d < r - 1; ++d) rows *= y->splits[d][c[d] + 1] - y->splits[d][c[d]];
     for (int64_t r0 = 0; r0 < rows; r0 += rows_per_task) {
-      tasks.push_back((int32_t)g);
-      tasks.push_back((int32_t)r0);
-      tasks.push_back((int32_t)std::min<int64_t>(rows_per_task, rows - r0));
-      tasks.push_back(0);
+      RowTask t;
+      memset(&t, 0, sizeof(t));
+      t.g = (int32_t)g;
+      t.row0 = (int32_t)r0;
+      t.nrows = (int32_t)std::min<int64_t>(rows_per_task, rows - r0);
+      if (qd >= 0) {
+        t.qlo = (int32_t)y->splits[qd][c[qd]];
+        t.qext = (int32_t)(y->splits[qd][c[qd] + 1] - y->splits[qd][c[qd]]);
+      }
+      if (aff) {
+        t.xrow = x->off[g * nseg] + r0 * L * es;
+        t.yrow = y->off[g * nseg] + r0 * L * esy;
+      }
+      tasks.push_back(t);
     }
   }
-  *row_len = (int32_t)y->shape[r - 1];
-  const ea_relation* x = ops[0];
-  const int es = dtype_size(x->dtype);
-  bool aligned = true;
-  for (int b = 0; b < x->nb[r - 1]; ++b) aligned &= (x->splits[r - 1][b + 1] - x->splits[r - 1][b]) * es % 16 == 0;
-  *vec = rows_vec_ok(y->shape[r - 1], x->nb[r - 1], aligned, es) ? 1 : 0;
-  // even segments (all but the last of one chunk count, the last no longer)
-  const int64_t first = (x->splits[r - 1][1] - x->splits[r - 1][0]) * es / 16;
-  bool even = aligned;
-  for (int b = 0; b < x->nb[r - 1]; ++b) {
-    const int64_t n = (x->splits[r - 1][b + 1] - x->splits[r - 1][b]) * es / 16;
-    even &= b + 1 < x->nb[r - 1] ? n == first : n <= first;
-  }
-  *seg_chunks = even ? (int32_t)first : 0;
   ex->work = img->put_vec(tasks);
-  ex->n_work = (int64_t)tasks.size() / 4;
-  (void)oi;
+  ex->n_work = (int64_t)tasks.size();
   return EA_OK;
 }
 
@@ -951,7 +989,7 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
       break;
     }
     case K_RMSNORM:
-    case K_SOFTMAX: e = build_rows(sp, ops, oi, &img, &ex, &p->row_len, &p->row_vec, &p->row_cps); break;
+    case K_SOFTMAX: e = build_rows(sp, ops, oi, &img, &ex, &p->rows); break;
     case K_ATTENTION: e = build_attention(ops, oi, ji, oi.causal, &img, &ex); break;
     default: e = fail(EA_ERR_UNSUPPORTED, "internal: unknown plan kind");
   }
@@ -1274,14 +1312,21 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
       a.blk_y = plan->d_blk[n_in];
       a.y = (char*)out->data;
       a.dt_y = out->dtype;
-      a.rows = (const int32_t*)plan->d_work;
+      a.tasks = (const RowTask*)plan->d_work;
       a.n_rowtasks = (int32_t)plan->n_work;
       a.tuple_stride = n_in + 1;
       a.rank = out->rank;
       a.causal = oi.causal;
-      a.row_len = plan->row_len;
-      a.vec = plan->row_vec;
-      a.seg_chunks = plan->row_cps;
+      a.row_len = plan->rows.row_len;
+      a.vec = plan->rows.vec;
+      a.seg_chunks = plan->rows.cps;
+      a.affine = plan->rows.affine;
+      a.seg_len = plan->rows.seg_len;
+      a.nseg = plan->rows.nseg;
+      a.xs = plan->rows.xs;
+      a.ys = plan->rows.ys;
+      a.ws = plan->rows.ws;
+      a.wbase = plan->rows.wbase;
       EA_HIP_TRY(plan->kind == K_RMSNORM ? launch_rmsnorm(a, s) : launch_softmax(a, s));
       break;
     }

@@ -161,6 +161,16 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
 // of its group (RMSNorm: column blocks of x with the matching w blocks;
 // softmax: key blocks).
 // ---------------------------------------------------------------------------
+// One workgroup's rows: up to four consecutive rows of one group.  The
+// remaining fields serve the affine layout (see RowArgs::affine): the query
+// block's start and extent along the causal letter, and the byte offsets of
+// the task's first row in the group's first x and y blocks.
+struct RowTask {
+  int32_t g, row0, nrows, qlo;
+  int32_t qext, pad;
+  int64_t xrow, yrow;
+};
+
 struct RowArgs {
   const int32_t* tuples;
   const int32_t* goff;
@@ -170,7 +180,7 @@ struct RowArgs {
   const char* x;
   const char* w;
   char* y;
-  const int32_t* rows;   // per workgroup row range: (group, first row, n rows, -)
+  const RowTask* tasks;  // one per workgroup
   int32_t n_rowtasks;
   int32_t tuple_stride;
   int32_t rank;          // rank of x / y
@@ -181,6 +191,14 @@ struct RowArgs {
   int32_t seg_chunks;    // register path: 16-byte chunks of every segment but the
                          // last (which has at most as many), or 0 if uneven
   float eps;
+  // Affine layout (set on the host when it holds): every segment has seg_len
+  // elements, x, y and w have the same partition of the normalised letter,
+  // and segment s of a row sits at a fixed byte stride from segment 0 (xs,
+  // ys, ws; w's segment 0 at wbase).  Every address then follows from the
+  // task record, with no tuple or block-table loads before the row loads.
+  int32_t affine;
+  int32_t seg_len, nseg;
+  int64_t xs, ys, ws, wbase;
 };
 
 bool rows_vec_ok(int64_t row_len, int64_t max_segments, bool seg_aligned, int es);

@@ -39,10 +39,10 @@ struct RowInfo {
 };
 
 __device__ __forceinline__ RowInfo row_info(const RowArgs& a, int task_row) {
-  const int32_t* task = a.rows + 4 * blockIdx.x;
+  const RowTask& task = a.tasks[blockIdx.x];
   RowInfo ri;
-  const int g = task[0];
-  ri.row = task[1] + task_row;
+  const int g = task.g;
+  ri.row = task.row0 + task_row;
   ri.t0 = a.goff[g];
   ri.nseg = a.goff[g + 1] - ri.t0;
   ri.qpos = 0;
@@ -115,31 +115,59 @@ __device__ __forceinline__ void unpack<float>(const uint4& v, float (&f)[8]) {
 // ---------------------------------------------------------------------------
 // K: 16-byte chunks of the row per lane (4, 8 or 16), chosen from the row
 // length so that short rows keep few registers and many waves per SIMD.
-template <typename XT, bool SOFTMAX, int K>
+// AFF: affine layout (RowArgs::affine): addresses come from the task record
+// and the strides, so the row loads go out at once; otherwise each wave
+// first builds its row's segment table from the join's tuples.
+template <typename XT, bool SOFTMAX, int K, bool AFF>
 __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
-  __shared__ SegTable tabs[kThreads / 64];
+  __shared__ SegTable tabs[AFF ? 1 : kThreads / 64];
   // RMSNorm: the weights of the group's row, in the row's chunk order as
   // fp32 (EPC values per chunk), staged once for the workgroup's rows
   constexpr int ES = sizeof(XT), EPC = 16 / ES;
   __shared__ float sw[SOFTMAX ? 1 : K * 64 * EPC];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int32_t* task = a.rows + 4 * blockIdx.x;
-  const bool active = wid < task[2];  // waves past the task's rows only help stage the weights
-  SegTable& st = tabs[wid];
-  const RowInfo ri = row_info(a, wid);  // every row of the task is in the same group
-  const int total = fill_segments(a, ri, st, lane, ES);
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const RowTask& task = a.tasks[blockIdx.x];
+  const bool active = wid < ld_uniform(&task.nrows);  // waves past the task's rows only help stage the weights
+  const int esy = a.dt_y == EA_F32 ? 4 : 2;
+  SegTable& st = tabs[AFF ? 0 : wid];
+  int total, nseg;
+  int qpos = 0;
+  int64_t xrow = 0, yrow = 0;
+  RowInfo ri{};
+  if constexpr (AFF) {
+    nseg = a.nseg;
+    total = nseg * a.seg_chunks;
+    const int row = ld_uniform(&task.row0) + wid;
+    xrow = ld_uniform(&task.xrow) + (int64_t)wid * a.seg_len * ES;
+    yrow = ld_uniform(&task.yrow) + (int64_t)wid * a.seg_len * esy;
+    if (SOFTMAX && a.causal) qpos = ld_uniform(&task.qlo) + row % ld_uniform(&task.qext);
+  } else {
+    ri = row_info(a, wid);  // every row of the task is in the same group
+    total = fill_segments(a, ri, st, lane, ES);
+    nseg = ri.nseg;
+    qpos = ri.qpos;
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
 
   // Segment of a chunk: direct when every segment but the last has the same
   // chunk count (the usual even split, ragged tail allowed), else a scan of
   // the segment table.
   const int cps = a.seg_chunks;
-  auto locate = [&](const SegTable& t, int c, int& s, int& e0) {
-    s = cps > 0 ? min(c / cps, ri.nseg - 1) : seg_of(t, ri.nseg, c);
-    e0 = (c - (cps > 0 ? s * cps : t.start[s])) * EPC;
+  auto locate = [&](int c, int& sg, int& e0) {
+    sg = cps > 0 ? min(c / cps, nseg - 1) : seg_of(st, nseg, c);
+    e0 = (c - (cps > 0 ? sg * cps : st.start[sg])) * EPC;
   };
+  auto klo = [&](int sg) { return AFF ? sg * a.seg_len : st.klo[sg]; };
+  auto x_at = [&](int sg, int e0) -> const char* {
+    return AFF ? a.x + xrow + sg * a.xs + (int64_t)e0 * ES : a.x + st.xoff[sg] + (int64_t)e0 * ES;
+  };
+  auto y_at = [&](int sg, int e0) -> char* {
+    return AFF ? a.y + yrow + sg * a.ys + (int64_t)e0 * esy
+               : a.y + st.yoff[sg] + ((int64_t)ri.row * st.len[sg] + e0) * esy;
+  };
+  auto w_at = [&](int sg) -> const char* { return AFF ? a.w + a.wbase + sg * a.ws : a.w + st.woff[sg]; };
 
   uint4 v[K];
   int seg[K], e0s[K];
@@ -153,21 +181,28 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     e0s[k] = 0;
     v[k] = make_uint4(0, 0, 0, 0);
     if (c < total) {
-      int s, e0;  // e0: element index inside the segment
-      locate(st, c, s, e0);
-      seg[k] = s;
+      int sg, e0;  // e0: element index inside the segment
+      locate(c, sg, e0);
+      seg[k] = sg;
       e0s[k] = e0;
-      vis[k] = active && (!(SOFTMAX && a.causal) || st.klo[s] + e0 <= ri.qpos);
-      if (vis[k]) v[k] = *reinterpret_cast<const uint4*>(a.x + st.xoff[s] + (int64_t)e0 * ES);
+      vis[k] = active && (!(SOFTMAX && a.causal) || klo(sg) + e0 <= qpos);
+      if (vis[k]) v[k] = *reinterpret_cast<const uint4*>(x_at(sg, e0));
     }
   }
   // RMSNorm: while the row's loads are in flight, every wave of the
   // workgroup helps stage the weights
   if constexpr (!SOFTMAX) {
     for (int c = threadIdx.x; c < total; c += kThreads) {
-      int s, e0;
-      locate(st, c, s, e0);
-      const char* wb = a.w + st.woff[s];
+      int sg, e0;
+      if constexpr (AFF) {
+        sg = c / cps;
+        e0 = (c - sg * cps) * EPC;
+      } else {
+        // the segment table of the wave that owns this chunk's row does not
+        // matter: the weights depend only on the group, shared by the task
+        locate(c, sg, e0);
+      }
+      const char* wb = w_at(sg);
       if (a.dt_w == EA_BF16 && EPC == 8) {  // one 16-byte load: 8 bf16 weights
         float f[8];
         unpack<uint16_t>(*reinterpret_cast<const uint4*>(wb + (int64_t)e0 * 2), f);
@@ -187,12 +222,11 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     if (!vis[k]) continue;
     float f[8];
     unpack<XT>(v[k], f);
-    const int s = seg[k];
-    const int e0 = e0s[k];
+    const int k0 = klo(seg[k]) + e0s[k];
 #pragma unroll
     for (int i = 0; i < EPC; ++i) {
       if constexpr (SOFTMAX) {
-        const bool ok = !a.causal || st.klo[s] + e0 + i <= ri.qpos;
+        const bool ok = !a.causal || k0 + i <= qpos;
         part = ok ? fmaxf(part, f[i]) : part;
       } else {
         part += f[i] * f[i];
@@ -208,11 +242,10 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
       if (!vis[k]) continue;
       float f[8];
       unpack<XT>(v[k], f);
-      const int s = seg[k];
-      const int e0 = e0s[k];
+      const int k0 = klo(seg[k]) + e0s[k];
 #pragma unroll
       for (int i = 0; i < EPC; ++i) {
-        const bool ok = !a.causal || st.klo[s] + e0 + i <= ri.qpos;
+        const bool ok = !a.causal || k0 + i <= qpos;
         l += ok ? __expf(f[i] - m) : 0.0f;
       }
     }
@@ -227,35 +260,35 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
   for (int k = 0; k < K; ++k) {
     const int c = k * 64 + lane;
     if (c >= total) continue;
-    const int s = seg[k];
+    const int sg = seg[k];
     const int e0 = e0s[k];
     float f[8];
     unpack<XT>(v[k], f);
     float o[8];
     if constexpr (SOFTMAX) {
+      const int k0 = klo(sg) + e0;
 #pragma unroll
       for (int i = 0; i < EPC; ++i) {
-        const bool ok = vis[k] && (!a.causal || st.klo[s] + e0 + i <= ri.qpos);
+        const bool ok = vis[k] && (!a.causal || k0 + i <= qpos);
         o[i] = ok ? __expf(f[i] - m) * scale : 0.0f;
       }
     } else {
 #pragma unroll
       for (int i = 0; i < EPC; ++i) o[i] = sw[c * EPC + i] * (f[i] * scale);
     }
-    const int64_t yidx = (int64_t)ri.row * st.len[s] + e0;
-    char* ybase = a.y + st.yoff[s];
+    char* yp = y_at(sg, e0);
     if (a.dt_y == EA_BF16 && ES == 2) {
       uint4 pk;
       uint32_t* w = reinterpret_cast<uint32_t*>(&pk);
 #pragma unroll
       for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f32_to_bf16(o[2 * i]) | ((uint32_t)f32_to_bf16(o[2 * i + 1]) << 16);
-      *reinterpret_cast<uint4*>(ybase + yidx * 2) = pk;
+      *reinterpret_cast<uint4*>(yp) = pk;
     } else if (a.dt_y == EA_F32 && ES == 4) {
-      *reinterpret_cast<uint4*>(ybase + yidx * 4) =
+      *reinterpret_cast<uint4*>(yp) =
           make_uint4(__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]), __float_as_uint(o[3]));
     } else {
 #pragma unroll
-      for (int i = 0; i < EPC; ++i) st_elem(ybase, yidx + i, a.dt_y, o[i]);
+      for (int i = 0; i < EPC; ++i) st_elem(yp, i, a.dt_y, o[i]);
     }
   }
 }
@@ -266,8 +299,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
 template <bool SOFTMAX>
 __global__ __launch_bounds__(kThreads) void rows_scalar_kernel(RowArgs a) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int32_t* task = a.rows + 4 * blockIdx.x;
-  if (wid >= task[2]) return;
+  if (wid >= a.tasks[blockIdx.x].nrows) return;
   const RowInfo ri = row_info(a, wid);
   const int d_last = a.rank - 1;
   auto visit = [&](auto&& fn) {
@@ -306,21 +338,27 @@ __global__ __launch_bounds__(kThreads) void rows_scalar_kernel(RowArgs a) {
   }
 }
 
+template <typename XT, bool SOFTMAX, int K>
+void launch_vec(const RowArgs& a, dim3 grid, dim3 block, hipStream_t s) {
+  if (a.affine) hipLaunchKernelGGL((rows_vec_kernel<XT, SOFTMAX, K, true>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((rows_vec_kernel<XT, SOFTMAX, K, false>), grid, block, 0, s, a);
+}
+
+template <typename XT, bool SOFTMAX>
+void launch_vec_k(const RowArgs& a, int64_t chunks, dim3 grid, dim3 block, hipStream_t s) {
+  if (chunks <= 4 * 64) launch_vec<XT, SOFTMAX, 4>(a, grid, block, s);
+  else if (chunks <= 8 * 64) launch_vec<XT, SOFTMAX, 8>(a, grid, block, s);
+  else launch_vec<XT, SOFTMAX, kMaxK>(a, grid, block, s);
+}
+
 template <bool SOFTMAX>
 hipError_t launch_rows(const RowArgs& a, hipStream_t s) {
   if (a.n_rowtasks == 0) return hipSuccess;
   const dim3 grid((uint32_t)a.n_rowtasks), block(kThreads);
   if (a.vec) {
     const int64_t chunks = (int64_t)a.row_len * (a.dt_x == EA_BF16 ? 2 : 4) / 16;
-    if (a.dt_x == EA_BF16) {
-      if (chunks <= 4 * 64) hipLaunchKernelGGL((rows_vec_kernel<uint16_t, SOFTMAX, 4>), grid, block, 0, s, a);
-      else if (chunks <= 8 * 64) hipLaunchKernelGGL((rows_vec_kernel<uint16_t, SOFTMAX, 8>), grid, block, 0, s, a);
-      else hipLaunchKernelGGL((rows_vec_kernel<uint16_t, SOFTMAX, kMaxK>), grid, block, 0, s, a);
-    } else {
-      if (chunks <= 4 * 64) hipLaunchKernelGGL((rows_vec_kernel<float, SOFTMAX, 4>), grid, block, 0, s, a);
-      else if (chunks <= 8 * 64) hipLaunchKernelGGL((rows_vec_kernel<float, SOFTMAX, 8>), grid, block, 0, s, a);
-      else hipLaunchKernelGGL((rows_vec_kernel<float, SOFTMAX, kMaxK>), grid, block, 0, s, a);
-    }
+    if (a.dt_x == EA_BF16) launch_vec_k<uint16_t, SOFTMAX>(a, chunks, grid, block, s);
+    else launch_vec_k<float, SOFTMAX>(a, chunks, grid, block, s);
   } else {
     hipLaunchKernelGGL((rows_scalar_kernel<SOFTMAX>), grid, block, 0, s, a);
   }

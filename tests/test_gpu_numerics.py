@@ -239,6 +239,36 @@ def test_causal_softmax_full_size_key_blocks():
     assert np.all(got[:, mask] == 0)
 
 
+def test_rmsnorm_vector_path_short_last_segment():
+    # 16-byte segments, all but the last of one length: register path with the
+    # direct segment lookup, but not the affine layout
+    T, C = 40, 1032
+    pt, pc = [0, 24, 40], [0, 512, 1024, 1032]
+    x = synth.normal((T, C), 65, dtype="bf16")
+    wv = synth.uniform((C,), 66, 0.5, 1.5, dtype="bf16")
+    X, Wt = upload(x, "bf16", [pt, pc]), upload(wv, "bf16", [pc])
+    Y = empty((T, C), "bf16", [pt, pc])
+    ea.joinagg("tc,c->tc", ea.OP_RMSNORM, ea.AGG_SUM, [X, Wt], Y, eps=1e-6)
+    ref = oracle.rmsnorm(synth.to_f64(x, "bf16"), synth.to_f64(wv, "bf16"), 1e-6)
+    assert_close(values(Y), expected(ref, "bf16"), what="rmsnorm short last segment")
+
+
+def test_causal_softmax_two_heads_per_block():
+    # equal blocks (affine layout), two heads per block: a group's rows run
+    # over both heads, so the query position wraps at the query block's extent
+    H, Q, K = 4, 96, 128
+    ph, pq, pk = synth.splits(H, 2), [0, 48, 96], synth.splits(K, 32)
+    s = synth.normal((H, Q, K), 72, 2.0, dtype="bf16")
+    Sr = upload(s, "bf16", [ph, pq, pk])
+    P = empty((H, Q, K), "bf16", [ph, pq, pk])
+    ea.joinagg("hqk->hqk", ea.OP_SOFTMAX, ea.AGG_LSE, [Sr], P, causal=True)
+    ref = oracle.softmax(synth.to_f64(s, "bf16"), True)
+    got = values(P)
+    assert_close(got, expected(ref, "bf16"), what="causal softmax, two heads per block")
+    mask = np.triu(np.ones((Q, K), dtype=bool), 1)
+    assert np.all(got[:, mask] == 0)
+
+
 @pytest.mark.parametrize("causal", [False, True])
 def test_softmax_ragged_and_f32(causal):
     rng = np.random.default_rng(9)
