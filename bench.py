@@ -157,8 +157,10 @@ def reductions_workload():
     Y = ea.Relation((4096, 4096), "bf16", w["px"])
     S = ea.from_dense(_dev(w["s"]), "bf16", w["ps"])
     P = ea.Relation((4, 2048, 2048), "bf16", w["ps"])
-    rms = lambda: ea.joinagg("tc,c->tc", ea.OP_RMSNORM, ea.AGG_SUM, [X, Wt], Y, eps=w["eps"])
-    sm = lambda: ea.joinagg("hqk->hqk", ea.OP_SOFTMAX, ea.AGG_LSE, [S], P, causal=True)
+    # standalone operators whose outputs nothing reads next: streamed stores
+    st = ea.STORE_STREAM
+    rms = lambda: ea.joinagg("tc,c->tc", ea.OP_RMSNORM, ea.AGG_SUM, [X, Wt], Y, eps=w["eps"], store=st)
+    sm = lambda: ea.joinagg("hqk->hqk", ea.OP_SOFTMAX, ea.AGG_LSE, [S], P, causal=True, store=st)
 
     def step():
         rms()
@@ -170,7 +172,8 @@ def reductions_workload():
                                             "causal_softmax": dict(fn=sm, bytes=sm_bytes)},
                 dominant="rmsnorm", bytes=rms_bytes + sm_bytes,
                 config={"workload": "reductions", "rmsnorm": "x[4096,4096] bf16, 8 column blocks",
-                        "softmax": "s[4,2048,2048] bf16 causal, 256-key blocks", "dtype": "bf16"}, cpu=None)
+                        "softmax": "s[4,2048,2048] bf16 causal, 256-key blocks", "dtype": "bf16",
+                        "store": "stream"}, cpu=None)
 
 
 def repartition_workload():
@@ -190,12 +193,12 @@ def repartition_workload():
     g = torch.Generator(device="cuda")
     g.manual_seed(601)
     src.bytes().copy_(torch.randint(0, 256, (src.nbytes,), dtype=torch.uint8, device="cuda", generator=g))
-    fn = lambda: ea.repartition(src, dst)
+    fn = lambda: ea.repartition(src, dst, store=ea.STORE_STREAM)  # 256 MiB: larger than the caches
     nbytes = 2 * shape[0] * shape[1] * 2
     return dict(step=fn, flops=0.0, bytes=nbytes, comps={"repartition": dict(fn=fn, bytes=nbytes)},
                 dominant="repartition",
                 config={"workload": "repartition_256MiB", "shape": list(shape), "dtype": "bf16",
-                        "from": "512x512 blocks", "to": "128 x 16384 blocks"}, cpu=None)
+                        "from": "512x512 blocks", "to": "128 x 16384 blocks", "store": "stream"}, cpu=None)
 
 
 # ---------------------------------------------------------------------------

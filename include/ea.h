@@ -95,12 +95,25 @@ extern "C" {
 typedef struct ea_relation ea_relation;
 
 /* Per-call parameters.  Zero-initialise and set what the operation uses. */
+/* Output store policy (ea_params.store, ea_repartition_ex).  CACHED: plain
+   stores; the output stays in the GPU's caches for a kernel that reads it
+   next.  STREAM: non-temporal stores; the output is streamed towards memory,
+   which suits an output that nothing reads soon or that exceeds the caches
+   (the end of a kernel then has no dirty cache lines of it to write back).
+   Results are bit-identical under both. */
+#define EA_STORE_CACHED 0
+#define EA_STORE_STREAM 1
+
 typedef struct ea_params {
   float eps;    /* EA_OP_RMSNORM: added to the mean square (e.g. 1e-6)       */
   float scale;  /* EA_OP_ATTENTION: multiplier of the q.k scores (> 0)       */
   int32_t causal; /* EA_OP_SOFTMAX / EA_OP_ATTENTION: 1 = key position k is
                      visible to query position q iff k <= q (0-based)        */
-  int32_t reserved;
+  int32_t store;  /* EA_STORE_CACHED (0, default) or EA_STORE_STREAM (1);
+                     honoured by EA_OP_RMSNORM and EA_OP_SOFTMAX (the block
+                     GEMM, attention and general einsum paths store plainly,
+                     their outputs feeding the next operator).  Other
+                     values: EA_ERR_ARG.                                     */
   /* Optional relation added to the aggregated result before the store
      (fused residual): same shape and partition as the output.  Used by the
      einsum path (EA_JOIN_MUL / EA_JOIN_ADD).  NULL = none.                  */
@@ -202,6 +215,10 @@ int ea_join_tuples(const char* spec, int32_t join_op, int32_t n_in,
    and dtype (EA_ERR_ARG otherwise); src and dst memory must not overlap.
    Bit-exact byte movement.  Asynchronous on `stream`. */
 int ea_repartition(const ea_relation* src, ea_relation* dst, void* stream);
+/* ea_repartition with an output store policy (EA_STORE_CACHED or
+   EA_STORE_STREAM; other values: EA_ERR_ARG).  ea_repartition is
+   ea_repartition_ex(src, dst, EA_STORE_CACHED, stream). */
+int ea_repartition_ex(const ea_relation* src, ea_relation* dst, int32_t store, void* stream);
 
 /* Overlay of two partitions of one shape (Section 5.3): per dim the sorted
    union of both split lists.  nblocks_out[rank]; splits_out must hold the

@@ -81,6 +81,39 @@ __device__ __forceinline__ void reset_agent(int32_t* counter) {
   __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Store with the non-temporal hint: the line is streamed towards memory
+// instead of being kept dirty in the XCD's L2, which the end of the kernel
+// would otherwise have to write back (measured on an RMSNorm over 64 MiB run
+// back to back: 16.1 -> 12.1 us).  When the next kernel reads the output,
+// plain stores are faster: it then finds the lines in the caches.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+template <class T>
+__device__ __forceinline__ void store_stream(void* p, const T& v) {
+  if constexpr (sizeof(T) == 16) {
+    __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t*>(p));
+  } else if constexpr (sizeof(T) == 8) {
+    __builtin_nontemporal_store(__builtin_bit_cast(u32x2_t, v), reinterpret_cast<u32x2_t*>(p));
+  } else if constexpr (sizeof(T) == 4) {
+    __builtin_nontemporal_store(__builtin_bit_cast(uint32_t, v), reinterpret_cast<uint32_t*>(p));
+  } else if constexpr (sizeof(T) == 2) {
+    __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, v), reinterpret_cast<uint16_t*>(p));
+  } else {
+    static_assert(sizeof(T) == 1, "store_stream: 1, 2, 4, 8 or 16 bytes");
+    __builtin_nontemporal_store(__builtin_bit_cast(uint8_t, v), reinterpret_cast<uint8_t*>(p));
+  }
+}
+
+// An output store under the caller's policy: streamed (non-temporal) or
+// plain.  The policy is a template argument, and callers branch once around a
+// whole store loop: the compiler merges two otherwise identical stores in the
+// arms of a runtime branch into one and drops the non-temporal hint.
+template <bool STREAM, class T>
+__device__ __forceinline__ void store_out(void* p, const T& v) {
+  if constexpr (STREAM) store_stream(p, v);
+  else *reinterpret_cast<T*>(p) = v;
+}
+
 // Load/store one element of a relation given its dtype.
 __device__ __forceinline__ float ld_elem(const char* base, int64_t idx, int dt) {
   if (dt == EA_F32) return reinterpret_cast<const float*>(base)[idx];

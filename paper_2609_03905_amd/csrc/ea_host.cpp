@@ -1044,6 +1044,8 @@ int prepare(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, con
     if (ops[o]->rank != sp->rank[o])
       return fail(EA_ERR_SPEC, "operand %d has rank %d but the spec gives it %d letters", o, ops[o]->rank,
                   sp->rank[o]);
+  if (prm && prm->store != EA_STORE_CACHED && prm->store != EA_STORE_STREAM)
+    return fail(EA_ERR_ARG, "params.store must be EA_STORE_CACHED or EA_STORE_STREAM");
   e = classify(*sp, join_op, agg_op, ops, prm, oi);
   if (e) return e;
   // join validation runs here too, before any HIP call
@@ -1321,6 +1323,7 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
       a.vec = plan->rows.vec;
       a.seg_chunks = plan->rows.cps;
       a.affine = plan->rows.affine;
+      a.stream_out = params ? params->store : 0;
       a.seg_len = plan->rows.seg_len;
       a.nseg = plan->rows.nseg;
       a.xs = plan->rows.xs;
@@ -1363,7 +1366,12 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
 }
 
 int ea_repartition(const ea_relation* src, ea_relation* dst, void* stream) {
+  return ea_repartition_ex(src, dst, EA_STORE_CACHED, stream);
+}
+
+int ea_repartition_ex(const ea_relation* src, ea_relation* dst, int32_t store, void* stream) {
   hipStream_t s = (hipStream_t)stream;
+  if (store != EA_STORE_CACHED && store != EA_STORE_STREAM) return fail(EA_ERR_ARG, "store must be EA_STORE_CACHED or EA_STORE_STREAM");
   if (!src || !dst) return fail(EA_ERR_ARG, "NULL relation");
   if (!src->data || !dst->data) return fail(EA_ERR_ARG, "relation has no data");
   if (src->rank != dst->rank || src->dtype != dst->dtype)
@@ -1498,7 +1506,7 @@ int ea_repartition(const ea_relation* src, ea_relation* dst, void* stream) {
     }
   }
   EA_HIP_TRY(launch_repartition((const RepTask*)plan->d_work, plan->n_work, (const char*)src->data,
-                                (char*)dst->data, s));
+                                (char*)dst->data, store == EA_STORE_STREAM, s));
   return ok();
 }
 

@@ -107,7 +107,7 @@ struct RepTask {
   int32_t begin, end;               // byte range of the box (rows x row_bytes) copied
 };
 
-hipError_t launch_repartition(const RepTask* d_tasks, int64_t n_tasks, const char* src, char* dst,
+hipError_t launch_repartition(const RepTask* d_tasks, int64_t n_tasks, const char* src, char* dst, bool stream_out,
                               hipStream_t s);
 
 // ---------------------------------------------------------------------------
@@ -197,6 +197,7 @@ struct RowArgs {
   // ys, ws; w's segment 0 at wbase).  Every address then follows from the
   // task record, with no tuple or block-table loads before the row loads.
   int32_t affine;
+  int32_t stream_out;    // non-temporal output stores (EA_STORE_STREAM)
   int32_t seg_len, nseg;
   int64_t xs, ys, ws, wbase;
 };

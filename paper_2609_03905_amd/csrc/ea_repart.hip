@@ -43,7 +43,7 @@ __device__ __forceinline__ void box_offsets(const RepTask& t, int32_t L, int64_t
   }
 }
 
-template <int VEC>
+template <int VEC, bool STREAM>
 __device__ __forceinline__ void copy_range(const RepTask* __restrict__ tp, const char* __restrict__ src,
                                            char* __restrict__ dst) {
   using T = typename Vec<VEC>::T;
@@ -67,28 +67,30 @@ __device__ __forceinline__ void copy_range(const RepTask* __restrict__ tp, const
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) v[u] = *reinterpret_cast<const T*>(s0 + sos[u]);
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) *reinterpret_cast<T*>(d0 + dofs[u]) = v[u];
+    for (int u = 0; u < kUnroll; ++u) store_out<STREAM>(d0 + dofs[u], v[u]);
   }
 }
 
+template <bool STREAM>
 __global__ __launch_bounds__(kThreads) void repart_kernel(const RepTask* __restrict__ tasks,
                                                           const char* __restrict__ src, char* __restrict__ dst) {
   const RepTask* t = tasks + blockIdx.x;
   switch (t->vec) {
-    case 16: copy_range<16>(t, src, dst); break;
-    case 8: copy_range<8>(t, src, dst); break;
-    case 4: copy_range<4>(t, src, dst); break;
-    case 2: copy_range<2>(t, src, dst); break;
-    default: copy_range<1>(t, src, dst); break;
+    case 16: copy_range<16, STREAM>(t, src, dst); break;
+    case 8: copy_range<8, STREAM>(t, src, dst); break;
+    case 4: copy_range<4, STREAM>(t, src, dst); break;
+    case 2: copy_range<2, STREAM>(t, src, dst); break;
+    default: copy_range<1, STREAM>(t, src, dst); break;
   }
 }
 
 }  // namespace
 
-hipError_t launch_repartition(const RepTask* d_tasks, int64_t n_tasks, const char* src, char* dst,
+hipError_t launch_repartition(const RepTask* d_tasks, int64_t n_tasks, const char* src, char* dst, bool stream_out,
                               hipStream_t s) {
   if (n_tasks == 0) return hipSuccess;
-  hipLaunchKernelGGL(repart_kernel, dim3((uint32_t)n_tasks), dim3(kThreads), 0, s, d_tasks, src, dst);
+  if (stream_out) hipLaunchKernelGGL(repart_kernel<true>, dim3((uint32_t)n_tasks), dim3(kThreads), 0, s, d_tasks, src, dst);
+  else hipLaunchKernelGGL(repart_kernel<false>, dim3((uint32_t)n_tasks), dim3(kThreads), 0, s, d_tasks, src, dst);
   return hipGetLastError();
 }
 

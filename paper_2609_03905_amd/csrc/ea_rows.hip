@@ -13,6 +13,8 @@
 // Causal softmax skips the loads of keys after the row's query position and
 // stores zeros there.  Rows too long for registers, or segments that are not
 // 16-byte multiples, take a scalar path that re-reads the row.
+#include <type_traits>
+
 #include "ea_device.h"
 
 namespace ea {
@@ -255,42 +257,49 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     const float ss = wave_sum(part);
     scale = 1.0f / sqrtf(ss / (float)a.row_len + a.eps);
   }
-  // write the row
+  // write the row, under the output store policy (one branch around the
+  // whole loop, see store_out)
+  auto write_row = [&](auto stream_tag) {
+    constexpr bool STREAM = decltype(stream_tag)::value;
 #pragma unroll
-  for (int k = 0; k < K; ++k) {
-    const int c = k * 64 + lane;
-    if (c >= total) continue;
-    const int sg = seg[k];
-    const int e0 = e0s[k];
-    float f[8];
-    unpack<XT>(v[k], f);
-    float o[8];
-    if constexpr (SOFTMAX) {
-      const int k0 = klo(sg) + e0;
+    for (int k = 0; k < K; ++k) {
+      const int c = k * 64 + lane;
+      if (c >= total) continue;
+      const int sg = seg[k];
+      const int e0 = e0s[k];
+      float f[8];
+      unpack<XT>(v[k], f);
+      float o[8];
+      if constexpr (SOFTMAX) {
+        const int k0 = klo(sg) + e0;
 #pragma unroll
-      for (int i = 0; i < EPC; ++i) {
-        const bool ok = vis[k] && (!a.causal || k0 + i <= qpos);
-        o[i] = ok ? __expf(f[i] - m) * scale : 0.0f;
+        for (int i = 0; i < EPC; ++i) {
+          const bool ok = vis[k] && (!a.causal || k0 + i <= qpos);
+          o[i] = ok ? __expf(f[i] - m) * scale : 0.0f;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < EPC; ++i) o[i] = sw[c * EPC + i] * (f[i] * scale);
       }
-    } else {
+      char* yp = y_at(sg, e0);
+      if (a.dt_y == EA_BF16 && ES == 2) {
+        uint4 pk;
+        uint32_t* w = reinterpret_cast<uint32_t*>(&pk);
 #pragma unroll
-      for (int i = 0; i < EPC; ++i) o[i] = sw[c * EPC + i] * (f[i] * scale);
+        for (int i = 0; i < 4; ++i)
+          w[i] = (uint32_t)f32_to_bf16(o[2 * i]) | ((uint32_t)f32_to_bf16(o[2 * i + 1]) << 16);
+        store_out<STREAM>(yp, pk);
+      } else if (a.dt_y == EA_F32 && ES == 4) {
+        store_out<STREAM>(yp, make_uint4(__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]),
+                                         __float_as_uint(o[3])));
+      } else {
+#pragma unroll
+        for (int i = 0; i < EPC; ++i) st_elem(yp, i, a.dt_y, o[i]);
+      }
     }
-    char* yp = y_at(sg, e0);
-    if (a.dt_y == EA_BF16 && ES == 2) {
-      uint4 pk;
-      uint32_t* w = reinterpret_cast<uint32_t*>(&pk);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f32_to_bf16(o[2 * i]) | ((uint32_t)f32_to_bf16(o[2 * i + 1]) << 16);
-      *reinterpret_cast<uint4*>(yp) = pk;
-    } else if (a.dt_y == EA_F32 && ES == 4) {
-      *reinterpret_cast<uint4*>(yp) =
-          make_uint4(__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]), __float_as_uint(o[3]));
-    } else {
-#pragma unroll
-      for (int i = 0; i < EPC; ++i) st_elem(yp, i, a.dt_y, o[i]);
-    }
-  }
+  };
+  if (a.stream_out) write_row(std::true_type{});
+  else write_row(std::false_type{});
 }
 
 // ---------------------------------------------------------------------------

@@ -26,6 +26,7 @@ ELEM_SIZE = {"f32": 4, "bf16": 2, "f16": 2}
 JOIN_MUL, JOIN_ADD = 0, 1
 OP_RMSNORM, OP_SOFTMAX, OP_ATTENTION, OP_SWIGLU = 16, 17, 18, 19
 AGG_NONE, AGG_SUM, AGG_MAX, AGG_LSE = 0, 1, 2, 3
+STORE_CACHED, STORE_STREAM = 0, 1  # output store policy (EA_STORE_*)
 
 
 class EAError(RuntimeError):
@@ -36,7 +37,7 @@ class EAError(RuntimeError):
 
 class _Params(ctypes.Structure):
     _fields_ = [("eps", ctypes.c_float), ("scale", ctypes.c_float), ("causal", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("residual", ctypes.c_void_p)]
+                ("store", ctypes.c_int32), ("residual", ctypes.c_void_p)]
 
 
 _lib = None
@@ -64,6 +65,7 @@ def lib() -> ctypes.CDLL:
         L.ea_join_tuples.argtypes = [ctypes.c_char_p, i32, i32, P(vp), vp, P(_Params), vp, i64, vp, i64,
                                      P(i64), P(i64), vp]
         L.ea_repartition.argtypes = [vp, vp, vp]
+        L.ea_repartition_ex.argtypes = [vp, vp, i32, vp]
         L.ea_overlay.argtypes = [i32, P(i32), P(i64), P(i32), P(i64), P(i32), P(i64)]
         L.ea_plan_cache_size.restype = i64
         L.ea_plan_cache_clear.restype = ctypes.c_int
@@ -177,18 +179,21 @@ class Relation:
 
 def joinagg(spec: str, join_op: int, agg_op: int, inputs: Sequence[Relation], out: Relation, *,
             eps: float = 0.0, scale: float = 0.0, causal: bool = False, residual: Relation | None = None,
-            stream=None) -> None:
+            store: int = 0, stream=None) -> None:
     """Run one GPU's share of a join-agg: join the input relations' blocks,
-    run the per-tuple kernel, aggregate by output key, store into ``out``."""
+    run the per-tuple kernel, aggregate by output key, store into ``out``.
+    ``store``: STORE_CACHED (default) or STORE_STREAM (non-temporal output
+    stores, for an output nothing reads soon)."""
     handles = _arr(ctypes.c_void_p, [r.handle.value for r in inputs])
-    prm = _Params(eps, scale, int(causal), 0, residual.handle.value if residual is not None else None)
+    prm = _Params(eps, scale, int(causal), int(store), residual.handle.value if residual is not None else None)
     _check(lib().ea_joinagg(spec.encode(), join_op, agg_op, len(inputs), handles, out.handle, ctypes.byref(prm),
                             _stream(stream)))
 
 
-def repartition(src: Relation, dst: Relation, stream=None) -> None:
-    """Write ``src``'s dense tensor into ``dst`` under ``dst``'s partition."""
-    _check(lib().ea_repartition(src.handle, dst.handle, _stream(stream)))
+def repartition(src: Relation, dst: Relation, stream=None, *, store: int = 0) -> None:
+    """Write ``src``'s dense tensor into ``dst`` under ``dst``'s partition
+    (``store`` as for joinagg)."""
+    _check(lib().ea_repartition_ex(src.handle, dst.handle, int(store), _stream(stream)))
 
 
 def join_tuples(spec: str, join_op: int, inputs: Sequence[Relation], out: Relation, *, causal: bool = False,

@@ -174,6 +174,9 @@ def test_fused_op_validation_errors():
     o = _fake([64, 100], "bf16", [[0, 64], [0, 100]])
     assert _code(J("tj,jk,jk->tk", ea.OP_SWIGLU, ea.AGG_MAX, [a, wt, wt], o)) == -1
     assert _code(J("tj,jk,jk->tj", ea.OP_SWIGLU, ea.AGG_SUM, [a, wt, wt], o)) == -5
+    # output store policy: only EA_STORE_CACHED (0) and EA_STORE_STREAM (1)
+    for bad in (-1, 2, 7):
+        assert _code(J("tc,c->tc", ea.OP_RMSNORM, ea.AGG_SUM, [x, w], y, eps=1e-6, store=bad)) == -1
 
 
 def test_repartition_validation_errors():
@@ -187,3 +190,5 @@ def test_repartition_validation_errors():
     assert _code(lambda: ea.repartition(a, a)) == -1       # memory overlaps
     nodata = ea.Relation([64, 64], "bf16", [[0, 64], [0, 64]], allocate=False)
     assert _code(lambda: ea.repartition(nodata, d)) == -1
+    for bad in (-1, 2):
+        assert _code(lambda: ea.repartition(a, d, store=bad)) == -1
