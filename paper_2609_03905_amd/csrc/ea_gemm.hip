@@ -259,8 +259,9 @@ struct KStep {
 };
 
 // Split output keys: every unit writes its partial sums, the last unit of
-// the key (device-scope arrival counter, no waiting) adds all partials in part
-// order -- a fixed order, so results are deterministic -- and stores.
+// the key (device-scope arrival counter, no waiting) adds the partials in a
+// fixed order -- part order, or for two parts its own plus the other's,
+// which is the same sum -- so results are deterministic, and stores.
 // Partials are laid out in accumulator order (lane-contiguous float4s).
 // Then the epilogue, with dtype and residual decided outside its unrolled loops.
 template <bool SWIGLU, int NB, int WN, int W>
@@ -269,34 +270,23 @@ __device__ __forceinline__ void finish_tile(f32x16_t (&acc)[NB][4][WN], const Ge
   __shared__ int s_last;
   const int tid = wid * 64 + lane;
   if (tile.n_parts > 1) {
-    constexpr int PER_WAVE = NB * 4 * WN * 16;  // floats per lane
-    float* mine = p.partials + ((int64_t)tile.slot * W + wid) * PER_WAVE * 64;
-#pragma unroll
-    for (int o = 0; o < NB; ++o)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < WN; ++j)
-#pragma unroll
-          for (int r4 = 0; r4 < 4; ++r4) {
-            const int q = ((o * 4 + i) * WN + j) * 4 + r4;
-            float* dst = mine + ((int64_t)q * 64 + lane) * 4;
-            store_agent2(dst, acc[o][i][j][4 * r4], acc[o][i][j][4 * r4 + 1]);
-            store_agent2(dst + 2, acc[o][i][j][4 * r4 + 2], acc[o][i][j][4 * r4 + 3]);
-          }
-    drain_vmem();
-    __syncthreads();
-    if (tid == 0) s_last = arrive_agent(p.counters + tile.counter) == tile.n_parts - 1;
-    __syncthreads();
-    if (!s_last) return;
-#pragma unroll
-    for (int o = 0; o < NB; ++o)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < WN; ++j) acc[o][i][j] = f32x16_t{};
-    for (int part = 0; part < tile.n_parts; ++part) {
-      const float* src = p.partials + ((int64_t)(tile.first_slot + part) * W + wid) * PER_WAVE * 64;
+    // Partial sums go through the plan's scratch as lane-contiguous 16-byte
+    // pieces (every store instruction writes whole 128-byte lines) with the
+    // sc1 cache policy, which keeps them coherent between the XCDs' L2s; the
+    // reader's loads carry it too.  Every lane holds PER_WAVE floats.
+    constexpr int PER_WAVE = NB * 4 * WN * 16;
+    constexpr int WAVE_BYTES = PER_WAVE * 64 * 4;
+    constexpr int kCoherent = 16;  // sc1
+    auto slot_rsrc = [&](int slot) {
+      return __builtin_amdgcn_make_buffer_rsrc(p.partials + (int64_t)slot * W * PER_WAVE * 64, 0, 0x7fffffff,
+                                               0x00020000);
+    };
+    auto piece = [&](int o, int i, int j, int r4) {  // byte offset of a lane's piece in its wave's area
+      const int q = ((o * 4 + i) * WN + j) * 4 + r4;
+      return (uint32_t)(wid * WAVE_BYTES + (q * 64 + lane) * 16);
+    };
+    {
+      const auto rs = slot_rsrc(tile.slot);
 #pragma unroll
       for (int o = 0; o < NB; ++o)
 #pragma unroll
@@ -305,15 +295,62 @@ __device__ __forceinline__ void finish_tile(f32x16_t (&acc)[NB][4][WN], const Ge
           for (int j = 0; j < WN; ++j)
 #pragma unroll
             for (int r4 = 0; r4 < 4; ++r4) {
-              const int q = ((o * 4 + i) * WN + j) * 4 + r4;
-              const float2 v0 = load_agent2(src + ((int64_t)q * 64 + lane) * 4);
-              const float2 v1 = load_agent2(src + ((int64_t)q * 64 + lane) * 4 + 2);
-              acc[o][i][j][4 * r4] += v0.x;
-              acc[o][i][j][4 * r4 + 1] += v0.y;
-              acc[o][i][j][4 * r4 + 2] += v1.x;
-              acc[o][i][j][4 * r4 + 3] += v1.y;
+              const f32x16_t& c = acc[o][i][j];
+              const u32x4_t v = {__float_as_uint(c[4 * r4]), __float_as_uint(c[4 * r4 + 1]),
+                                 __float_as_uint(c[4 * r4 + 2]), __float_as_uint(c[4 * r4 + 3])};
+              __builtin_amdgcn_raw_buffer_store_b128(v, rs, piece(o, i, j, r4), 0, kCoherent);
             }
     }
+    drain_vmem();
+    __syncthreads();
+    if (tid == 0) s_last = arrive_agent(p.counters + tile.counter) == tile.n_parts - 1;
+    __syncthreads();
+    if (!s_last) return;
+    // add one slot's partials: 16 loads in flight per batch (latency hidden,
+    // 64 registers), then their adds
+    auto add_slot = [&](int slot) {
+      const auto rs = slot_rsrc(slot);
+      constexpr int NQ = PER_WAVE / 4, BATCH = 16;
+      static_assert(NQ % BATCH == 0, "batches of pieces");
+#pragma unroll
+      for (int q0 = 0; q0 < NQ; q0 += BATCH) {
+        u32x4_t v[BATCH];
+#pragma unroll
+        for (int t = 0; t < BATCH; ++t) {
+          const int q = q0 + t;
+          v[t] = __builtin_amdgcn_raw_buffer_load_b128(rs, piece(q / (16 * WN), (q / (4 * WN)) % 4, (q / 4) % WN, q % 4),
+                                                       0, kCoherent);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < BATCH; ++t) {
+          const int q = q0 + t;
+          f32x16_t& c = acc[q / (16 * WN)][(q / (4 * WN)) % 4][(q / 4) % WN];
+          const int r4 = q % 4;
+          c[4 * r4] += __uint_as_float(v[t].x);
+          c[4 * r4 + 1] += __uint_as_float(v[t].y);
+          c[4 * r4 + 2] += __uint_as_float(v[t].z);
+          c[4 * r4 + 3] += __uint_as_float(v[t].w);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    // Two parts: own + other, and a + b == b + a exactly, so the result does
+    // not depend on which part arrived last and our own partial is not
+    // reloaded.  More parts: the sum in part order from zero, a fixed order
+    // whoever arrives last.
+    const bool two = tile.n_parts == 2;
+    const int other = tile.first_slot + (tile.slot == tile.first_slot ? 1 : 0);
+    if (!two) {
+#pragma unroll
+      for (int o = 0; o < NB; ++o)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < WN; ++j) acc[o][i][j] = f32x16_t{};
+    }
+    const int n_add = two ? 1 : tile.n_parts;
+    for (int k = 0; k < n_add; ++k) add_slot(two ? other : tile.first_slot + k);
     if (tid == 0) reset_agent(p.counters + tile.counter);  // ready for the next call (stream-ordered)
   }
   const DevBlk& cb = p.blk_c[tile.block];
