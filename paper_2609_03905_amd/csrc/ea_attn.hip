@@ -354,90 +354,123 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
     }
   }
 
-  // ---- epilogue (group 0).  acc_o[dt] register r of lane (lq, g) holds O^T
-  // row d = 32 dt + 8 (r/4) + 4 g + r%4, column = this lane's query.
-  if (u.slot < 0) {
-    if (grp != 0) return;
-    const float inv = l > 0.0f ? 1.0f / l : 0.0f;
-    char* orow = p.o + oblk.off;
+  // ---- split group: write this unit's partial (m, l, O), the last unit of
+  // the (group, tile) merges in registers.  Partials go through the plan's
+  // scratch with the sc1 cache policy (coherent between the XCDs' L2s): O as
+  // lane-contiguous 16-byte pieces (every store writes whole lines), (m, l)
+  // as one 8-byte pair per query row.
+  if (u.slot >= 0) {
+    constexpr int kCoherent = 16;  // sc1
+    auto o_rsrc = [&](int slot) {
+      return __builtin_amdgcn_make_buffer_rsrc(p.part_o + (int64_t)slot * 128 * D, 0, 0x7fffffff, 0x00020000);
+    };
+    auto ml_rsrc = [&](int slot) {
+      return __builtin_amdgcn_make_buffer_rsrc(p.part_ml + (int64_t)slot * 128 * 2, 0, 0x7fffffff, 0x00020000);
+    };
+    auto o_piece = [&](int q) { return (uint32_t)(((wq * 16 + q) * 64 + lane) * 16); };
+    const uint32_t ml_off = (uint32_t)((wq * 32 + lq) * 8);
+    if (grp == 0) {
+      const auto ro = o_rsrc(u.slot);
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int d = 32 * dt + 8 * rr + 4 * g;
-        const int64_t idx = (int64_t)row * D + d;
-        const float o0 = acc_o[dt][4 * rr] * inv, o1 = acc_o[dt][4 * rr + 1] * inv;
-        const float o2 = acc_o[dt][4 * rr + 2] * inv, o3 = acc_o[dt][4 * rr + 3] * inv;
-        if (p.dt_o == EA_BF16) {
-          uint2 w;
-          w.x = (uint32_t)f32_to_bf16(o0) | ((uint32_t)f32_to_bf16(o1) << 16);
-          w.y = (uint32_t)f32_to_bf16(o2) | ((uint32_t)f32_to_bf16(o3) << 16);
-          *reinterpret_cast<uint2*>(orow + idx * 2) = w;
-        } else {
-          *reinterpret_cast<float4*>(orow + idx * 4) = make_float4(o0, o1, o2, o3);
-        }
+      for (int q = 0; q < 16; ++q) {
+        const f32x16_t& c = acc_o[q / 4];
+        const int r0 = 4 * (q % 4);
+        const u32x4_t v = {__float_as_uint(c[r0]), __float_as_uint(c[r0 + 1]), __float_as_uint(c[r0 + 2]),
+                           __float_as_uint(c[r0 + 3])};
+        __builtin_amdgcn_raw_buffer_store_b128(v, ro, o_piece(q), 0, kCoherent);
       }
-    return;
+      if (g == 0) {
+        const u32x2_t ml = {__float_as_uint(m), __float_as_uint(l)};
+        __builtin_amdgcn_raw_buffer_store_b64(ml, ml_rsrc(u.slot), ml_off, 0, kCoherent);
+      }
+    }
+    drain_vmem();
+    __syncthreads();
+    if (tid == 0) s_last = arrive_agent(p.counters + u.counter) == u.n_parts - 1;
+    __syncthreads();
+    if (!s_last || grp != 0) return;
+    if (tid == 0) reset_agent(p.counters + u.counter);  // ready for the next call (stream-ordered)
+    auto load_ml = [&](int slot) {
+      const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(ml_rsrc(slot), ml_off, 0, kCoherent);
+      return make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
+    };
+    // acc_o = a_own * acc_o + w * O_slot, loads in batches of 8 pieces
+    auto add_slot = [&](int slot, float a_own, float w) {
+      const auto ro = o_rsrc(slot);
+#pragma unroll
+      for (int q0 = 0; q0 < 16; q0 += 8) {
+        u32x4_t v[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) v[t] = __builtin_amdgcn_raw_buffer_load_b128(ro, o_piece(q0 + t), 0, kCoherent);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          // both products rounded before the add (no fused multiply-add):
+          // the sum must not depend on which operand is own and which loaded
+#pragma clang fp contract(off)
+          f32x16_t& c = acc_o[(q0 + t) / 4];
+          const int r0 = 4 * ((q0 + t) % 4);
+          c[r0] = c[r0] * a_own + __uint_as_float(v[t].x) * w;
+          c[r0 + 1] = c[r0 + 1] * a_own + __uint_as_float(v[t].y) * w;
+          c[r0 + 2] = c[r0 + 2] * a_own + __uint_as_float(v[t].z) * w;
+          c[r0 + 3] = c[r0 + 3] * a_own + __uint_as_float(v[t].w) * w;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    if (u.n_parts == 2) {
+      // own + other: every term is formed the same way whichever part holds
+      // it, and a + b == b + a exactly, so the bits do not depend on which
+      // part arrived last
+      const float2 ml1 = load_ml(u.first_slot + (u.slot == u.first_slot ? 1 : 0));
+      const float M = fmaxf(m, ml1.x);
+      const float Mu = M == -INFINITY ? 0.0f : M;
+      const float a0 = exp2f(m - Mu), a1 = exp2f(ml1.x - Mu);
+      add_slot(u.first_slot + (u.slot == u.first_slot ? 1 : 0), a0, a1);
+      {
+#pragma clang fp contract(off)
+        l = l * a0 + ml1.y * a1;
+      }
+    } else {
+      // more parts: from zero, in part order (own partial re-read), a fixed
+      // order whoever arrives last
+      float M = -INFINITY;
+      for (int q = 0; q < u.n_parts; ++q) M = fmaxf(M, load_ml(u.first_slot + q).x);
+      const float Mu = M == -INFINITY ? 0.0f : M;
+      l = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc_o[i] = f32x16_t{};
+      for (int q = 0; q < u.n_parts; ++q) {
+        const float2 mlq = load_ml(u.first_slot + q);
+        const float w = exp2f(mlq.x - Mu);
+        add_slot(u.first_slot + q, 1.0f, w);
+        l += mlq.y * w;
+      }
+    }
   }
 
-  // ---- split group: write this unit's partial, the last unit merges
-  if (grp == 0) {
-    float* po = p.part_o + (int64_t)u.slot * 128 * D;
-    const int rt = wq * 32 + lq;  // row inside the tile
+  // ---- epilogue (group 0).  acc_o[dt] register r of lane (lq, g) holds O^T
+  // row d = 32 dt + 8 (r/4) + 4 g + r%4, column = this lane's query.
+  if (grp != 0) return;
+  const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+  char* orow = p.o + oblk.off;
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
+  for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int d = 32 * dt + 8 * rr + 4 * g;
-        store_agent2(po + rt * D + d, acc_o[dt][4 * rr], acc_o[dt][4 * rr + 1]);
-        store_agent2(po + rt * D + d + 2, acc_o[dt][4 * rr + 2], acc_o[dt][4 * rr + 3]);
-      }
-    if (g == 0) store_agent2(p.part_ml + ((int64_t)u.slot * 128 + rt) * 2, m, l);
-  }
-  drain_vmem();
-  __syncthreads();
-  if (tid == 0) s_last = arrive_agent(p.counters + u.counter) == u.n_parts - 1;
-  __syncthreads();
-  if (!s_last) return;
-  {
-    // 512 threads: row rt = tid / 4, a quarter of its 128 dims each
-    const int rt = tid >> 2, dlo = (tid & 3) * 32;
-    float M = -INFINITY;
-    for (int q = 0; q < u.n_parts; ++q)
-      M = fmaxf(M, load_agent(p.part_ml + ((int64_t)(u.first_slot + q) * 128 + rt) * 2));
-    const float Mu = M == -INFINITY ? 0.0f : M;
-    float L = 0.0f;
-    for (int q = 0; q < u.n_parts; ++q) {
-      const float2 ml = load_agent2(p.part_ml + ((int64_t)(u.first_slot + q) * 128 + rt) * 2);
-      L += ml.y * exp2f(ml.x - Mu);
-    }
-    const float inv = L > 0.0f ? 1.0f / L : 0.0f;
-    const int64_t orow_idx = (int64_t)(u.q0 + rt) * D;
-    char* obase = p.o + oblk.off;
-    for (int d = dlo; d < dlo + 32; d += 4) {
-      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int q = 0; q < u.n_parts; ++q) {
-        const int64_t sl = u.first_slot + q;
-        const float w = exp2f(load_agent(p.part_ml + (sl * 128 + rt) * 2) - Mu);
-        const float2 v0 = load_agent2(p.part_o + (sl * 128 + rt) * D + d);
-        const float2 v1 = load_agent2(p.part_o + (sl * 128 + rt) * D + d + 2);
-        acc.x += v0.x * w;
-        acc.y += v0.y * w;
-        acc.z += v1.x * w;
-        acc.w += v1.y * w;
-      }
-      const float o0 = acc.x * inv, o1 = acc.y * inv, o2 = acc.z * inv, o3 = acc.w * inv;
+    for (int rr = 0; rr < 4; ++rr) {
+      const int d = 32 * dt + 8 * rr + 4 * g;
+      const int64_t idx = (int64_t)row * D + d;
+      const float o0 = acc_o[dt][4 * rr] * inv, o1 = acc_o[dt][4 * rr + 1] * inv;
+      const float o2 = acc_o[dt][4 * rr + 2] * inv, o3 = acc_o[dt][4 * rr + 3] * inv;
       if (p.dt_o == EA_BF16) {
         uint2 w;
         w.x = (uint32_t)f32_to_bf16(o0) | ((uint32_t)f32_to_bf16(o1) << 16);
         w.y = (uint32_t)f32_to_bf16(o2) | ((uint32_t)f32_to_bf16(o3) << 16);
-        *reinterpret_cast<uint2*>(obase + (orow_idx + d) * 2) = w;
+        *reinterpret_cast<uint2*>(orow + idx * 2) = w;
       } else {
-        *reinterpret_cast<float4*>(obase + (orow_idx + d) * 4) = make_float4(o0, o1, o2, o3);
+        *reinterpret_cast<float4*>(orow + idx * 4) = make_float4(o0, o1, o2, o3);
       }
     }
-  }
-  if (tid == 0) reset_agent(p.counters + u.counter);  // ready for the next call (stream-ordered)
 }
 
 }  // namespace

@@ -41,6 +41,23 @@ def test_attention_f32_output_and_determinism():
     assert torch.equal(O.bytes(), O2.bytes())
 
 
+def test_attention_split_tiles_two_and_three_parts_deterministic():
+    # 24 key blocks of 128: query tiles past the 8th split their keys over two
+    # and three work units, merged by the last one to arrive; the merge must
+    # give the same bits whichever unit that is
+    B, H, S = 1, 1, 3072
+    q, k, v = (synth.normal((B, H, S, 128), 430 + i, dtype="bf16") for i in range(3))
+    p = [[0, 1], [0, 1], synth.splits(S, 128), [0, 128]]
+    scale = 1.0 / np.sqrt(128)
+    ref = oracle.attention(*(synth.to_f64(a, "bf16") for a in (q, k, v)), True, scale)
+    O = _run(q, k, v, p, p, scale, True, "f32")
+    assert_close(values(O), ref, rel_fro=1e-3, what="attention, split tiles")
+    for _ in range(3):
+        O2 = _run(q, k, v, p, p, scale, True, "f32")
+        torch.cuda.synchronize()
+        assert torch.equal(O.bytes(), O2.bytes())
+
+
 @pytest.mark.parametrize("qb,kb", [(256, 128), (128, 256), (512, 512), (128, 1024)])
 def test_attention_block_size_invariance(qb, kb):
     B, H, S = 1, 2, 1024
