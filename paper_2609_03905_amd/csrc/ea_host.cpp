@@ -893,44 +893,71 @@ int build_attention(const ea_relation* const* ops, const OpInfo& oi, const JoinI
   std::vector<AttnUnit> units;
   int32_t slot = 0, counter = 0;
   int32_t c[kMaxRank];
-  constexpr int chunk = 8;  // key blocks per unit (the online-softmax partial)
-  static_assert(chunk <= kAttnMaxUnitTuples, "attention unit size");
+  // expected tuples of every (group, 128-row tile): the key blocks the causal
+  // rule keeps; used only to size the split -- the kernel reads its tuple
+  // range from the GPU-built group offsets
+  struct TileWork {
+    int64_t g, q0;
+    int n_t;
+  };
+  std::vector<TileWork> tiles;
   for (int64_t g = 0; g < n_groups; ++g) {
     block_coords(Q, g, c);
     const int64_t q_lo = Q->splits[r - 2][c[r - 2]];
     const int64_t q_hi = Q->splits[r - 2][c[r - 2] + 1];
-    // expected tuples of this group (key blocks the causal rule keeps); used
-    // only to size the split -- the kernel reads its tuple range from the
-    // GPU-built group offsets
     int n_t = 0;
     for (int kb = 0; kb < K->nb[r - 2]; ++kb) {
       const int64_t k_lo = K->splits[r - 2][kb];
       if (!causal || k_lo <= q_hi - 1) ++n_t;
     }
-    for (int64_t q0 = 0; q0 < q_hi - q_lo; q0 += 128) {
-      const int parts = (n_t + chunk - 1) / chunk;
-      for (int p = 0; p < parts; ++p) {
-        AttnUnit u;
-        u.group = (int32_t)g;
-        u.q0 = (int32_t)q0;
-        u.part = p;
-        u.n_parts = parts;
-        u.weight = (n_t * (p + 1)) / parts - (n_t * p) / parts;
-        if (parts > 1) {
-          u.slot = slot + p;
-          u.first_slot = slot;
-          u.counter = counter;
-        } else {
-          u.slot = -1;
-          u.first_slot = -1;
-          u.counter = -1;
-        }
-        units.push_back(u);
-      }
+    for (int64_t q0 = 0; q0 < q_hi - q_lo; q0 += 128) tiles.push_back(TileWork{g, q0, n_t});
+  }
+  // key blocks per unit (the online-softmax partial): the run that minimises
+  // waves of units over the 256 CUs x (longest unit + half a key block per
+  // extra part of a split tile, the merge); ties go to the longer run
+  const int kCUs = 256;
+  int max_nt = 1;
+  for (const TileWork& t : tiles) max_nt = std::max(max_nt, t.n_t);
+  int chunk = kAttnMaxUnitTuples;
+  double best = 1e300;
+  for (int cc = kAttnMaxUnitTuples; cc >= 1; --cc) {
+    int64_t n_units = 0;
+    int max_parts = 1;
+    for (const TileWork& t : tiles) {
+      const int parts = std::max(1, (t.n_t + cc - 1) / cc);
+      n_units += parts;
+      max_parts = std::max(max_parts, parts);
+    }
+    const double waves = (double)((n_units + kCUs - 1) / kCUs);
+    const double cost = waves * (std::min(cc, max_nt) + 0.5 * (max_parts - 1));
+    if (cost < best - 1e-9) {
+      best = cost;
+      chunk = cc;
+    }
+  }
+  for (const TileWork& t : tiles) {
+    const int parts = std::max(1, (t.n_t + chunk - 1) / chunk);
+    for (int p = 0; p < parts; ++p) {
+      AttnUnit u;
+      u.group = (int32_t)t.g;
+      u.q0 = (int32_t)t.q0;
+      u.part = p;
+      u.n_parts = parts;
+      u.weight = (t.n_t * (p + 1)) / parts - (t.n_t * p) / parts;
       if (parts > 1) {
-        slot += parts;
-        ++counter;
+        u.slot = slot + p;
+        u.first_slot = slot;
+        u.counter = counter;
+      } else {
+        u.slot = -1;
+        u.first_slot = -1;
+        u.counter = -1;
       }
+      units.push_back(u);
+    }
+    if (parts > 1) {
+      slot += parts;
+      ++counter;
     }
   }
   // heaviest units first so that the long runs start early
