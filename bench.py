@@ -108,27 +108,62 @@ def block_workload():
                 cpu=cpu_baseline_block)
 
 
+ROTATE_BYTES = 1 << 30
+
+
+class _Rotation:
+    """Round-robin over copies of a workload's buffers, placed at different
+    addresses: consecutive calls use different copies, and the copies together
+    (>= 1 GiB) exceed the 256 MB Infinity Cache, so a timed call reads its
+    inputs from HBM rather than from what the previous call left cached."""
+
+    def __init__(self, sets):
+        self.sets, self.i = sets, -1
+
+    def next(self):
+        self.i = (self.i + 1) % len(self.sets)
+        return self.sets[self.i]
+
+
+def _buffer_sets(make_set, set_bytes: int):
+    return [make_set(i) for i in range(max(1, -(-ROTATE_BYTES // set_bytes)))]
+
+
+def _copy(rel, ea):
+    """Relation with the same partition and contents in a new allocation."""
+    return ea.Relation(rel.shape, rel.dtype, rel.partition, data=rel.bytes().clone())
+
+
 def qkv_workload():
     import synth
     from paper_2609_03905_amd import ea
 
     w = synth.qkv_projection()
-    X = ea.from_dense(_dev(w["X"]), "bf16", w["pX"])
-    W = ea.from_dense(_dev(w["W"]), "bf16", w["pW"])
-    Y = ea.Relation((4096, 1536), "bf16", w["pY"])
-    Yh = ea.Relation((4096, 1536), "bf16", w["pHead"])
-    gemm = lambda: ea.joinagg("tj,jk->tk", ea.JOIN_MUL, ea.AGG_SUM, [X, W], Y)
-    repart = lambda: ea.repartition(Y, Yh)
+    X0 = ea.from_dense(_dev(w["X"]), "bf16", w["pX"])
+    W0 = ea.from_dense(_dev(w["W"]), "bf16", w["pW"])
+
+    def make_set(i):
+        X, W = (X0, W0) if i == 0 else (_copy(X0, ea), _copy(W0, ea))
+        return X, W, ea.Relation((4096, 1536), "bf16", w["pY"]), ea.Relation((4096, 1536), "bf16", w["pHead"])
+
+    set_bytes = 4096 * 4096 * 2 + 3 * 4096 * 1536 * 2
+    sets = _buffer_sets(make_set, set_bytes)
+    rot, rot_g, rot_r = (_Rotation(sets) for _ in range(3))
+    run_gemm = lambda X, W, Y: ea.joinagg("tj,jk->tk", ea.JOIN_MUL, ea.AGG_SUM, [X, W], Y)
+    gemm = lambda: run_gemm(*rot_g.next()[:3])
+    repart = lambda: (lambda st: ea.repartition(st[2], st[3]))(rot_r.next())
 
     def step():
-        gemm()
-        repart()
+        X, W, Y, Yh = rot.next()
+        run_gemm(X, W, Y)
+        ea.repartition(Y, Yh)
 
     flops = 2.0 * 4096 * 4096 * 1536
     comps = {"joinagg_gemm": dict(fn=gemm, flops=flops), "repartition": dict(fn=repart, bytes=2 * 4096 * 1536 * 2)}
     return dict(step=step, flops=flops, comps=comps, dominant="joinagg_gemm",
                 config={"workload": "llama7b_qkv_projection_share", "spec": "tj,jk->tk", "t": 4096, "j": 4096,
-                        "k": 1536, "block": 512, "repartition": "512x512 -> 4096x128", "dtype": "bf16"},
+                        "k": 1536, "block": 512, "repartition": "512x512 -> 4096x128", "dtype": "bf16",
+                        "buffer_sets": len(rot.sets)},
                 cpu=cpu_baseline_qkv)
 
 
@@ -137,14 +172,23 @@ def attention_workload():
     from paper_2609_03905_amd import ea
 
     w = synth.attention()
-    Q, K, V = (ea.from_dense(_dev(w[n]), "bf16", w["pq"]) for n in "qkv")
-    O = ea.Relation((2, 4, 2048, 128), "bf16", w["pq"])
-    fn = lambda: ea.joinagg("bhqd,bhkd,bhkd->bhqd", ea.OP_ATTENTION, ea.AGG_LSE, [Q, K, V], O, scale=w["scale"],
-                            causal=True)
+    base = [ea.from_dense(_dev(w[n]), "bf16", w["pq"]) for n in "qkv"]
+
+    def make_set(i):
+        qkv = base if i == 0 else [_copy(r, ea) for r in base]
+        return qkv + [ea.Relation((2, 4, 2048, 128), "bf16", w["pq"])]
+
+    rot = _Rotation(_buffer_sets(make_set, 4 * 2 * 4 * 2048 * 128 * 2))
+
+    def fn():
+        Q, K, V, O = rot.next()
+        ea.joinagg("bhqd,bhkd,bhkd->bhqd", ea.OP_ATTENTION, ea.AGG_LSE, [Q, K, V], O, scale=w["scale"], causal=True)
+
     flops = 4.0 * 128 * 2 * 4 * 2048 * 2049 / 2
     return dict(step=fn, flops=flops, comps={"attention": dict(fn=fn, flops=flops)}, dominant="attention",
                 config={"workload": "llama7b_causal_attention_share", "batch": 2, "heads": 4, "seq": 2048,
-                        "d_head": 128, "q_block": 128, "k_block": 128, "dtype": "bf16"}, cpu=None)
+                        "d_head": 128, "q_block": 128, "k_block": 128, "dtype": "bf16",
+                        "buffer_sets": len(rot.sets)}, cpu=None)
 
 
 def reductions_workload():
@@ -152,19 +196,28 @@ def reductions_workload():
     from paper_2609_03905_amd import ea
 
     w = synth.reductions()
-    X = ea.from_dense(_dev(w["x"]), "bf16", w["px"])
+    X0 = ea.from_dense(_dev(w["x"]), "bf16", w["px"])
     Wt = ea.from_dense(_dev(w["w"]), "bf16", w["pw"])
-    Y = ea.Relation((4096, 4096), "bf16", w["px"])
-    S = ea.from_dense(_dev(w["s"]), "bf16", w["ps"])
-    P = ea.Relation((4, 2048, 2048), "bf16", w["ps"])
+    S0 = ea.from_dense(_dev(w["s"]), "bf16", w["ps"])
+
+    def make_set(i):
+        X, S = (X0, S0) if i == 0 else (_copy(X0, ea), _copy(S0, ea))
+        return X, ea.Relation((4096, 4096), "bf16", w["px"]), S, ea.Relation((4, 2048, 2048), "bf16", w["ps"])
+
+    set_bytes = 2 * 4096 * 4096 * 2 + 2 * 4 * 2048 * 2048 * 2
+    sets = _buffer_sets(make_set, set_bytes)
+    rot, rot_r, rot_s = (_Rotation(sets) for _ in range(3))
     # standalone operators whose outputs nothing reads next: streamed stores
     st = ea.STORE_STREAM
-    rms = lambda: ea.joinagg("tc,c->tc", ea.OP_RMSNORM, ea.AGG_SUM, [X, Wt], Y, eps=w["eps"], store=st)
-    sm = lambda: ea.joinagg("hqk->hqk", ea.OP_SOFTMAX, ea.AGG_LSE, [S], P, causal=True, store=st)
+    run_rms = lambda X, Y: ea.joinagg("tc,c->tc", ea.OP_RMSNORM, ea.AGG_SUM, [X, Wt], Y, eps=w["eps"], store=st)
+    run_sm = lambda S, P: ea.joinagg("hqk->hqk", ea.OP_SOFTMAX, ea.AGG_LSE, [S], P, causal=True, store=st)
+    rms = lambda: (lambda b: run_rms(b[0], b[1]))(rot_r.next())
+    sm = lambda: (lambda b: run_sm(b[2], b[3]))(rot_s.next())
 
     def step():
-        rms()
-        sm()
+        X, Y, S, P = rot.next()
+        run_rms(X, Y)
+        run_sm(S, P)
 
     rms_bytes = 2 * 4096 * 4096 * 2 + 4096 * 2
     sm_bytes = 4 * (2048 * 2049 // 2) * 2 + 4 * 2048 * 2048 * 2
@@ -173,7 +226,7 @@ def reductions_workload():
                 dominant="rmsnorm", bytes=rms_bytes + sm_bytes,
                 config={"workload": "reductions", "rmsnorm": "x[4096,4096] bf16, 8 column blocks",
                         "softmax": "s[4,2048,2048] bf16 causal, 256-key blocks", "dtype": "bf16",
-                        "store": "stream"}, cpu=None)
+                        "store": "stream", "buffer_sets": len(rot.sets)}, cpu=None)
 
 
 def repartition_workload():
