@@ -195,6 +195,31 @@ __device__ __forceinline__ void epilogue(const f32x16_t (&acc)[NB][4][WN], const
   static_assert(CPR % W == 0, "epilogue chunking");
   const int wm = wid / WGN, wn = wid % WGN, g = lane >> 5, lq = lane & 31;
   const int tid = wid * 64 + lane;
+  // chunk k of pass i: tile row and 8-column group, global position
+  auto chunk_pos = [&](int i, int k, int& row, int& c8, int& gm, int& gn) {
+    const int c = tid + 64 * W * k;
+    row = c / CPR;
+    c8 = c % CPR;
+    gm = e.m0 + (row >> 5) * 128 + 32 * i + (row & 31);
+    gn = e.n0 + 8 * c8;
+  };
+  // A 16-bit residual is loaded for all four passes before the first one
+  // (64 registers), so that one memory latency covers the whole epilogue
+  // instead of one per pass; an fp32 residual is loaded pass by pass.
+  constexpr bool RES16 = RES && DT != EA_F32;
+  uint4 rres[RES16 ? 4 : 1][RES16 ? CHUNKS : 1];
+  if constexpr (RES16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int k = 0; k < CHUNKS; ++k) {
+        int row, c8, gm, gn;
+        chunk_pos(i, k, row, c8, gm, gn);
+        rres[i][k] = gm < e.mext && gn < e.next
+                         ? *reinterpret_cast<const uint4*>(e.res + ((int64_t)gm * e.next + gn) * 2)
+                         : make_uint4(0, 0, 0, 0);
+      }
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     __syncthreads();  // the stage area is free (K loop or previous pass done)
@@ -210,10 +235,8 @@ __device__ __forceinline__ void epilogue(const f32x16_t (&acc)[NB][4][WN], const
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < CHUNKS; ++k) {
-      const int c = tid + 64 * W * k;
-      const int row = c / CPR, c8 = c % CPR;
-      const int gm = e.m0 + (row >> 5) * 128 + 32 * i + (row & 31);
-      const int gn = e.n0 + 8 * c8;
+      int row, c8, gm, gn;
+      chunk_pos(i, k, row, c8, gm, gn);
       if (gm < e.mext && gn < e.next) {
         const float4 lo = *reinterpret_cast<const float4*>(stage + row * kEpiPitch + 8 * c8);
         const float4 hi = *reinterpret_cast<const float4*>(stage + row * kEpiPitch + 8 * c8 + 4);
@@ -230,7 +253,7 @@ __device__ __forceinline__ void epilogue(const f32x16_t (&acc)[NB][4][WN], const
           *reinterpret_cast<float4*>(e.c + idx * 4 + 16) = make_float4(o[4], o[5], o[6], o[7]);
         } else {
           if constexpr (RES) {
-            const uint4 rv = *reinterpret_cast<const uint4*>(e.res + idx * 2);
+            const uint4 rv = rres[i][k];
             const uint32_t w[4] = {rv.x, rv.y, rv.z, rv.w};
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
