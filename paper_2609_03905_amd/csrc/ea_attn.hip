@@ -51,6 +51,9 @@ struct KvMeta {
   int32_t klo, kext;   // key interval of the block
 };
 constexpr float kLog2e = 1.4426950408889634f;
+// LDS byte offset of the epilogue's per-wave row staging: past the area the
+// two groups' (m, l, O) merge uses (16384 + 512 floats)
+constexpr int kEpiStageOffset = 68 * 1024;
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
@@ -125,17 +128,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   const int grp = wid >> 2, wq = wid & 3;  // group, and wave inside it (32 query rows)
   const int g = lane >> 5, lq = lane & 31;
   const AttnUnit u = p.units[blockIdx.x];
-  const int32_t* __restrict__ tuples = p.tuples;
-  const int32_t gb = p.goff[u.group], ge = p.goff[u.group + 1];
-  const int n = ge - gb;
-  const int tb = gb + (int)(((int64_t)u.part * n) / u.n_parts);
-  const int te = gb + (int)(((int64_t)(u.part + 1) * n) / u.n_parts);
-  const int qd = p.q_dim, kd = p.k_dim;
-
-  // every tuple of the group carries the same output and Q blocks
-  const DevBlk& qblk = p.blk_q[tuples[(int64_t)gb * 4 + 1]];
-  const DevBlk& oblk = p.blk_o[tuples[(int64_t)gb * 4 + 0]];
-  const int q_lo = qblk.lo[qd];
+  // the unit's blocks, resolved at plan time from the tuple table
+  const AttnUnitMeta& um = p.meta[blockIdx.x];
+  const int nt = ld_uniform(&um.nt);
+  const int q_lo = ld_uniform(&um.q_lo);
+  const int64_t qoff = ld_uniform(&um.qoff), ooff = ld_uniform(&um.ooff);
   const int row = u.q0 + wq * 32 + lq;  // this lane's query row inside the block
   const int qpos = q_lo + row;          // its position
   const int qpos_wave_min = q_lo + u.q0 + wq * 32;
@@ -145,10 +142,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   const bool causal = p.causal != 0;
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t*)sKV;
 
+  // the unit's tuples' K/V metadata (nt <= kAttnMaxUnitTuples: host
+  // guarantee), loaded first so that its wait does not cover the Q loads
+  AttnKv kv{};
+  if (tid < nt) kv = um.kv[tid];
+
   // Q^T operand: lane holds Q[row][16 s + 8 g .. + 7] for s = 0..7
   uint4 qreg[8];
   {
-    const char* qrow = p.q + qblk.off + (int64_t)row * D * 2;
+    const char* qrow = p.q + qoff + (int64_t)row * D * 2;
 #pragma unroll
     for (int s = 0; s < 8; ++s) qreg[s] = *reinterpret_cast<const uint4*>(qrow + (16 * s + 8 * g) * 2);
   }
@@ -158,20 +160,20 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   for (int i = 0; i < 4; ++i) acc_o[i] = f32x16_t{};
   float m = -INFINITY, l = 0.0f;  // running max (log2 domain, scaled) and sum
 
-  // the unit's tuples' K/V metadata into LDS (nt <= kAttnMaxUnitTuples: host guarantee)
-  const int nt = te - tb;
+  // metadata into LDS; the barrier waits for LDS only (not for the Q loads,
+  // which stay in flight under the first chunk loads)
   if (tid < nt) {
-    const int32_t* tp = tuples + (int64_t)(tb + tid) * 4;
-    const DevBlk& kb = p.blk_k[tp[2]];
-    const DevBlk& vb = p.blk_v[tp[3]];
     KvMeta mt;
-    mt.koff = kb.off;
-    mt.voff = vb.off;
-    mt.klo = kb.lo[kd];
-    mt.kext = kb.ext[kd];
+    mt.koff = kv.koff;
+    mt.voff = kv.voff;
+    mt.klo = kv.klo;
+    mt.kext = kv.kext;
     s_tm[tid] = mt;
   }
-  __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
   // The unit's 64-key chunks, ascending: (tuple, offset) pairs up to the
   // first chunk past the tile's last query (later ones are masked for every row).
   int nc = 0;
@@ -453,7 +455,33 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   // row d = 32 dt + 8 (r/4) + 4 g + r%4, column = this lane's query.
   if (grp != 0) return;
   const float inv = l > 0.0f ? 1.0f / l : 0.0f;
-  char* orow = p.o + oblk.off;
+  char* orow = p.o + ooff;
+  if (p.dt_o == EA_BF16) {
+    // Each wave stages its 32 rows in its own LDS region (past the group
+    // merge area, so no barrier with the other waves) and writes them as
+    // 16-byte pieces of contiguous rows: the tile's rows are contiguous in
+    // the O block, so every store instruction writes whole lines.
+    constexpr int kPitch = 128 * 2 + 16;  // bytes per staged row
+    char* stage = reinterpret_cast<char*>(sKV) + kEpiStageOffset + wq * 32 * kPitch;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int d = 32 * dt + 8 * rr + 4 * g;
+        uint2 w;
+        w.x = pack_bf16x2(acc_o[dt][4 * rr] * inv, acc_o[dt][4 * rr + 1] * inv);
+        w.y = pack_bf16x2(acc_o[dt][4 * rr + 2] * inv, acc_o[dt][4 * rr + 3] * inv);
+        *reinterpret_cast<uint2*>(stage + lq * kPitch + d * 2) = w;
+      }
+    const int64_t row0 = u.q0 + wq * 32;  // first row of this wave inside the block
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int c = k * 64 + lane, r = c >> 4, c16 = c & 15;
+      const uint4 v = *reinterpret_cast<const uint4*>(stage + r * kPitch + c16 * 16);
+      *reinterpret_cast<uint4*>(orow + ((row0 + r) * D + c16 * 8) * 2) = v;
+    }
+    return;
+  }
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -462,18 +490,47 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
       const int64_t idx = (int64_t)row * D + d;
       const float o0 = acc_o[dt][4 * rr] * inv, o1 = acc_o[dt][4 * rr + 1] * inv;
       const float o2 = acc_o[dt][4 * rr + 2] * inv, o3 = acc_o[dt][4 * rr + 3] * inv;
-      if (p.dt_o == EA_BF16) {
-        uint2 w;
-        w.x = (uint32_t)f32_to_bf16(o0) | ((uint32_t)f32_to_bf16(o1) << 16);
-        w.y = (uint32_t)f32_to_bf16(o2) | ((uint32_t)f32_to_bf16(o3) << 16);
-        *reinterpret_cast<uint2*>(orow + idx * 2) = w;
-      } else {
-        *reinterpret_cast<float4*>(orow + idx * 4) = make_float4(o0, o1, o2, o3);
-      }
+      *reinterpret_cast<float4*>(orow + idx * 4) = make_float4(o0, o1, o2, o3);
     }
 }
 
+// Plan time: per unit, the Q and O blocks of its group and the K/V blocks of
+// its run of tuples (one lane per tuple), from the GPU-built tuple table.
+__global__ __launch_bounds__(64) void attn_prep_kernel(const AttnArgs p) {
+  const AttnUnit u = p.units[blockIdx.x];
+  const int32_t gb = p.goff[u.group], ge = p.goff[u.group + 1];
+  const int n = ge - gb;
+  const int tb = gb + (int)(((int64_t)u.part * n) / u.n_parts);
+  const int te = gb + (int)(((int64_t)(u.part + 1) * n) / u.n_parts);
+  AttnUnitMeta& um = p.meta[blockIdx.x];
+  const int lane = threadIdx.x;
+  if (lane == 0) {
+    // every tuple of the group carries the same output and Q blocks
+    const DevBlk& qb = p.blk_q[p.tuples[(int64_t)gb * 4 + 1]];
+    um.qoff = qb.off;
+    um.ooff = p.blk_o[p.tuples[(int64_t)gb * 4 + 0]].off;
+    um.q_lo = qb.lo[p.q_dim];
+    um.nt = te - tb;
+  }
+  for (int t = lane; t < te - tb && t < kAttnMaxUnitTuples; t += 64) {
+    const int32_t* tp = p.tuples + (int64_t)(tb + t) * 4;
+    const DevBlk& kb = p.blk_k[tp[2]];
+    AttnKv kv;
+    kv.koff = kb.off;
+    kv.voff = p.blk_v[tp[3]].off;
+    kv.klo = kb.lo[p.k_dim];
+    kv.kext = kb.ext[p.k_dim];
+    um.kv[t] = kv;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_attention_prep(const AttnArgs& a, hipStream_t s) {
+  if (a.n_units == 0) return hipSuccess;
+  hipLaunchKernelGGL(attn_prep_kernel, dim3((uint32_t)a.n_units), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.n_units == 0) return hipSuccess;

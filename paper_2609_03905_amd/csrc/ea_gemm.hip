@@ -264,11 +264,9 @@ __device__ __forceinline__ void epilogue(const f32x16_t (&acc)[NB][4][WN], const
           }
           uint32_t w[4];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const uint32_t h0 = DT == EA_BF16 ? f32_to_bf16(o[2 * q]) : f32_to_f16(o[2 * q]);
-            const uint32_t h1 = DT == EA_BF16 ? f32_to_bf16(o[2 * q + 1]) : f32_to_f16(o[2 * q + 1]);
-            w[q] = h0 | (h1 << 16);
-          }
+          for (int q = 0; q < 4; ++q)
+            w[q] = DT == EA_BF16 ? pack_bf16x2(o[2 * q], o[2 * q + 1])
+                                 : (uint32_t)f32_to_f16(o[2 * q]) | ((uint32_t)f32_to_f16(o[2 * q + 1]) << 16);
           *reinterpret_cast<uint4*>(e.c + idx * 2) = make_uint4(w[0], w[1], w[2], w[3]);
         }
       }

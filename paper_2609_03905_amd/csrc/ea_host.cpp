@@ -319,6 +319,7 @@ struct Plan {
   int gemm_parts = 1;
   // rows
   RowLayout rows;
+  AttnUnitMeta* attn_meta = nullptr;
   // attention scratch
   float* part_o = nullptr;
   float* part_ml = nullptr;
@@ -622,6 +623,7 @@ struct Extra {
   int64_t n_work = 0;
   // attention scratch layout (offsets inside the scratch area)
   size_t part_o = 0, part_ml = 0, counters = 0;
+  size_t meta = 0;  // attention: per-unit block metadata (filled at plan time)
 };
 
 int build_generic(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation* const* ops,
@@ -965,6 +967,7 @@ int build_attention(const ea_relation* const* ops, const OpInfo& oi, const JoinI
                    [](const AttnUnit& a, const AttnUnit& b) { return a.weight > b.weight; });
   ex->work = img->put_vec(units);
   ex->n_work = (int64_t)units.size();
+  ex->meta = img->put_zero(units.size() * sizeof(AttnUnitMeta));
   ex->part_o = 0;
   ex->part_ml = (size_t)slot * 128 * 128 * sizeof(float);
   ex->counters = ex->part_ml + (size_t)slot * 128 * 2 * sizeof(float);
@@ -1038,6 +1041,24 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
   }
   e = finish_join(p.get(), js, sp.n_in + 1, s);
   if (e) return e;
+  if (oi.kind == K_ATTENTION) {
+    p->attn_meta = (AttnUnitMeta*)(p->dmem + ex.meta);
+    AttnArgs a;
+    memset(&a, 0, sizeof(a));
+    a.tuples = p->d_tuples;
+    a.goff = p->d_goff;
+    a.blk_q = p->d_blk[0];
+    a.blk_k = p->d_blk[1];
+    a.blk_v = p->d_blk[2];
+    a.blk_o = p->d_blk[3];
+    a.units = (const AttnUnit*)p->d_work;
+    a.n_units = (int32_t)p->n_work;
+    a.q_dim = oi.q_dim;
+    a.k_dim = oi.k_dim;
+    a.meta = p->attn_meta;
+    EA_HIP_TRY(launch_attention_prep(a, s));
+    EA_HIP_TRY(hipStreamSynchronize(s));
+  }
   *out = p.get();
   cache()[key] = std::move(p);
   return EA_OK;
@@ -1383,6 +1404,7 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
       a.part_ml = plan->part_ml;
       a.counters = plan->counters;
       a.dt_o = out->dtype;
+      a.meta = plan->attn_meta;
       EA_HIP_TRY(launch_attention(a, s));
       break;
     }

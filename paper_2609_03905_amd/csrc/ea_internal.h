@@ -226,6 +226,20 @@ struct AttnUnit {
 
 constexpr int kAttnMaxUnitTuples = 32;  // key blocks per attention work unit (LDS table size)
 
+// Per-unit block metadata, resolved once per plan from the GPU-built tuple
+// table (attention prep kernel), so that the attention kernel reaches its
+// first loads without the chain unit -> group offsets -> tuples -> blocks.
+struct AttnKv {
+  int64_t koff, voff;  // byte offsets of the K and V blocks
+  int32_t klo, kext;   // key interval of the block
+};
+struct AttnUnitMeta {
+  int64_t qoff, ooff;  // byte offsets of the unit's Q and O blocks
+  int32_t q_lo, nt;    // query position of the Q block's first row; the unit's tuples
+  int32_t pad[2];
+  AttnKv kv[kAttnMaxUnitTuples];
+};
+
 struct AttnArgs {
   const int32_t* tuples;
   const int32_t* goff;
@@ -246,8 +260,11 @@ struct AttnArgs {
   float* part_ml;        // [slots][128 rows][2]
   int32_t* counters;     // one per split (group, tile); zero between calls
   int32_t dt_o;
+  AttnUnitMeta* meta;    // one per unit (written by the prep kernel at plan time)
 };
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+// Plan time: fill a.meta from the tuple table (a's data pointers unused).
+hipError_t launch_attention_prep(const AttnArgs& a, hipStream_t s);
 
 }  // namespace ea

@@ -286,8 +286,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
         uint4 pk;
         uint32_t* w = reinterpret_cast<uint32_t*>(&pk);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          w[i] = (uint32_t)f32_to_bf16(o[2 * i]) | ((uint32_t)f32_to_bf16(o[2 * i + 1]) << 16);
+        for (int i = 0; i < 4; ++i) w[i] = pack_bf16x2(o[2 * i], o[2 * i + 1]);
         store_out<STREAM>(yp, pk);
       } else if (a.dt_y == EA_F32 && ES == 4) {
         store_out<STREAM>(yp, make_uint4(__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]),
