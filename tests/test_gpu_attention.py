@@ -100,3 +100,19 @@ def test_attention_closed_forms():
     got = values(O)
     assert_close(got, prefix_mean, rel_fro=1e-3, what="zero keys")
     np.testing.assert_allclose(got[0, 0, 0], fv[0, 0, 0], rtol=1e-3, atol=1e-3)
+
+
+def test_attention_single_block_and_first_query():
+    # one query and one key block of 128 per head (a single work unit, no merge);
+    # causal: query 0 sees only key 0, so its output is value row 0 exactly
+    B, H, S = 1, 3, 128
+    q, k, v = (synth.normal((B, H, S, 128), 450 + i, dtype="bf16") for i in range(3))
+    p = [[0, 1], synth.splits(H, 1), [0, 128], [0, 128]]
+    scale = 1.0 / np.sqrt(128)
+    for causal in (True, False):
+        O = _run(q, k, v, p, p, scale, causal, "f32")
+        ref = oracle.attention(*(synth.to_f64(a, "bf16") for a in (q, k, v)), causal, scale)
+        got = values(O)
+        assert_close(got, ref, rel_fro=1e-3, what=f"single block, causal={causal}")
+        if causal:
+            assert np.array_equal(got[:, :, 0, :], synth.to_f64(v, "bf16")[:, :, 0, :])

@@ -131,6 +131,78 @@ def test_swiglu_f16_inputs():
     assert_close(values(A), expected(ref, "f16"), what="swiglu f16")
 
 
+def test_gemm_many_split_parts_deterministic():
+    # one 256x256 output tile over 8 contracted blocks: the key is split over
+    # several workgroups (more than two parts: the part-order sum), merged by
+    # the last to arrive; parity with the oracle, and the same bits every run
+    T, J, K = 256, 4096, 256
+    p = [synth.splits(T, 256), synth.splits(J, 512)]
+    x = synth.normal((T, J), 45, dtype="bf16")
+    w = synth.normal((J, K), 46, 0.05, dtype="bf16")
+    X, W = upload(x, "bf16", p), upload(w, "bf16", [synth.splits(J, 512), synth.splits(K, 256)])
+    pout = [synth.splits(T, 256), synth.splits(K, 256)]
+    Y = empty((T, K), "f32", pout)
+    ea.joinagg("tj,jk->tk", ea.JOIN_MUL, ea.AGG_SUM, [X, W], Y)
+    ref = oracle.matmul(synth.to_f64(x, "bf16"), synth.to_f64(w, "bf16"))
+    assert_close(values(Y), ref, rel_fro=1e-5, what="gemm, many split parts")
+    for _ in range(3):
+        Y2 = empty((T, K), "f32", pout)
+        ea.joinagg("tj,jk->tk", ea.JOIN_MUL, ea.AGG_SUM, [X, W], Y2)
+        torch.cuda.synchronize()
+        assert torch.equal(Y.bytes(), Y2.bytes())
+
+
+def _sampled_rows(T, band=256, rng_seed=3):
+    # a few rows of every 256-row tile band, its first and last among them
+    rng = np.random.default_rng(rng_seed)
+    rows = []
+    for b0 in range(0, T, band):
+        b1 = min(T, b0 + band)
+        rows += [b0, b1 - 1] + list(rng.choice(np.arange(b0 + 1, b1 - 1), 2, replace=False))
+    return np.array(sorted(set(rows)))
+
+
+@pytest.mark.parametrize("swiglu", [False, True])
+def test_gemm_block_share_shapes_full_size_sampled_rows(swiglu):
+    # 2048 tokens x 8192 hidden in 512-blocks against a 3072-wide projection
+    # (96 tiles, keys split in two) or SwiGLU's two 2752-wide weights (176
+    # tiles, a ragged last column block): every tile is checked on sampled
+    # rows, and repeated calls give the same bytes
+    T, J, F = 2048, 8192, 2752 if swiglu else 3072
+    pt, pj, pf = synth.splits(T, 512), synth.splits(J, 512), synth.splits(F, 512)
+    x = synth.normal((T, J), 55, dtype="bf16")
+    ws = [synth.normal((J, F), 56 + i, 0.02, dtype="bf16") for i in range(2 if swiglu else 1)]
+    X = upload(x, "bf16", [pt, pj])
+    Ws = [upload(w, "bf16", [pj, pf]) for w in ws]
+    spec, op = ("tj,jk,jk->tk", ea.OP_SWIGLU) if swiglu else ("tj,jk->tk", ea.JOIN_MUL)
+    Y = empty((T, F), "bf16", [pt, pf])
+    ea.joinagg(spec, op, ea.AGG_SUM, [X] + Ws, Y)
+    rows = _sampled_rows(T)
+    fx = synth.to_f64(x, "bf16")[rows]
+    prods = [oracle.matmul(fx, synth.to_f64(w, "bf16")) for w in ws]
+    ref = oracle.silu_mul(*prods) if swiglu else prods[0]
+    assert_close(values(Y)[rows], expected(ref, "bf16"), what="block-share GEMM, sampled rows")
+    for _ in range(2):
+        Y2 = empty((T, F), "bf16", [pt, pf])
+        ea.joinagg(spec, op, ea.AGG_SUM, [X] + Ws, Y2)
+        torch.cuda.synchronize()
+        assert torch.equal(Y.bytes(), Y2.bytes())
+
+
+@pytest.mark.parametrize("T,J,K", [(1, 32, 8), (3, 8, 8), (1, 64, 256), (5, 96, 40), (257, 32, 264)])
+def test_gemm_tiny_and_single_row_shapes(T, J, K):
+    # a single tile mostly masked: one row, one 8-wide column group, a
+    # contracted extent of one MFMA step (direct path) or of 8 (register path)
+    x = synth.normal((T, J), 47, dtype="bf16")
+    w = synth.normal((J, K), 48, 0.1, dtype="bf16")
+    pt, pj, pk = synth.whole(T), synth.whole(J), synth.whole(K)
+    X, W = upload(x, "bf16", [pt, pj]), upload(w, "bf16", [pj, pk])
+    Y = empty((T, K), "f32", [pt, pk])
+    ea.joinagg("tj,jk->tk", ea.JOIN_MUL, ea.AGG_SUM, [X, W], Y)
+    ref = oracle.matmul(synth.to_f64(x, "bf16"), synth.to_f64(w, "bf16"))
+    assert_close(values(Y), ref, rel_fro=1e-5, what=f"gemm {T}x{J}x{K}")
+
+
 def test_gemm_integer_data_bitexact_and_residual():
     T, J, K = 256, 512, 384
     pt, pj, pk = synth.splits(T, 128), synth.splits(J, 128), synth.splits(K, 128)
@@ -280,3 +352,37 @@ def test_softmax_ragged_and_f32(causal):
     ea.joinagg("hqk->hqk", ea.OP_SOFTMAX, ea.AGG_LSE, [Sr], P, causal=causal)
     ref = oracle.softmax(synth.to_f64(s, "f32"), causal)
     assert_close(values(P), ref, rel_fro=1e-5, what="softmax ragged")
+
+
+@pytest.mark.parametrize("T,C", [(1, 1), (1, 7), (5, 1), (1, 4096)])
+def test_rmsnorm_degenerate_shapes(T, C):
+    # one row and/or one column: with C = 1 every output is w / sqrt(1 + eps / x^2)
+    x = synth.normal((T, C), 67, dtype="bf16")
+    wv = synth.uniform((C,), 68, 0.5, 1.5, dtype="bf16")
+    pt, pc = synth.whole(T), synth.whole(C)
+    X, Wt = upload(x, "bf16", [pt, pc]), upload(wv, "bf16", [pc])
+    Y = empty((T, C), "f32", [pt, pc])
+    ea.joinagg("tc,c->tc", ea.OP_RMSNORM, ea.AGG_SUM, [X, Wt], Y, eps=1e-6)
+    fx, fw = synth.to_f64(x, "bf16"), synth.to_f64(wv, "bf16")
+    ref = oracle.rmsnorm(fx, fw, 1e-6)
+    assert_close(values(Y), ref, rel_fro=1e-5, what=f"rmsnorm {T}x{C}")
+    if C == 1:
+        assert_close(values(Y), np.sign(fx) * fw / np.sqrt(1 + 1e-6 / fx ** 2), rel_fro=1e-5, what="C = 1")
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_softmax_degenerate_shapes(causal):
+    # one key per row gives exactly 1; a 1 x 1 causal block is its diagonal;
+    # one query row over many key blocks sees only key 0 when causal
+    for shape, parts in [((3, 5, 1), [synth.splits(3, 1), synth.whole(5), [0, 1]]),
+                         ((1, 1, 1), [[0, 1], [0, 1], [0, 1]]),
+                         ((1, 1, 300), [[0, 1], [0, 1], [0, 100, 200, 300]])]:
+        s = synth.normal(shape, 73, 2.0, dtype="bf16")
+        Sr = upload(s, "bf16", parts)
+        P = empty(shape, "f32", parts)
+        ea.joinagg("hqk->hqk", ea.OP_SOFTMAX, ea.AGG_LSE, [Sr], P, causal=causal)
+        got = values(P)
+        ref = oracle.softmax(synth.to_f64(s, "bf16"), causal)
+        assert_close(got, ref, rel_fro=1e-5, what=f"softmax {shape}")
+        if shape[2] == 1 or causal:
+            assert np.all(got[..., 0] == 1.0) and np.all(got[..., 1:] == 0.0)
