@@ -27,7 +27,11 @@ Pin status (what each function is checked against, in tests/test_oracle_pins.py)
   rmsnorm .......... torch rms_norm (library), constant-row closed form
   softmax .......... torch softmax (library), constant-row 1/(q+1) closed form
   attention ........ torch scaled_dot_product_attention (library), equal-V and
-                     zero-K closed forms
+                     zero-K closed forms; grouped-query heads against SDPA on
+                     K/V heads repeated per group, packed sequences against
+                     SDPA run on each sequence alone
+  join (attention predicates) grouped-query and packed-sequence tuple counts
+                     in closed form (the paper's three-sequence example)
   llama_block ...... composition of the pinned parts only: the paper does not
                      define the block, so its chain is "parity unpinned" beyond
                      that composition
@@ -77,12 +81,18 @@ def lib():
         L.or_join.restype = ctypes.c_int64
         L.or_join.argtypes = [ctypes.c_char_p, i64p, i64p, ctypes.c_char_p, ctypes.c_char, ctypes.c_char,
                               ctypes.POINTER(ctypes.c_int32), ctypes.c_int64, i64p, ctypes.c_int64, i64p]
+        L.or_join_ex.restype = ctypes.c_int64
+        L.or_join_ex.argtypes = [ctypes.c_char_p, i64p, i64p, ctypes.c_char_p, ctypes.c_char, ctypes.c_char,
+                                 ctypes.c_int, ctypes.c_int64, i64p, ctypes.c_int64, ctypes.c_char, ctypes.c_char,
+                                 ctypes.POINTER(ctypes.c_int32), ctypes.c_int64, i64p, ctypes.c_int64, i64p]
         L.or_einsum.argtypes = [ctypes.c_char_p, ctypes.c_int, ctypes.c_int, i64p,
                                 ctypes.POINTER(dp), dp]
         L.or_matmul.argtypes = [ctypes.c_int64] * 3 + [dp, dp, dp]
         L.or_rmsnorm.argtypes = [ctypes.c_int64, ctypes.c_int64, dp, dp, ctypes.c_double, dp]
         L.or_softmax.argtypes = [ctypes.c_int64] * 3 + [dp, ctypes.c_int, dp]
         L.or_attention.argtypes = [ctypes.c_int64] * 4 + [dp, dp, dp, ctypes.c_int, ctypes.c_double, dp]
+        L.or_attention_ex.argtypes = [ctypes.c_int64] * 5 + [dp, dp, dp, ctypes.c_int, ctypes.c_double,
+                                                            ctypes.c_int64, i64p, dp]
         L.or_silu_mul.argtypes = [ctypes.c_int64, dp, dp, dp]
         L.or_add.argtypes = [ctypes.c_int64, dp, dp, dp]
         _lib = L
@@ -183,13 +193,20 @@ def repartition(blocked: np.ndarray, src_partition, dst_partition, dtype) -> np.
 # --------------------------------------------------------------------------
 # join (Section 3.2 Definitions "Join-agg spec" and "Implementation" step 1)
 # --------------------------------------------------------------------------
-def join(spec: str, partitions, group: str | None = None, causal: tuple[str, str] | None = None):
+def join(spec: str, partitions, group: str | None = None, causal: tuple[str, str] | None = None,
+         positions: tuple[str, str] | None = None, seq_ends=None, gqa: tuple[int, str, str] | None = None):
     """Brute-force join of block relations.
 
     partitions: one partition per operand (inputs, then the output).
     group: letters whose block coordinates form the group key (default: the
-    output letters).  causal: (q_letter, k_letter) keeps a tuple iff its k
-    block starts at or before its last q position.
+    output letters).  causal: (q_letter, k_letter) keeps a tuple iff some q
+    position of its q block is at or after some k position of its k block.
+    Attention predicates (Section 3.2, Example "Flash attention"):
+    positions (q_letter, k_letter) with seq_ends, the ends of packed
+    sequences, keep a tuple iff some q position and some k position of its
+    blocks lie in one sequence (and satisfy causal order, if causal);
+    gqa (G, h_letter, g_letter) keeps it iff every query head h of its
+    h block reads key/value head h // G inside its g block.
     Returns (tuples int32 [n, 1 + n_in] = (out_block, in_blocks...), group_off int64).
     """
     out_letters = spec.split("->")[1]
@@ -199,17 +216,24 @@ def join(spec: str, partitions, group: str | None = None, causal: tuple[str, str
     sp = _i64([p for part in partitions for s in part for p in s])
     n_in = len(spec.split("->")[0].split(","))
     ng = np.zeros(1, dtype=np.int64)
-    cq = causal[0].encode() if causal else b"\0"
-    ck = causal[1].encode() if causal else b"\0"
+    pos = causal or positions
+    pq = pos[0].encode() if pos else b"\0"
+    pk = pos[1].encode() if pos else b"\0"
+    ends = _i64(seq_ends if seq_ends is not None else [0])
+    n_seq = 0 if seq_ends is None else len(seq_ends)
+    G, gh, gg = (gqa[0], gqa[1].encode(), gqa[2].encode()) if gqa else (1, b"\0", b"\0")
     L = lib()
-    n = L.or_join(spec.encode(), _i64p(nb), _i64p(sp), group.encode(), cq, ck, None, 0, None, 0, _i64p(ng))
+
+    def call(tp, cap, go, gcap):
+        return L.or_join_ex(spec.encode(), _i64p(nb), _i64p(sp), group.encode(), pq, pk, int(causal is not None),
+                            n_seq, _i64p(ends), G, gh, gg, tp, cap, go, gcap, _i64p(ng))
+
+    n = call(None, 0, None, 0)
     if n < 0:
         raise ValueError(f"oracle join failed with code {n}")
     tuples = np.zeros((max(n, 1), n_in + 1), dtype=np.int32)
     goff = np.zeros(int(ng[0]) + 1, dtype=np.int64)
-    n2 = L.or_join(spec.encode(), _i64p(nb), _i64p(sp), group.encode(), cq, ck,
-                   tuples.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), tuples.shape[0],
-                   _i64p(goff), goff.size, _i64p(ng))
+    n2 = call(tuples.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), tuples.shape[0], _i64p(goff), goff.size)
     if n2 != n:
         raise ValueError(f"oracle join failed with code {n2}")
     return tuples[:n], goff
@@ -269,6 +293,20 @@ def attention(q, k, v, causal: bool, scale: float) -> np.ndarray:
     B, H, S, D = q.shape
     o = np.empty_like(q)
     _check(lib().or_attention(B, H, S, D, _dp(q), _dp(k), _dp(v), int(causal), scale, _dp(o)), "attention")
+    return o
+
+
+def attention_ex(q, k, v, causal: bool, scale: float, seq_ends=None) -> np.ndarray:
+    """Attention with grouped-query heads (k, v [B, Hkv, S, D], query head h
+    reading key/value head h // (Hq // Hkv)) and packed sequences ending at
+    seq_ends (None: one sequence); Section 3.2, Example "Flash attention"."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    B, Hq, S, D = q.shape
+    Hkv = k.shape[1]
+    ends = _i64(seq_ends if seq_ends is not None else [S])
+    o = np.empty_like(q)
+    _check(lib().or_attention_ex(B, Hq, Hkv, S, D, _dp(q), _dp(k), _dp(v), int(causal), scale,
+                                 0 if seq_ends is None else len(ends), _i64p(ends), _dp(o)), "attention_ex")
     return o
 
 

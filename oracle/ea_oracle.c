@@ -262,10 +262,54 @@ static int tuple_cmp(const void* a, const void* b) {
   return 0;
 }
 
+/* Sequence of position x among packed sequences ending at ends[0..n): the
+   number of ends at or below x (Section 3.2, Example "Flash attention"). */
+static int64_t seq_index(const int64_t* ends, int64_t n, int64_t x) {
+  int64_t s = 0;
+  while (s < n && ends[s] <= x) ++s;
+  return s;
+}
+
+/* Attention visibility of key position kp to query position qp: the same
+   sequence (when sequences are given) and, when causal, kp <= qp. */
+static int visible(int64_t qp, int64_t kp, int causal, const int64_t* ends, int64_t n_seq) {
+  if (causal && kp > qp) return 0;
+  if (n_seq > 0 && seq_index(ends, n_seq, qp) != seq_index(ends, n_seq, kp)) return 0;
+  return 1;
+}
+
+int64_t or_join_ex(const char* spec, const int64_t* nblocks_all, const int64_t* splits_all,
+                   const char* group, char pos_q, char pos_k, int causal, int64_t n_seq,
+                   const int64_t* seq_ends, int64_t gqa, char gqa_h, char gqa_g,
+                   int32_t* tuples, int64_t cap, int64_t* group_off, int64_t gcap,
+                   int64_t* n_groups_out);
+
+/* The plain join: causal_q/causal_k (0 = none) name the letters of the
+   causal predicate. */
 int64_t or_join(const char* spec, const int64_t* nblocks_all, const int64_t* splits_all,
                 const char* group, char causal_q, char causal_k,
                 int32_t* tuples, int64_t cap, int64_t* group_off, int64_t gcap,
                 int64_t* n_groups_out) {
+  return or_join_ex(spec, nblocks_all, splits_all, group, causal_q, causal_k, causal_q != 0, 0, NULL, 1, 0, 0,
+                    tuples, cap, group_off, gcap, n_groups_out);
+}
+
+/* The join with attention's predicates.  pos_q/pos_k name the query and key
+   position letters (0: no position predicate).  A tuple is kept iff some
+   query position of its query block sees some key position of its key block
+   (visible() above: causal order if `causal`, and with n_seq > 0 packed
+   sequences the same sequence).  gqa > 1: grouped-query heads, letter gqa_h
+   (query heads) over gqa_g (key/value heads); a tuple is kept iff every
+   query head h of its gqa_h block reads key/value head floor(h / gqa),
+   inside its gqa_g block. */
+int64_t or_join_ex(const char* spec, const int64_t* nblocks_all, const int64_t* splits_all,
+                   const char* group, char pos_q, char pos_k, int causal, int64_t n_seq,
+                   const int64_t* seq_ends, int64_t gqa, char gqa_h, char gqa_g,
+                   int32_t* tuples, int64_t cap, int64_t* group_off, int64_t gcap,
+                   int64_t* n_groups_out) {
+  const char causal_q = pos_q, causal_k = pos_k;
+  if ((causal || n_seq > 0) && !pos_q) return -1;
+  if (n_seq < 0 || (n_seq > 0 && !seq_ends) || gqa < 1 || (gqa > 1 && (!gqa_h || !gqa_g))) return -1;
   or_spec sp;
   if (parse_spec(spec, &sp) || !nblocks_all || !splits_all || !group) return -1;
   const int n_in = sp.n_ops - 1, out = n_in;
@@ -317,6 +361,15 @@ int64_t or_join(const char* spec, const int64_t* nblocks_all, const int64_t* spl
       if ((ck_dim = find_dim(&sp, o, causal_k)) >= 0) ck_op = o;
     if (cq_op < 0 || ck_op < 0) return -1;
   }
+  /* grouped-query head letters */
+  int gh_op = -1, gh_dim = -1, gg_op = -1, gg_dim = -1;
+  if (gqa > 1) {
+    for (int o = 0; o < n_in && gh_op < 0; ++o)
+      if ((gh_dim = find_dim(&sp, o, gqa_h)) >= 0) gh_op = o;
+    for (int o = 0; o < n_in && gg_op < 0; ++o)
+      if ((gg_dim = find_dim(&sp, o, gqa_g)) >= 0) gg_op = o;
+    if (gh_op < 0 || gg_op < 0) return -1;
+  }
 
   int64_t n_comb = 1;
   for (int o = 0; o < n_in; ++o) n_comb *= nb_tot[o];
@@ -350,7 +403,19 @@ int64_t or_join(const char* spec, const int64_t* nblocks_all, const int64_t* spl
           if (d2 >= 0 && (lo[o2][d2] != lo[o][d] || hi[o2][d2] != hi[o][d])) ok = 0;
         }
     if (!ok) continue;
-    if (causal_q && !(lo[ck_op][ck_dim] <= hi[cq_op][cq_dim] - 1)) continue;
+    if (causal_q && (causal || n_seq > 0)) {
+      int any = 0;
+      for (int64_t qp = lo[cq_op][cq_dim]; qp < hi[cq_op][cq_dim] && !any; ++qp)
+        for (int64_t kp = lo[ck_op][ck_dim]; kp < hi[ck_op][ck_dim] && !any; ++kp)
+          any = visible(qp, kp, causal, seq_ends, n_seq);
+      if (!any) continue;
+    }
+    if (gqa > 1) {
+      int all = 1;
+      for (int64_t h = lo[gh_op][gh_dim]; h < hi[gh_op][gh_dim] && all; ++h)
+        all = h / gqa >= lo[gg_op][gg_dim] && h / gqa < hi[gg_op][gg_dim];
+      if (!all) continue;
+    }
     /* output block: the one whose intervals equal the tuple's on every output letter */
     or_tuple t;
     memset(&t, 0, sizeof(t));
@@ -584,6 +649,58 @@ int or_attention(int64_t B, int64_t H, int64_t S, int64_t D, const double* q,
       }
     }
     free(srow);
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Attention with grouped-query heads and packed sequences (Section 3.2,     */
+/* Example "Flash attention"): q [B, Hq, S, D], k and v [B, Hkv, S, D] with   */
+/* Hq a multiple of Hkv; query head h reads key/value head h / (Hq / Hkv).   */
+/* The sequence axis holds n_seq sequences ending at seq_ends (n_seq 0: one  */
+/* sequence).  Query qi sees key j iff visible(qi, j): same sequence and,    */
+/* if causal, j <= qi.  s = scale * q.k; o = softmax over the visible keys   */
+/* of s, times v.  A row with no visible key (impossible for the causal or   */
+/* packed rules, which keep j = qi) is 0.                                    */
+/* ------------------------------------------------------------------------ */
+int or_attention_ex(int64_t B, int64_t Hq, int64_t Hkv, int64_t S, int64_t D, const double* q,
+                    const double* k, const double* v, int causal, double scale, int64_t n_seq,
+                    const int64_t* seq_ends, double* o) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || S < 1 || D < 1 || !q || !k || !v || !o) return -1;
+  if (n_seq < 0 || (n_seq > 0 && (!seq_ends || seq_ends[n_seq - 1] != S))) return -1;
+  const int64_t G = Hq / Hkv;
+#pragma omp parallel
+  {
+    double* srow = (double*)malloc(sizeof(double) * (size_t)S);
+    char* vis = (char*)malloc((size_t)S);
+#pragma omp for schedule(dynamic, 4)
+    for (int64_t r = 0; r < B * Hq * S; ++r) {
+      const int64_t b = r / (Hq * S), h = (r / S) % Hq, qi = r % S;
+      const double* qr = q + r * D;
+      const double* kb = k + (b * Hkv + h / G) * S * D;
+      const double* vb = v + (b * Hkv + h / G) * S * D;
+      double m = -INFINITY;
+      for (int64_t j = 0; j < S; ++j) {
+        vis[j] = (char)visible(qi, j, causal, seq_ends, n_seq);
+        if (!vis[j]) continue;
+        double acc = 0.0;
+        for (int64_t d = 0; d < D; ++d) acc += qr[d] * kb[j * D + d];
+        srow[j] = scale * acc;
+        m = srow[j] > m ? srow[j] : m;
+      }
+      double l = 0.0;
+      for (int64_t j = 0; j < S; ++j)
+        if (vis[j]) { srow[j] = exp(srow[j] - m); l += srow[j]; }
+      double* orow = o + r * D;
+      for (int64_t d = 0; d < D; ++d) orow[d] = 0.0;
+      for (int64_t j = 0; j < S && l > 0.0; ++j) {
+        if (!vis[j]) continue;
+        const double pj = srow[j] / l;
+        for (int64_t d = 0; d < D; ++d) orow[d] += pj * vb[j * D + d];
+      }
+    }
+    free(srow);
+    free(vis);
   }
   return 0;
 }

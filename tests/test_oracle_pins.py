@@ -354,3 +354,93 @@ def test_llama_block_composition_and_causal_prefix():
     # causal prefix: the first 20 rows of the output depend only on the first 20 rows of x
     pre = oracle.llama_block(f["x"][:20], *args[1:], heads=2, d_head=16, eps=1e-6)
     np.testing.assert_array_equal(pre["y"], out["y"][:20])
+
+
+# ---------------------------------------------------------------------------
+# grouped-query heads and packed sequences (Section 3.2, Example "Flash
+# attention")
+# ---------------------------------------------------------------------------
+def _flash_example():
+    with open(os.path.join(GOLDEN, "flash_attention_example.json")) as f:
+        return json.load(f)
+
+
+def _sdpa(q, k, v, causal, scale):
+    return F.scaled_dot_product_attention(torch.from_numpy(q), torch.from_numpy(k), torch.from_numpy(v),
+                                          is_causal=causal, scale=scale).numpy()
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_attention_ex_grouped_heads_match_sdpa_on_repeated_kv(causal):
+    # Hq = 8 over Hkv = 2: query head h reads key/value head h // 4, the same
+    # as plain attention with each key/value head repeated for its 4 query heads
+    rng = np.random.default_rng(18)
+    B, Hq, Hkv, S, D = 2, 8, 2, 29, 16
+    q = rng.standard_normal((B, Hq, S, D))
+    k, v = (rng.standard_normal((B, Hkv, S, D)) for _ in range(2))
+    scale = 0.3
+    ref = _sdpa(q, np.repeat(k, Hq // Hkv, axis=1), np.repeat(v, Hq // Hkv, axis=1), causal, scale)
+    np.testing.assert_allclose(oracle.attention_ex(q, k, v, causal, scale), ref, rtol=1e-10, atol=1e-12)
+    # one group: the plain definition
+    ref1 = _sdpa(q, q, q, causal, scale)
+    np.testing.assert_allclose(oracle.attention_ex(q, q, q, causal, scale), ref1, rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_attention_ex_packed_sequences_match_each_sequence_alone(causal):
+    # attention never crosses a sequence end: packed, it equals attention run
+    # on every sequence by itself (here with grouped heads too)
+    rng = np.random.default_rng(19)
+    B, Hq, Hkv, D = 1, 4, 2, 8
+    ends = [7, 20, 21, 40]
+    S = ends[-1]
+    q = rng.standard_normal((B, Hq, S, D))
+    k, v = (rng.standard_normal((B, Hkv, S, D)) for _ in range(2))
+    o = oracle.attention_ex(q, k, v, causal, 0.5, seq_ends=ends)
+    lo = 0
+    for hi in ends:
+        sl = slice(lo, hi)
+        ref = _sdpa(q[:, :, sl], np.repeat(k[:, :, sl], 2, axis=1), np.repeat(v[:, :, sl], 2, axis=1), causal, 0.5)
+        np.testing.assert_allclose(o[:, :, sl], ref, rtol=1e-10, atol=1e-12)
+        lo = hi
+    # a one-position sequence returns its own value row
+    np.testing.assert_allclose(o[0, :, 20], np.repeat(v[0, :, 20], 2, axis=0), rtol=1e-14)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_join_packed_sequences_of_the_papers_example(causal):
+    # ends 1024, 2560, 4096 in 128-blocks: sequences of 8, 12 and 12 blocks;
+    # a query block keeps the key blocks of its own sequence (causal: those at
+    # or before it), so sum n(n+1)/2 = 36 + 78 + 78 = 192 or sum n^2 = 352
+    ex = _flash_example()
+    S, ends = ex["sequence"], ex["ends"]
+    p = [[0, 1], [0, 1], synth.splits(S, 128), [0, 128]]
+    tuples, goff = oracle.join("bhqd,bhkd,bhkd->bhqd", [p, p, p, p], group="bhqd",
+                               causal=("q", "k") if causal else None, positions=("q", "k"), seq_ends=ends)
+    seq = np.searchsorted(ends, np.arange(0, S, 128), side="right")
+    want = [(qb, kb) for qb in range(S // 128) for kb in range(S // 128)
+            if seq[qb] == seq[kb] and (not causal or kb <= qb)]
+    assert len(tuples) == (192 if causal else 352) == len(want)
+    assert [(t[1], t[2]) for t in tuples.tolist()] == want
+    assert np.all(tuples[:, 3] == tuples[:, 2])
+
+
+def test_join_grouped_heads_of_the_papers_example():
+    # 32 query heads over 8 key/value heads: query head h joins only key/value
+    # head h // 4; with the query heads in blocks of 4, block m joins head m
+    ex = _flash_example()
+    Hq, Hkv = ex["heads_q"], ex["heads_kv"]
+    G = Hq // Hkv
+    pk = [[0, 1], synth.splits(Hkv, 1), [0, 256, 512], [0, 128]]
+    for hb in (1, G):
+        pq = [[0, 1], synth.splits(Hq, hb), [0, 256, 512], [0, 128]]
+        tuples, _ = oracle.join("bhqd,bgkd,bgkd->bhqd", [pq, pk, pk, pq], group="bhqd", gqa=(G, "h", "g"))
+        assert len(tuples) == (Hq // hb) * 2 * 2  # head blocks x query blocks x key blocks
+        qhead = tuples[:, 1] // 2  # Q block index = head block * 2 query blocks + query block
+        khead = tuples[:, 2] // 2
+        assert np.all(khead == qhead * hb // G)
+    # query-head blocks straddling two key/value heads join neither
+    pq = [[0, 1], [0, 2, 6, 8], [0, 512], [0, 128]]
+    tuples, _ = oracle.join("bhqd,bgkd,bgkd->bhqd", [pq, [[0, 1], [0, 1, 2], [0, 512], [0, 128]]] * 1 +
+                            [[[0, 1], [0, 1, 2], [0, 512], [0, 128]], pq], group="bhqd", gqa=(4, "h", "g"))
+    assert sorted(t[1] for t in tuples.tolist()) == [0, 2]
