@@ -81,7 +81,8 @@ extern "C" {
 /* Fused operators (each a join-agg with a fixed spec shape):               */
 #define EA_OP_RMSNORM 16   /* "<r>c,c-><r>c": y = w*x/sqrt(mean_c x^2 + eps) */
 #define EA_OP_SOFTMAX 17   /* "<r>k-><r>k": softmax over the last letter      */
-#define EA_OP_ATTENTION 18 /* "<b>qd,<b>kd,<b>kd-><b>qd": softmax(s*QK^T) V   */
+#define EA_OP_ATTENTION 18 /* "<b>qd,<b>kd,<b>kd-><b>qd": softmax(s*QK^T) V;
+                              grouped-query: see ea_params.gqa_group       */
 #define EA_OP_SWIGLU 19    /* "tj,jk,jk->tk": silu(X W1) * (X W2)              */
 
 /* ---- aggregation operations (the combiner of tuples sharing a key) ---- */
@@ -118,6 +119,25 @@ typedef struct ea_params {
      (fused residual): same shape and partition as the output.  Used by the
      einsum path (EA_JOIN_MUL / EA_JOIN_ADD).  NULL = none.                  */
   const ea_relation* residual;
+  /* EA_OP_ATTENTION, grouped-query attention (Section 3.2, Example "Flash
+     attention"): query heads per key-value head.  0 or 1: Q, K and V share
+     every batch letter.  G > 1: K and V name their head letter apart from
+     Q's ("bhqd,bgkd,bgkd->bhqd"), Q's head extent is G times theirs, and
+     query head h reads key-value head floor(h / G); the join keeps a tuple
+     iff the K/V head block holds the heads of the Q head block divided by G.
+     Head letters take one block per index.  Negative: EA_ERR_ARG.           */
+  int32_t gqa_group;
+  /* EA_OP_ATTENTION, packed sequences (same example): the query/key letter
+     holds n_seq independent sequences end to end, ending at the host array
+     seq_ends[0..n_seq) (strictly increasing, the last equal to the extent,
+     read during the call only).  A query attends only to keys of its own
+     sequence (and, if causal, at or before its position); the join keeps a
+     query block and a key block iff they lie in the same sequence.  Every
+     end must be a split point of the query and of the key partition: no
+     block straddles two sequences (EA_ERR_UNSUPPORTED otherwise).  n_seq 0:
+     one sequence; seq_ends NULL with n_seq > 0, or a bad list: EA_ERR_ARG.  */
+  int32_t n_seq;
+  const int64_t* seq_ends;
 } ea_params;
 
 /* ---- version and errors ---------------------------------------------- */

@@ -510,7 +510,7 @@ __global__ __launch_bounds__(64) void attn_prep_kernel(const AttnArgs p) {
     um.qoff = qb.off;
     um.ooff = p.blk_o[p.tuples[(int64_t)gb * 4 + 0]].off;
     um.q_lo = qb.lo[p.q_dim];
-    um.nt = te - tb;
+    um.nt = min(te - tb, kAttnMaxUnitTuples);  // the plan sizes units to fit; a guard on the record
   }
   for (int t = lane; t < te - tb && t < kAttnMaxUnitTuples; t += 64) {
     const int32_t* tp = p.tuples + (int64_t)(tb + t) * 4;

@@ -7,7 +7,8 @@
 // block keys: for each of the operand's letters the candidate interval
 // (lo, hi) must be one of the operand's intervals (binary search on its split
 // points, then an exact comparison of both bounds).  A matched candidate that
-// passes the optional causal predicate becomes a tuple
+// passes the optional predicates (causal; grouped-query heads; packed
+// sequences, Section 3.2 Example "Flash attention") becomes a tuple
 // (output block, input blocks...).  Kept tuples are compacted with a
 // workgroup prefix sum, so the table comes out grouped by output key with no
 // sort, and the CSR group offsets fall out of the same scan.
@@ -28,6 +29,17 @@ __device__ __forceinline__ int find_interval(const int32_t* s, int n, int32_t lo
     else z = m;
   }
   return (s[a] == lo && s[a + 1] == hi) ? a : -1;
+}
+
+// index of the sequence holding position x: the first end above it
+__device__ __forceinline__ int seq_of(const int32_t* ends, int n, int32_t x) {
+  int a = 0, z = n;  // invariant: every end before a is <= x, end z-1 (if z < n) is > x
+  while (a < z) {
+    const int m = (a + z) >> 1;
+    if (ends[m] <= x) a = m + 1;
+    else z = m;
+  }
+  return a;
 }
 
 __global__ __launch_bounds__(kThreads) void enumerate_kernel(const EnumDesc* __restrict__ dp,
@@ -78,6 +90,18 @@ __global__ __launch_bounds__(kThreads) void enumerate_kernel(const EnumDesc* __r
         const int32_t q_hi = splits[d.letter_split[d.cq] + coord[d.cq] + 1];
         const int32_t k_lo = splits[d.letter_split[d.ck] + coord[d.ck]];
         keep = k_lo <= q_hi - 1;
+      }
+      if (keep && d.gqa > 1) {  // the K/V head block holds the Q head block's heads / gqa
+        const int32_t h_lo = splits[d.letter_split[d.gh] + coord[d.gh]];
+        const int32_t h_hi = splits[d.letter_split[d.gh] + coord[d.gh] + 1];
+        const int32_t g_lo = splits[d.letter_split[d.gg] + coord[d.gg]];
+        const int32_t g_hi = splits[d.letter_split[d.gg] + coord[d.gg] + 1];
+        keep = (int64_t)g_lo * d.gqa <= h_lo && h_hi <= (int64_t)g_hi * d.gqa;
+      }
+      if (keep && d.n_seq > 0) {  // query and key blocks in one sequence (no block straddles one)
+        const int32_t q_lo = splits[d.letter_split[d.cq] + coord[d.cq]];
+        const int32_t k_lo = splits[d.letter_split[d.ck] + coord[d.ck]];
+        keep = seq_of(splits + d.seq_split, d.n_seq, q_lo) == seq_of(splits + d.seq_split, d.n_seq, k_lo);
       }
     }
     const uint64_t mask = __ballot(keep);

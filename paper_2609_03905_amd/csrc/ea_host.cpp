@@ -370,8 +370,23 @@ struct JoinSections {
   size_t blk[kMaxOps];
 };
 
-int build_join(const Spec& sp, const ea_relation* const* ops, const JoinInfo& ji, int causal, char cq,
-               char ck, Image* img, JoinSections* js, int64_t* n_groups, int64_t* tuple_cap) {
+struct OpInfo {
+  Kind kind = K_GENERIC;
+  std::string group;   // group letters
+  int causal = 0;      // the kernel masks keys after the query position
+  int join_causal = 0; // the join drops tuples whose key block is fully masked
+  char cq = 0, ck = 0; // causal letters
+  int b_kmajor = 0;
+  int q_dim = 0, k_dim = 0;
+  int gqa = 1;                   // query heads per key/value head (attention)
+  char gh = 0, gg = 0;           // query-head and key/value-head letters (gqa > 1)
+  int head_dim = -1;             // their dim in Q and in K/V
+  std::vector<int64_t> seq_ends; // packed sequences along cq/ck (attention), empty: one
+};
+
+int build_join(const Spec& sp, const ea_relation* const* ops, const JoinInfo& ji, const OpInfo& oi, Image* img,
+               JoinSections* js, int64_t* n_groups, int64_t* tuple_cap) {
+  const int causal = oi.join_causal;
   EnumDesc e;
   memset(&e, 0, sizeof(e));
   e.n_in = sp.n_in;
@@ -396,10 +411,21 @@ int build_join(const Spec& sp, const ea_relation* const* ops, const JoinInfo& ji
     }
   }
   e.causal = causal;
-  if (causal) {
-    e.cq = ji.index(cq);
-    e.ck = ji.index(ck);
-    if (e.cq < 0 || e.ck < 0) return fail(EA_ERR_SPEC, "causal letters not in the spec");
+  if (causal || !oi.seq_ends.empty()) {
+    e.cq = ji.index(oi.cq);
+    e.ck = ji.index(oi.ck);
+    if (e.cq < 0 || e.ck < 0) return fail(EA_ERR_SPEC, "query/key letters not in the spec");
+  }
+  if (oi.gqa > 1) {  // grouped-query heads
+    e.gqa = oi.gqa;
+    e.gh = ji.index(oi.gh);
+    e.gg = ji.index(oi.gg);
+    if (e.gh < 0 || e.gg < 0) return fail(EA_ERR_SPEC, "head letters not in the spec");
+  }
+  if (!oi.seq_ends.empty()) {  // packed sequences: their ends after the split lists
+    e.n_seq = (int32_t)oi.seq_ends.size();
+    e.seq_split = (int32_t)sp32.size();
+    for (int64_t v : oi.seq_ends) sp32.push_back((int32_t)v);
   }
   e.per_group = per_group;
   e.n_groups = ng;
@@ -430,15 +456,6 @@ int finish_join(Plan* p, const JoinSections& js, int n_ops, hipStream_t s) {
 // ---------------------------------------------------------------------------
 // operation classification and validation
 // ---------------------------------------------------------------------------
-struct OpInfo {
-  Kind kind = K_GENERIC;
-  std::string group;   // group letters
-  int causal = 0;      // the kernel masks keys after the query position
-  int join_causal = 0; // the join drops tuples whose key block is fully masked
-  char cq = 0, ck = 0; // causal letters
-  int b_kmajor = 0;
-  int q_dim = 0, k_dim = 0;
-};
 
 // largest block of a relation, in bytes
 int64_t max_block_bytes(const ea_relation* r) {
@@ -568,18 +585,35 @@ int classify(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation*
       if (agg_op != EA_AGG_LSE) return fail(EA_ERR_ARG, "ATTENTION aggregates with LSE (online softmax)");
       if (n_in != 3) return fail(EA_ERR_SPEC, "ATTENTION spec must be '<b>qd,<b>kd,<b>kd-><b>qd'");
       const int r = sp.rank[0];
+      const int gqa = prm && prm->gqa_group > 1 ? prm->gqa_group : 1;
       bool good = r >= 2 && sp.rank[1] == r && sp.rank[2] == r && sp.rank[out] == r;
       char q = 0, k = 0, d = 0;
+      int hd = -1;  // grouped-query: the batch dim where K/V name their own head letter
       if (good) {
         q = sp.let[0][r - 2];
         d = sp.let[0][r - 1];
         k = sp.let[1][r - 2];
         good = k != q && k != d && sp.let[1][r - 1] == d && sp.let[2][r - 2] == k && sp.let[2][r - 1] == d;
-        for (int i = 0; i < r - 2 && good; ++i)
-          good = sp.let[1][i] == sp.let[0][i] && sp.let[2][i] == sp.let[0][i];
+        for (int i = 0; i < r - 2 && good; ++i) {
+          good = sp.let[2][i] == sp.let[1][i];
+          if (sp.let[1][i] == sp.let[0][i]) continue;
+          // a K/V letter apart from Q's: only the one head letter of GQA
+          good = good && gqa > 1 && hd < 0 && find_dim(sp, 0, sp.let[1][i]) < 0;
+          hd = i;
+        }
         good = good && out_letters == std::string(sp.let[0], sp.let[0] + r);
       }
-      if (!good) return fail(EA_ERR_SPEC, "ATTENTION spec must be '<b>qd,<b>kd,<b>kd-><b>qd'");
+      if (!good)
+        return fail(EA_ERR_SPEC, gqa > 1 ? "grouped-query ATTENTION spec must be '<b>hqd,<b>gkd,<b>gkd-><b>hqd'"
+                                         : "ATTENTION spec must be '<b>qd,<b>kd,<b>kd-><b>qd'");
+      if (gqa > 1) {
+        if (hd < 0) return fail(EA_ERR_SPEC, "grouped-query ATTENTION needs a key/value head letter apart from Q's");
+        if (ops[0]->shape[hd] != (int64_t)gqa * ops[1]->shape[hd])
+          return fail(EA_ERR_SPEC, "grouped-query ATTENTION: %lld query heads are not %d x %lld key/value heads",
+                      (long long)ops[0]->shape[hd], gqa, (long long)ops[1]->shape[hd]);
+        if (ops[1]->nb[hd] != ops[1]->shape[hd])
+          return fail(EA_ERR_UNSUPPORTED, "ATTENTION needs one block per key/value head");
+      }
       for (int i = 0; i < 3; ++i)
         if (ops[i]->dtype != EA_BF16) return fail(EA_ERR_DTYPE, "ATTENTION takes bf16 Q, K, V");
       if (o->dtype == EA_F16) return fail(EA_ERR_DTYPE, "ATTENTION writes f32 or bf16");
@@ -598,6 +632,30 @@ int classify(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation*
       if (!prm || !(std::isfinite(prm->scale)) || !(prm->scale > 0.0f))
         return fail(EA_ERR_ARG, "ATTENTION needs params with a positive finite scale");
       if (prm->residual) return fail(EA_ERR_UNSUPPORTED, "ATTENTION takes no residual");
+      if (prm->n_seq < 0 || (prm->n_seq > 0 && !prm->seq_ends))
+        return fail(EA_ERR_ARG, "ATTENTION: n_seq %d with seq_ends %p", prm->n_seq, (const void*)prm->seq_ends);
+      if (prm->n_seq > 0) {
+        // packed sequences: strictly increasing ends, the last the extent,
+        // each a split point of the query and of the key partition
+        const int64_t S = ops[0]->shape[r - 2];
+        if (ops[1]->shape[r - 2] != S) return fail(EA_ERR_SPEC, "packed-sequence ATTENTION needs as many queries as keys");
+        if (prm->n_seq > (1 << 20)) return fail(EA_ERR_ARG, "ATTENTION: %d sequences", prm->n_seq);
+        int64_t prev = 0;
+        for (int i = 0; i < prm->n_seq; ++i) {
+          const int64_t e = prm->seq_ends[i];
+          if (e <= prev || e > S) return fail(EA_ERR_ARG, "ATTENTION: sequence end %d (%lld) out of order", i, (long long)e);
+          for (int op = 0; op < 2; ++op) {
+            const std::vector<int64_t>& ss = ops[op]->splits[r - 2];
+            if (!std::binary_search(ss.begin(), ss.end(), e))
+              return fail(EA_ERR_UNSUPPORTED, "ATTENTION: sequence end %lld is not a %s block bound", (long long)e,
+                          op ? "key" : "query");
+          }
+          prev = e;
+        }
+        if (prev != S) return fail(EA_ERR_ARG, "ATTENTION: the last sequence end %lld is not the extent %lld",
+                                   (long long)prev, (long long)S);
+        oi->seq_ends.assign(prm->seq_ends, prm->seq_ends + prm->n_seq);
+      }
       // A fully masked key block contributes nothing to O: the join drops it.
       oi->kind = K_ATTENTION;
       oi->group = out_letters;
@@ -607,6 +665,12 @@ int classify(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation*
       oi->ck = k;
       oi->q_dim = r - 2;
       oi->k_dim = r - 2;
+      if (gqa > 1) {
+        oi->gqa = gqa;
+        oi->gh = sp.let[0][hd];
+        oi->gg = sp.let[1][hd];
+        oi->head_dim = hd;
+      }
       return EA_OK;
     }
     default:
@@ -895,9 +959,11 @@ int build_attention(const ea_relation* const* ops, const OpInfo& oi, const JoinI
   std::vector<AttnUnit> units;
   int32_t slot = 0, counter = 0;
   int32_t c[kMaxRank];
-  // expected tuples of every (group, 128-row tile): the key blocks the causal
-  // rule keeps; used only to size the split -- the kernel reads its tuple
-  // range from the GPU-built group offsets
+  // tuples of every (group, 128-row tile): the key blocks the causal and
+  // sequence rules keep (the GPU join's predicates; grouped-query heads keep
+  // one key/value head per query head, so they do not change the count).
+  // It sizes the split, which holds at most kAttnMaxUnitTuples per unit; the
+  // kernel reads its tuple range from the GPU-built group offsets
   struct TileWork {
     int64_t g, q0;
     int n_t;
@@ -907,10 +973,12 @@ int build_attention(const ea_relation* const* ops, const OpInfo& oi, const JoinI
     block_coords(Q, g, c);
     const int64_t q_lo = Q->splits[r - 2][c[r - 2]];
     const int64_t q_hi = Q->splits[r - 2][c[r - 2] + 1];
+    const std::vector<int64_t>& ends = oi.seq_ends;
+    auto seq_of = [&](int64_t x) { return std::upper_bound(ends.begin(), ends.end(), x) - ends.begin(); };
     int n_t = 0;
     for (int kb = 0; kb < K->nb[r - 2]; ++kb) {
       const int64_t k_lo = K->splits[r - 2][kb];
-      if (!causal || k_lo <= q_hi - 1) ++n_t;
+      if ((!causal || k_lo <= q_hi - 1) && (ends.empty() || seq_of(k_lo) == seq_of(q_lo))) ++n_t;
     }
     for (int64_t q0 = 0; q0 < q_hi - q_lo; q0 += 128) tiles.push_back(TileWork{g, q0, n_t});
   }
@@ -983,7 +1051,9 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
   int dev = 0;
   EA_HIP_TRY(hipGetDevice(&dev));
   std::ostringstream k;
-  k << "J|" << dev << "|" << spec_str << "|" << join_op << "|" << agg_op << "|" << oi.causal << oi.join_causal;
+  k << "J|" << dev << "|" << spec_str << "|" << join_op << "|" << agg_op << "|" << oi.causal << oi.join_causal
+    << "|g" << oi.gqa << "|s";
+  for (int64_t e : oi.seq_ends) k << e << ",";
   for (int o = 0; o <= sp.n_in; ++o) key_rel(k, ops[o]);
   const ea_relation* res = prm ? prm->residual : nullptr;
   if (res && (oi.kind == K_GEMM || oi.kind == K_GENERIC)) k << "|res" << res->dtype;
@@ -1003,7 +1073,7 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
   p->kind = oi.kind;
   p->n_in = sp.n_in;
   p->b_kmajor = oi.b_kmajor;
-  e = build_join(sp, ops, ji, oi.join_causal, oi.cq, oi.ck, &img, &js, &p->n_groups, &p->tuple_cap);
+  e = build_join(sp, ops, ji, oi, &img, &js, &p->n_groups, &p->tuple_cap);
   if (e) return e;
   Extra ex;
   switch (oi.kind) {
@@ -1094,6 +1164,9 @@ int prepare(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, con
                   sp->rank[o]);
   if (prm && prm->store != EA_STORE_CACHED && prm->store != EA_STORE_STREAM)
     return fail(EA_ERR_ARG, "params.store must be EA_STORE_CACHED or EA_STORE_STREAM");
+  if (prm && prm->gqa_group < 0) return fail(EA_ERR_ARG, "params.gqa_group %d is negative", prm->gqa_group);
+  if (prm && join_op != EA_OP_ATTENTION && (prm->gqa_group > 1 || prm->n_seq != 0))
+    return fail(EA_ERR_ARG, "params.gqa_group and params.n_seq apply to EA_OP_ATTENTION only");
   e = classify(*sp, join_op, agg_op, ops, prm, oi);
   if (e) return e;
   // join validation runs here too, before any HIP call

@@ -41,7 +41,11 @@ struct EnumDesc {
   int32_t n_letters;
   int32_t n_group_letters;
   int32_t causal;
-  int32_t cq, ck;           // letter indices of the causal pair
+  int32_t cq, ck;           // letter indices of the query/key position pair (causal, sequences)
+  int32_t gqa;              // > 1: grouped-query heads, letter gh over letter gg
+  int32_t gh, gg;
+  int32_t n_seq;            // > 0: packed sequences, ends at splits[seq_split ..]
+  int32_t seq_split;
   int64_t per_group;        // candidates per group
   int64_t n_groups;
   int64_t n_cand;

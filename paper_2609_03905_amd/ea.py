@@ -37,7 +37,8 @@ class EAError(RuntimeError):
 
 class _Params(ctypes.Structure):
     _fields_ = [("eps", ctypes.c_float), ("scale", ctypes.c_float), ("causal", ctypes.c_int32),
-                ("store", ctypes.c_int32), ("residual", ctypes.c_void_p)]
+                ("store", ctypes.c_int32), ("residual", ctypes.c_void_p), ("gqa_group", ctypes.c_int32),
+                ("n_seq", ctypes.c_int32), ("seq_ends", ctypes.c_void_p)]
 
 
 _lib = None
@@ -177,15 +178,28 @@ class Relation:
         return list(lo), list(hi), int(off.value)
 
 
+def _params(eps=0.0, scale=0.0, causal=False, store=0, residual=None, gqa_group=0, seq_ends=None):
+    """ea_params plus the host array it points at (kept alive by the caller)."""
+    ends = None
+    if seq_ends is not None:
+        ends = (ctypes.c_int64 * max(1, len(seq_ends)))(*[int(e) for e in seq_ends])
+    prm = _Params(eps, scale, int(causal), int(store), residual.handle.value if residual is not None else None,
+                  int(gqa_group), 0 if seq_ends is None else len(seq_ends),
+                  ctypes.cast(ends, ctypes.c_void_p) if ends is not None else None)
+    return prm, ends
+
+
 def joinagg(spec: str, join_op: int, agg_op: int, inputs: Sequence[Relation], out: Relation, *,
             eps: float = 0.0, scale: float = 0.0, causal: bool = False, residual: Relation | None = None,
-            store: int = 0, stream=None) -> None:
+            store: int = 0, gqa_group: int = 0, seq_ends=None, stream=None) -> None:
     """Run one GPU's share of a join-agg: join the input relations' blocks,
     run the per-tuple kernel, aggregate by output key, store into ``out``.
     ``store``: STORE_CACHED (default) or STORE_STREAM (non-temporal output
-    stores, for an output nothing reads soon)."""
+    stores, for an output nothing reads soon).  Attention: ``gqa_group``
+    query heads per key-value head, ``seq_ends`` the ends of packed
+    sequences."""
     handles = _arr(ctypes.c_void_p, [r.handle.value for r in inputs])
-    prm = _Params(eps, scale, int(causal), int(store), residual.handle.value if residual is not None else None)
+    prm, _ends = _params(eps, scale, causal, store, residual, gqa_group, seq_ends)
     _check(lib().ea_joinagg(spec.encode(), join_op, agg_op, len(inputs), handles, out.handle, ctypes.byref(prm),
                             _stream(stream)))
 
@@ -197,10 +211,10 @@ def repartition(src: Relation, dst: Relation, stream=None, *, store: int = 0) ->
 
 
 def join_tuples(spec: str, join_op: int, inputs: Sequence[Relation], out: Relation, *, causal: bool = False,
-                scale: float = 1.0, eps: float = 1e-6, stream=None):
+                scale: float = 1.0, eps: float = 1e-6, gqa_group: int = 0, seq_ends=None, stream=None):
     """The GPU-built tuple table and CSR group offsets of a join (synchronous)."""
     handles = _arr(ctypes.c_void_p, [r.handle.value for r in inputs])
-    prm = _Params(eps, scale, int(causal), 0, None)
+    prm, _ends = _params(eps, scale, causal, 0, None, gqa_group, seq_ends)
     n_t, n_g = ctypes.c_int64(), ctypes.c_int64()
     dev = out.data.device if out.data is not None else torch.device("cuda")
     # first call sizes the tables (it fails with EA_ERR_CAPACITY but reports the counts)

@@ -192,3 +192,35 @@ def test_repartition_validation_errors():
     assert _code(lambda: ea.repartition(nodata, d)) == -1
     for bad in (-1, 2):
         assert _code(lambda: ea.repartition(a, d, store=bad)) == -1
+
+
+def test_grouped_query_and_packed_sequence_validation_errors():
+    J = lambda *a, **k: (lambda: ea.joinagg(*a, **k))
+    pq = [[0, 1], synth.splits(8, 1), synth.splits(512, 128), [0, 128]]
+    pk = [[0, 1], synth.splits(2, 1), synth.splits(512, 128), [0, 128]]
+    q = _fake([1, 8, 512, 128], "bf16", pq)
+    kv = _fake([1, 2, 512, 128], "bf16", pk)
+    GQA = "bhqd,bgkd,bgkd->bhqd"
+    # negative group size; the parameters on another operator
+    assert _code(J(GQA, ea.OP_ATTENTION, ea.AGG_LSE, [q, kv, kv], q, scale=0.1, gqa_group=-2)) == -1
+    x = _fake([64, 256], "bf16", [[0, 64], synth.splits(256, 64)])
+    w = _fake([256], "bf16", [synth.splits(256, 64)])
+    assert _code(J("tc,c->tc", ea.OP_RMSNORM, ea.AGG_SUM, [x, w], x, eps=1e-6, gqa_group=4)) == -1
+    assert _code(J("tc,c->tc", ea.OP_RMSNORM, ea.AGG_SUM, [x, w], x, eps=1e-6, seq_ends=[64])) == -1
+    # 8 query heads are not 3 x 2; a separate K/V head letter without a group
+    assert _code(J(GQA, ea.OP_ATTENTION, ea.AGG_LSE, [q, kv, kv], q, scale=0.1, gqa_group=3)) == -5
+    assert _code(J(GQA, ea.OP_ATTENTION, ea.AGG_LSE, [q, kv, kv], q, scale=0.1)) == -5
+    # K and V name different head letters
+    assert _code(J("bhqd,bgkd,bfkd->bhqd", ea.OP_ATTENTION, ea.AGG_LSE, [q, kv, kv], q, scale=0.1,
+                   gqa_group=4)) == -5
+    # key/value heads in blocks of two
+    kv2 = _fake([1, 2, 512, 128], "bf16", [[0, 1], [0, 2], synth.splits(512, 128), [0, 128]])
+    assert _code(J(GQA, ea.OP_ATTENTION, ea.AGG_LSE, [q, kv2, kv2], q, scale=0.1, gqa_group=4)) == -7
+    # packed sequences: out of order, past the extent, last not the extent,
+    # an end inside a block
+    p1 = [[0, 1], [0, 1], synth.splits(512, 128), [0, 128]]
+    a = _fake([1, 1, 512, 128], "bf16", p1)
+    MHA = "bhqd,bhkd,bhkd->bhqd"
+    for ends, code in (([256, 128, 512], -1), ([256, 640], -1), ([128, 256], -1), ([192, 512], -7)):
+        assert _code(J(MHA, ea.OP_ATTENTION, ea.AGG_LSE, [a, a, a], a, scale=0.1, causal=True,
+                       seq_ends=ends)) == code, ends

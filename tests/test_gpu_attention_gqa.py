@@ -1,0 +1,124 @@
+"""GPU parity of grouped-query and packed-sequence attention (Section 3.2,
+Example "Flash attention") against the fp64 oracle: the join's tuple table
+bit for bit, the outputs within the attention tolerance."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from helpers import assert_close, empty, expected, upload, values
+from paper_2609_03905_amd import ea
+
+pytestmark = pytest.mark.gpu
+
+GQA = "bhqd,bgkd,bgkd->bhqd"
+MHA = "bhqd,bhkd,bhkd->bhqd"
+
+
+def _example():
+    with open(os.path.join(os.path.dirname(__file__), "golden", "flash_attention_example.json")) as f:
+        return json.load(f)
+
+
+def _inputs(B, Hq, Hkv, S, seed):
+    q = synth.normal((B, Hq, S, 128), seed, dtype="bf16")
+    k = synth.normal((B, Hkv, S, 128), seed + 1, dtype="bf16")
+    v = synth.normal((B, Hkv, S, 128), seed + 2, dtype="bf16")
+    return q, k, v
+
+
+def _run(q, k, v, pq, pk, causal, seq_ends=None, out_dtype="f32", scale=None):
+    G = q.shape[1] // k.shape[1]
+    Q, K, V = upload(q, "bf16", pq), upload(k, "bf16", pk), upload(v, "bf16", pk)
+    O = empty(q.shape, out_dtype, pq)
+    ea.joinagg(GQA if G > 1 else MHA, ea.OP_ATTENTION, ea.AGG_LSE, [Q, K, V], O,
+               scale=scale or 1.0 / np.sqrt(128), causal=causal, gqa_group=G if G > 1 else 0, seq_ends=seq_ends)
+    return O
+
+
+def _ref(q, k, v, causal, seq_ends=None, scale=None):
+    return oracle.attention_ex(*(synth.to_f64(a, "bf16") for a in (q, k, v)), causal,
+                               scale or 1.0 / np.sqrt(128), seq_ends=seq_ends)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_join_grouped_heads_and_packed_sequences_bitexact(causal):
+    # the paper's example: 32 query heads over 8 key/value heads, 4096
+    # positions holding sequences ending at 1024, 2560 and 4096, 128-blocks
+    ex = _example()
+    Hq, Hkv, S, ends = ex["heads_q"], ex["heads_kv"], ex["sequence"], ex["ends"]
+    pq = [[0, 1], synth.splits(Hq, 1), synth.splits(S, 128), [0, 128]]
+    pk = [[0, 1], synth.splits(Hkv, 1), synth.splits(S, 128), [0, 128]]
+    Q = ea.Relation((1, Hq, S, 128), "bf16", pq)
+    K = ea.Relation((1, Hkv, S, 128), "bf16", pk)
+    tuples, goff = ea.join_tuples(GQA, ea.OP_ATTENTION, [Q, K, K], Q, causal=causal, scale=0.1,
+                                  gqa_group=Hq // Hkv, seq_ends=ends)
+    ref_t, ref_g = oracle.join(GQA, [pq, pk, pk, pq], group="bhqd", causal=("q", "k") if causal else None,
+                               positions=("q", "k"), seq_ends=ends, gqa=(Hq // Hkv, "h", "g"))
+    np.testing.assert_array_equal(tuples.cpu().numpy(), ref_t)
+    np.testing.assert_array_equal(goff.cpu().numpy(), ref_g)
+    assert len(ref_t) == Hq * (192 if causal else 352)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_attention_grouped_query_heads(causal):
+    B, Hq, Hkv, S = 2, 8, 2, 1024
+    q, k, v = _inputs(B, Hq, Hkv, S, 460)
+    pq = [synth.splits(B, 1), synth.splits(Hq, 1), synth.splits(S, 128), [0, 128]]
+    pk = [synth.splits(B, 1), synth.splits(Hkv, 1), synth.splits(S, 256), [0, 128]]
+    O = _run(q, k, v, pq, pk, causal)
+    assert_close(values(O), _ref(q, k, v, causal), rel_fro=1e-3, what=f"GQA 8 over 2, causal={causal}")
+
+
+def test_attention_packed_sequences_of_the_papers_example():
+    # three sequences ending at 1024, 2560, 4096; 4 query heads over one
+    # key/value head; causal; bf16 output; split tiles (12-block sequences)
+    # merged the same way every run
+    ex = _example()
+    S, ends = ex["sequence"], ex["ends"]
+    q, k, v = _inputs(1, 4, 1, S, 470)
+    pq = [[0, 1], synth.splits(4, 1), synth.splits(S, 128), [0, 128]]
+    pk = [[0, 1], [0, 1], synth.splits(S, 128), [0, 128]]
+    O = _run(q, k, v, pq, pk, True, seq_ends=ends, out_dtype="bf16")
+    ref = _ref(q, k, v, True, seq_ends=ends)
+    assert_close(values(O), expected(ref, "bf16"), what="packed sequences, paper example")
+    for _ in range(2):
+        O2 = _run(q, k, v, pq, pk, True, seq_ends=ends, out_dtype="bf16")
+        torch.cuda.synchronize()
+        assert torch.equal(O.bytes(), O2.bytes())
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_attention_packed_sequences_ragged_partitions(causal):
+    # sequences of 384, 256, 128, 1280 and 128 positions; the query partition
+    # cuts at the ends and elsewhere in 256s, the key partition in 128s; the
+    # first query of every sequence sees only its own key when causal
+    ends = [384, 640, 768, 2048, 2176]
+    S = ends[-1]
+    q, k, v = _inputs(1, 4, 2, S, 480)
+    qcuts = sorted(set(ends) | set(range(0, S, 256)))
+    pq = [[0, 1], synth.splits(4, 1), qcuts, [0, 128]]
+    pk = [[0, 1], synth.splits(2, 1), synth.splits(S, 128), [0, 128]]
+    O = _run(q, k, v, pq, pk, causal, seq_ends=ends)
+    got = values(O)
+    ref = _ref(q, k, v, causal, seq_ends=ends)
+    assert_close(got, ref, rel_fro=1e-3, what=f"packed ragged, causal={causal}")
+    if causal:
+        fv = synth.to_f64(v, "bf16")
+        for start in [0] + ends[:-1]:  # exact but for V values in fp16's subnormal range
+            np.testing.assert_allclose(got[0, :, start], np.repeat(fv[0, :, start], 2, axis=0), rtol=1e-6, atol=1e-7)
+
+
+def test_attention_one_sequence_list_equals_plain():
+    # seq_ends = [S] is one sequence: the same bytes as no list at all
+    S = 1024
+    q, k, v = _inputs(1, 2, 2, S, 490)
+    p = [[0, 1], synth.splits(2, 1), synth.splits(S, 128), [0, 128]]
+    a = _run(q, k, v, p, p, True)
+    b = _run(q, k, v, p, p, True, seq_ends=[S])
+    torch.cuda.synchronize()
+    assert torch.equal(a.bytes(), b.bytes())
