@@ -191,6 +191,34 @@ def attention_workload():
                         "buffer_sets": len(rot.sets)}, cpu=None)
 
 
+def packed_gqa_workload():
+    import synth
+    from paper_2609_03905_amd import ea
+
+    w = synth.packed_gqa_attention()
+    Q0 = ea.from_dense(_dev(w["q"]), "bf16", w["pq"])
+    K0, V0 = (ea.from_dense(_dev(w[n]), "bf16", w["pk"]) for n in "kv")
+    hq, s = w["q"].shape[1], w["q"].shape[2]
+
+    def make_set(i):
+        qkv = [Q0, K0, V0] if i == 0 else [_copy(r, ea) for r in (Q0, K0, V0)]
+        return qkv + [ea.Relation((1, hq, s, 128), "bf16", w["pq"])]
+
+    rot = _Rotation(_buffer_sets(make_set, (2 * hq + 2) * s * 128 * 2))
+
+    def fn():
+        Q, K, V, O = rot.next()
+        ea.joinagg("bhqd,bgkd,bgkd->bhqd", ea.OP_ATTENTION, ea.AGG_LSE, [Q, K, V], O, scale=w["scale"],
+                   causal=True, gqa_group=w["gqa"], seq_ends=w["ends"])
+
+    L = w["ends"][0]
+    flops = 4.0 * 128 * hq * len(w["ends"]) * L * (L + 1) / 2
+    return dict(step=fn, flops=flops, comps={"attention": dict(fn=fn, flops=flops)}, dominant="attention",
+                config={"workload": "packed_gqa_attention_share", "sequences": len(w["ends"]), "seq_len": L,
+                        "heads_q": hq, "heads_kv": w["k"].shape[1], "d_head": 128, "q_block": 128, "k_block": 128,
+                        "causal": True, "dtype": "bf16", "buffer_sets": len(rot.sets)}, cpu=None)
+
+
 def reductions_workload():
     import synth
     from paper_2609_03905_amd import ea
@@ -310,7 +338,8 @@ def cpu_baseline_qkv(target_s: float = 12.0):
 
 
 WORKLOADS = {"block": block_workload, "qkv": qkv_workload, "attention": attention_workload,
-             "reductions": reductions_workload, "repartition": repartition_workload}
+             "packed_gqa": packed_gqa_workload, "reductions": reductions_workload,
+             "repartition": repartition_workload}
 
 
 def main():

@@ -138,6 +138,21 @@ def attention(b=2, h=4, s=2048, d=128, qblock=128, kblock=128):
     return dict(q=q, k=k, v=v, pq=pq, pk=pk, scale=1.0 / np.sqrt(d))
 
 
+def packed_gqa_attention(n_seq=8, seq_len=1024, heads_q=4, heads_kv=1, d=128, block=128):
+    """Causal attention over packed sequences with grouped-query heads: one
+    GPU's head share (4 query heads over 1 key/value head = 32 over 8 split
+    eight ways) of a 4096-wide, 32-head LLaMA-style model on a batch of eight
+    1K-token sequences packed end to end, bf16."""
+    s = n_seq * seq_len
+    q = normal((1, heads_q, s, d), 411, 1.0, "bf16")
+    k = normal((1, heads_kv, s, d), 412, 1.0, "bf16")
+    v = normal((1, heads_kv, s, d), 413, 1.0, "bf16")
+    pq = [[0, 1], splits(heads_q, 1), splits(s, block), whole(d)]
+    pk = [[0, 1], splits(heads_kv, 1), splits(s, block), whole(d)]
+    ends = [seq_len * (i + 1) for i in range(n_seq)]
+    return dict(q=q, k=k, v=v, pq=pq, pk=pk, ends=ends, scale=1.0 / np.sqrt(d), gqa=heads_q // heads_kv)
+
+
 def llama_block(t=2048, hidden=8192, heads=8, d_head=128, ffn=2752, block=512):
     """One GPU's share of a LLaMA-65B-shape block: hidden 8192, 8 of 64 heads,
     SwiGLU FFN 2752 = 22016/8, batch 1 x seq 2048."""

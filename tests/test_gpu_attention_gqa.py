@@ -122,3 +122,13 @@ def test_attention_one_sequence_list_equals_plain():
     b = _run(q, k, v, p, p, True, seq_ends=[S])
     torch.cuda.synchronize()
     assert torch.equal(a.bytes(), b.bytes())
+
+
+def test_attention_packed_gqa_workload_full_size():
+    # the benchmarked share: 4 query heads over 1 key/value head, eight 1K
+    # sequences packed into 8192 positions, causal, bf16 out
+    w = synth.packed_gqa_attention()
+    O = _run(w["q"], w["k"], w["v"], w["pq"], w["pk"], True, seq_ends=w["ends"], out_dtype="bf16",
+             scale=w["scale"])
+    ref = _ref(w["q"], w["k"], w["v"], True, seq_ends=w["ends"], scale=w["scale"])
+    assert_close(values(O), expected(ref, "bf16"), what="packed GQA workload")
