@@ -219,6 +219,34 @@ def packed_gqa_workload():
                         "causal": True, "dtype": "bf16", "buffer_sets": len(rot.sets)}, cpu=None)
 
 
+def chains_workload():
+    import synth
+    from paper_2609_03905_amd import chain
+
+    chains, comps, total = {}, {}, 0.0
+    for name in sorted(synth.CHAINS):
+        dims, tree = synth.CHAINS[name]
+        ch = chain.MatrixChain(dims, tree)
+        for i in range(len(dims) - 1):
+            std = 1.0 if i == 0 else 1.0 / dims[i] ** 0.5
+            ch.load(i, synth.chain_matrix_device((dims[i], dims[i + 1]), 900 + 20 * "ABCDE".index(name) + i, std))
+        chains[name] = ch
+        fl = chain.flops(dims, tree)
+        comps[f"chain_{name}"] = dict(fn=ch.run, flops=fl)
+        total += fl
+
+    def step():
+        for ch in chains.values():
+            ch.run()
+
+    return dict(step=step, flops=total, comps=comps, dominant="chain_E",
+                data="synthetic (seeded on the device: first matrix N(0,1), matrix i N(0,1/d_i))",
+                config={"workload": "matrix_chains_A_to_E", "chains": "A,B,C,D,E (Section 6 dims, fixed trees)",
+                        "block": 512, "dtype": "bf16", "products": sum(len(chain.products(t)) for _, t in
+                                                                     synth.CHAINS.values())},
+                cpu=None)
+
+
 def reductions_workload():
     import synth
     from paper_2609_03905_amd import ea
@@ -338,7 +366,7 @@ def cpu_baseline_qkv(target_s: float = 12.0):
 
 
 WORKLOADS = {"block": block_workload, "qkv": qkv_workload, "attention": attention_workload,
-             "packed_gqa": packed_gqa_workload, "reductions": reductions_workload,
+             "packed_gqa": packed_gqa_workload, "chains": chains_workload, "reductions": reductions_workload,
              "repartition": repartition_workload}
 
 
@@ -402,7 +430,7 @@ def main():
     out = {
         "metric": METRIC, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic (seeded N(0,1) activations, N(0,0.02) weights, random init)",
+        "dtype": "bf16", "data": wl.get("data", "synthetic (seeded N(0,1) activations, N(0,0.02) weights, random init)"),
         "config": wl["config"], "roofline": roof, "components": comps, "wall_s": round(wall, 4),
     }
     if not args.no_cpu_baseline and wl.get("cpu"):

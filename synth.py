@@ -153,6 +153,53 @@ def packed_gqa_attention(n_seq=8, seq_len=1024, heads_q=4, heads_kv=1, d=128, bl
     return dict(q=q, k=k, v=v, pq=pq, pk=pk, ends=ends, scale=1.0 / np.sqrt(d), gqa=heads_q // heads_kv)
 
 
+def _right_nested(first: int, last: int):
+    """(first, (first + 1, ( ... (last - 1, last))))."""
+    return last if first == last else (first, _right_nested(first + 1, last))
+
+
+# The matrix chains of Section 6: dims (matrix i is [dims[i], dims[i+1]]) and
+# parenthesization (nested pairs of 0-based matrix indices); each multiply
+# averages about 8192^3 scalar multiplies
+CHAINS = {
+    # nine matrices, dims alternating 16,384 and 6,144 between ends of 10,240:
+    # (M1 M2) (((M3 M4) ((M5 M6) (M7 M8))) M9)
+    "A": ([10240, 16384, 6144, 16384, 6144, 16384, 6144, 16384, 6144, 10240],
+          ((0, 1), (((2, 3), ((4, 5), (6, 7))), 8))),
+    # five matrices, dims alternating 20,480 and 5,120 between ends of 9,216:
+    # (M1 M2) ((M3 M4) M5)
+    "B": ([9216, 20480, 5120, 20480, 5120, 9216], ((0, 1), ((2, 3), 4))),
+    # three matrices, right-associated: M1 (M2 M3)
+    "C": ([10240, 12288, 32768, 2048], (0, (1, 2))),
+    # nine matrices, ends 24,576, necks 1,536, interior 20,480:
+    # M1 ((M2 (M3 (M4 (M5 (M6 (M7 M8)))))) M9)
+    "D": ([24576, 1536] + [20480] * 6 + [1536, 24576], (0, (_right_nested(1, 7), 8))),
+    # thirteen matrices, ends 49,152, necks 1,024, interior 20,480:
+    # M1 ((M2 (M3 ( ... (M11 M12)))) M13)
+    "E": ([49152, 1024] + [20480] * 10 + [1024, 49152], (0, (_right_nested(1, 11), 12))),
+}
+
+
+def chain_matrices(dims, seed: int, div: int = 1):
+    """Matrices of a matrix chain (dims divided by `div`), bf16, host: matrix
+    i is [d_i, d_(i+1)] with N(0, 1/d_i) entries (N(0, 1) for the first), so
+    every product of the chain stays of order one."""
+    d = [x // div for x in dims]
+    return [normal((d[i], d[i + 1]), seed + i, 1.0 if i == 0 else 1.0 / np.sqrt(d[i]), "bf16")
+            for i in range(len(d) - 1)], d
+
+
+def chain_matrix_device(shape, seed: int, std: float, device="cuda"):
+    """One full-size chain matrix drawn on the device (torch's seeded
+    generator, N(0, std^2), fp32 then RNE to bf16), for runs with no oracle
+    check: full-size chains hold up to 7.5 GB of inputs."""
+    import torch
+
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    return (torch.randn(shape, generator=g, device=device, dtype=torch.float32) * std).to(torch.bfloat16)
+
+
 def llama_block(t=2048, hidden=8192, heads=8, d_head=128, ffn=2752, block=512):
     """One GPU's share of a LLaMA-65B-shape block: hidden 8192, 8 of 64 heads,
     SwiGLU FFN 2752 = 22016/8, batch 1 x seq 2048."""
