@@ -327,7 +327,8 @@ def add(a, b) -> np.ndarray:
 # --------------------------------------------------------------------------
 # composite: one GPU's share of a pre-norm LLaMA-shaped block
 # --------------------------------------------------------------------------
-def llama_block(x, n1, wqkv, wo, wg, wu, wd, n2, heads: int, d_head: int, eps: float):
+def llama_block(x, n1, wqkv, wo, wg, wu, wd, n2, heads: int, d_head: int, eps: float, heads_kv: int | None = None,
+                seq_ends=None):
     """The block chain with a bf16 round-to-nearest-even at every relation
     boundary (each arrow of the chain below stores a bf16 relation):
 
@@ -336,24 +337,30 @@ def llama_block(x, n1, wqkv, wo, wg, wu, wd, n2, heads: int, d_head: int, eps: f
       -> a = SiLU(h2 W_g) * (h2 W_u) -> y = x2 + a W_d
 
     qkv's columns are [Q heads | K heads | V heads], head h of each taking
-    columns [h*d_head, (h+1)*d_head).  RoPE is not part of the chain.  Causal
+    columns [h*d_head, (h+1)*d_head) of its part; with heads_kv < heads the K
+    and V parts have heads_kv heads (grouped-query attention), and seq_ends
+    packs independent sequences along the tokens.  RoPE is not part of the chain.  Causal
     attention makes row t of every output depend only on rows <= t of x, so a
     prefix of x yields the same prefix of y.  All inputs are fp64 values.
     Returns every boundary relation as a dict of dense fp64 arrays.
     """
     r = rne_bf16
     T = x.shape[0]
-    hd = heads * d_head
+    hkv = heads if heads_kv is None else heads_kv
+    hd, kvd = heads * d_head, hkv * d_head
     h1 = r(rmsnorm(x, n1, eps))
     qkv = r(matmul(h1, wqkv))
 
-    def heads_view(cols):
-        return np.ascontiguousarray(cols.reshape(T, heads, d_head).transpose(1, 0, 2))[None]
+    def heads_view(cols, n):
+        return np.ascontiguousarray(cols.reshape(T, n, d_head).transpose(1, 0, 2))[None]
 
-    q = heads_view(qkv[:, 0:hd])
-    k = heads_view(qkv[:, hd:2 * hd])
-    v = heads_view(qkv[:, 2 * hd:3 * hd])
-    o = r(attention(q, k, v, True, 1.0 / np.sqrt(d_head)))
+    q = heads_view(qkv[:, 0:hd], heads)
+    k = heads_view(qkv[:, hd:hd + kvd], hkv)
+    v = heads_view(qkv[:, hd + kvd:hd + 2 * kvd], hkv)
+    if hkv == heads and seq_ends is None:
+        o = r(attention(q, k, v, True, 1.0 / np.sqrt(d_head)))
+    else:
+        o = r(attention_ex(q, k, v, True, 1.0 / np.sqrt(d_head), seq_ends=seq_ends))
     attn = np.ascontiguousarray(o[0].transpose(1, 0, 2).reshape(T, hd))
     x2 = r(add(x, matmul(attn, wo)))
     h2 = r(rmsnorm(x2, n2, eps))

@@ -444,3 +444,30 @@ def test_join_grouped_heads_of_the_papers_example():
     tuples, _ = oracle.join("bhqd,bgkd,bgkd->bhqd", [pq, [[0, 1], [0, 1, 2], [0, 512], [0, 128]]] * 1 +
                             [[[0, 1], [0, 1, 2], [0, 512], [0, 128]], pq], group="bhqd", gqa=(4, "h", "g"))
     assert sorted(t[1] for t in tuples.tolist()) == [0, 2]
+
+
+def test_llama_block_grouped_heads_and_packed_sequences():
+    # grouped-query: the block with 4 query heads over 2 key/value heads equals
+    # the (torch-pinned) plain block whose W_qkv repeats each K and V head for
+    # its 2 query heads; packed: a later sequence's rows equal the block run on
+    # that sequence alone (every step but attention is row by row)
+    w = synth.llama_block(t=48, hidden=64, heads=4, d_head=16, ffn=40)
+    f = {k: synth.to_f64(w[k], "bf16") for k in ("x", "wqkv", "wo", "wg", "wu", "wd", "n1", "n2")}
+    hd, kvd = 4 * 16, 2 * 16
+    wqkv = f["wqkv"][:, :hd + 2 * kvd]
+    rep = lambda cols: np.repeat(cols.reshape(64, 2, 16), 2, axis=1).reshape(64, hd)
+    wqkv_mha = np.concatenate([wqkv[:, :hd], rep(wqkv[:, hd:hd + kvd]), rep(wqkv[:, hd + kvd:])], axis=1)
+    rest = (f["wo"], f["wg"], f["wu"], f["wd"], f["n2"])
+    gqa = oracle.llama_block(f["x"], f["n1"], wqkv, *rest, heads=4, d_head=16, eps=1e-6, heads_kv=2)
+    mha = oracle.llama_block(f["x"], f["n1"], wqkv_mha, *rest, heads=4, d_head=16, eps=1e-6)
+    diff = np.abs(gqa["y"] - mha["y"])
+    assert np.mean(diff > 0) < 0.01
+    assert np.linalg.norm(diff) / np.linalg.norm(mha["y"]) < 1e-3
+    packed = oracle.llama_block(f["x"], f["n1"], wqkv, *rest, heads=4, d_head=16, eps=1e-6, heads_kv=2,
+                                seq_ends=[20, 48])
+    alone = oracle.llama_block(f["x"][20:], f["n1"], wqkv, *rest, heads=4, d_head=16, eps=1e-6, heads_kv=2,
+                               seq_ends=[28])
+    np.testing.assert_array_equal(packed["y"][20:], alone["y"])
+    first = oracle.llama_block(f["x"][:20], f["n1"], wqkv, *rest, heads=4, d_head=16, eps=1e-6, heads_kv=2,
+                               seq_ends=[20])
+    np.testing.assert_array_equal(packed["y"][:20], first["y"])
