@@ -219,6 +219,25 @@ def packed_gqa_workload():
                         "causal": True, "dtype": "bf16", "buffer_sets": len(rot.sets)}, cpu=None)
 
 
+def w1_block_workload():
+    import synth
+    from paper_2609_03905_amd.block import LlamaBlockShare
+
+    w = synth.w1_block()
+    blk = LlamaBlockShare(w["t"], w["hidden"], w["heads"], w["d_head"], w["ffn"], block=w["block"], eps=w["eps"],
+                          heads_kv=w["heads_kv"], seq_ends=w["seq_ends"])
+    blk.load({k: _dev(w[k]) for k in ("x", "n1", "n2", "wqkv", "wo", "wg", "wu", "wd")})
+    work = blk.work()
+    stages = blk.stages()
+    comps = {name: dict(fn=fn, **work[name]) for name, fn in stages}
+    flops = sum(c.get("flops", 0) for c in comps.values())
+    return dict(step=blk.forward, flops=flops, comps=comps, dominant="swiglu_gemm",
+                config={"workload": "w1_block_share", "hidden": 4096, "heads_q": "4 of 32", "heads_kv": "1 of 8",
+                        "d_head": 128, "ffn": "1792 of 14336", "tokens": 8192, "sequences": "8 x 1024 packed",
+                        "block": 512, "dtype": "bf16", "chain": [n for n, _ in stages]},
+                cpu=None)
+
+
 def chains_workload():
     import synth
     from paper_2609_03905_amd import chain
@@ -366,7 +385,8 @@ def cpu_baseline_qkv(target_s: float = 12.0):
 
 
 WORKLOADS = {"block": block_workload, "qkv": qkv_workload, "attention": attention_workload,
-             "packed_gqa": packed_gqa_workload, "chains": chains_workload, "reductions": reductions_workload,
+             "packed_gqa": packed_gqa_workload, "w1_block": w1_block_workload, "chains": chains_workload,
+             "reductions": reductions_workload,
              "repartition": repartition_workload}
 
 

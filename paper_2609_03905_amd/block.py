@@ -12,7 +12,9 @@ chain of join-aggs and repartitions through libea.
     y   = x2 + a W_d                  'tj,jk->tk' + residual epilogue
 
 Every arrow stores a bf16 relation.  The columns of qkv are [Q heads | K
-heads | V heads], 128 each.  After the first repartition the qkv relation has
+heads | V heads], 128 each; with grouped-query attention there are fewer K
+and V heads than Q heads (query head h reads key/value head h / group), and
+packed sequences restrict attention to each query's own sequence.  After the first repartition the qkv relation has
 one row block and 128-wide column blocks, so head h of Q, K or V is one
 contiguous [T, 128] block; Q, K and V are then viewed, without a copy, as
 [1, heads, T, 128] relations with 128-row blocks (the same bytes).  The
@@ -33,20 +35,24 @@ def _splits(n: int, b: int):
 
 class LlamaBlockShare:
     def __init__(self, t: int, hidden: int, heads: int, d_head: int, ffn: int, block: int = 512,
-                 eps: float = 1e-6, device="cuda"):
+                 eps: float = 1e-6, device="cuda", heads_kv: int | None = None, seq_ends=None):
         assert d_head == 128, "the attention join-agg takes head dim 128"
+        heads_kv = heads if heads_kv is None else heads_kv
+        assert heads % heads_kv == 0, "query heads must be a multiple of key/value heads"
         self.t, self.hidden, self.heads, self.d_head, self.ffn = t, hidden, heads, d_head, ffn
+        self.heads_kv, self.seq_ends = heads_kv, None if seq_ends is None else [int(e) for e in seq_ends]
         self.eps = eps
         self.scale = 1.0 / d_head ** 0.5
         hd = heads * d_head
         self.hd = hd
+        wqkv = (heads + 2 * heads_kv) * d_head  # [Q heads | K heads | V heads]
         pt, ph = _splits(t, block), _splits(hidden, block)
-        pf, phd, pqkv = _splits(ffn, block), _splits(hd, block), _splits(3 * hd, block)
+        pf, phd, pqkv = _splits(ffn, block), _splits(hd, block), _splits(wqkv, block)
         R = lambda shape, part: ea.Relation(shape, "bf16", part, device=device)
         # parameters (filled by load())
         self.n1 = R((hidden,), [ph])
         self.n2 = R((hidden,), [ph])
-        self.wqkv = R((hidden, 3 * hd), [ph, pqkv])
+        self.wqkv = R((hidden, wqkv), [ph, pqkv])
         self.wo = R((hd, hidden), [phd, ph])
         self.wg = R((hidden, ffn), [ph, pf])
         self.wu = R((hidden, ffn), [ph, pf])
@@ -54,13 +60,15 @@ class LlamaBlockShare:
         # activations
         self.x = R((t, hidden), [pt, ph])
         self.h1 = R((t, hidden), [pt, ph])
-        self.qkv = R((t, 3 * hd), [pt, pqkv])
-        self.qkv_heads = R((t, 3 * hd), [[0, t], _splits(3 * hd, d_head)])
+        self.qkv = R((t, wqkv), [pt, pqkv])
+        self.qkv_heads = R((t, wqkv), [[0, t], _splits(wqkv, d_head)])
         head_part = [[0, 1], _splits(heads, 1), _splits(t, 128), [0, d_head]]
+        kv_part = [[0, 1], _splits(heads_kv, 1), _splits(t, 128), [0, d_head]]
         head_bytes = heads * t * d_head * 2
+        kv_bytes = heads_kv * t * d_head * 2
         self.q = self.qkv_heads.view(0, (1, heads, t, d_head), "bf16", head_part)
-        self.k = self.qkv_heads.view(head_bytes, (1, heads, t, d_head), "bf16", head_part)
-        self.v = self.qkv_heads.view(2 * head_bytes, (1, heads, t, d_head), "bf16", head_part)
+        self.k = self.qkv_heads.view(head_bytes, (1, heads_kv, t, d_head), "bf16", kv_part)
+        self.v = self.qkv_heads.view(head_bytes + kv_bytes, (1, heads_kv, t, d_head), "bf16", kv_part)
         self.o = R((1, heads, t, d_head), head_part)
         self.o_cols = self.o.view(0, (t, hd), "bf16", [[0, t], _splits(hd, d_head)])
         self.attn = R((t, hd), [pt, phd])
@@ -82,12 +90,14 @@ class LlamaBlockShare:
     # each stage is one library call; the list is what a step runs
     def stages(self):
         J, S = ea.joinagg, ea.AGG_SUM
+        group = self.heads // self.heads_kv if self.heads_kv < self.heads else 0
+        attn_spec = "bhqd,bgkd,bgkd->bhqd" if group else "bhqd,bhkd,bhkd->bhqd"
         return [
             ("rmsnorm1", lambda: J("tc,c->tc", ea.OP_RMSNORM, S, [self.x, self.n1], self.h1, eps=self.eps)),
             ("qkv_gemm", lambda: J("tj,jk->tk", ea.JOIN_MUL, S, [self.h1, self.wqkv], self.qkv)),
             ("repart_heads", lambda: ea.repartition(self.qkv, self.qkv_heads)),
-            ("attention", lambda: J("bhqd,bhkd,bhkd->bhqd", ea.OP_ATTENTION, ea.AGG_LSE, [self.q, self.k, self.v],
-                                    self.o, scale=self.scale, causal=True)),
+            ("attention", lambda: J(attn_spec, ea.OP_ATTENTION, ea.AGG_LSE, [self.q, self.k, self.v], self.o,
+                                    scale=self.scale, causal=True, gqa_group=group, seq_ends=self.seq_ends)),
             ("repart_cols", lambda: ea.repartition(self.o_cols, self.attn)),
             ("o_gemm_residual", lambda: J("tj,jk->tk", ea.JOIN_MUL, S, [self.attn, self.wo], self.x2,
                                           residual=self.x)),
@@ -106,11 +116,14 @@ class LlamaBlockShare:
     # memory-bound stages: read + write of the tensors they must touch)
     def work(self):
         T, Hd, hd, F = self.t, self.hidden, self.hd, self.ffn
-        causal_pairs = self.heads * T * (T + 1) // 2
+        wqkv = (self.heads + 2 * self.heads_kv) * self.d_head
+        ends = self.seq_ends or [T]
+        lens = [e - s for s, e in zip([0] + ends[:-1], ends)]
+        causal_pairs = self.heads * sum(n * (n + 1) // 2 for n in lens)
         return {
             "rmsnorm1": dict(bytes=2 * T * Hd * 2 + Hd * 2),
-            "qkv_gemm": dict(flops=2 * T * Hd * 3 * hd),
-            "repart_heads": dict(bytes=2 * T * 3 * hd * 2),
+            "qkv_gemm": dict(flops=2 * T * Hd * wqkv),
+            "repart_heads": dict(bytes=2 * T * wqkv * 2),
             "attention": dict(flops=4 * self.d_head * causal_pairs),
             "repart_cols": dict(bytes=2 * T * hd * 2),
             "o_gemm_residual": dict(flops=2 * T * hd * Hd),

@@ -180,6 +180,25 @@ CHAINS = {
 }
 
 
+def w1_block(t=8192, hidden=4096, heads=4, heads_kv=1, d_head=128, ffn=1792, block=512, seq_len=1024):
+    """One GPU's head share (8-way) of the paper's LLaMA-scale block: model
+    dim 4096, 32 query heads over 8 key/value heads of dim 128, FFN 14336,
+    on a batch of eight 1K-token sequences packed end to end."""
+    qkv = (heads + 2 * heads_kv) * d_head
+    hd = heads * d_head
+    x = normal((t, hidden), 521, 1.0, "bf16")
+    wqkv = normal((hidden, qkv), 522, 0.02, "bf16")
+    wo = normal((hd, hidden), 523, 0.02, "bf16")
+    wg = normal((hidden, ffn), 524, 0.02, "bf16")
+    wu = normal((hidden, ffn), 525, 0.02, "bf16")
+    wd = normal((ffn, hidden), 526, 0.02, "bf16")
+    n1 = uniform((hidden,), 527, 0.5, 1.5, "bf16")
+    n2 = uniform((hidden,), 528, 0.5, 1.5, "bf16")
+    return dict(x=x, wqkv=wqkv, wo=wo, wg=wg, wu=wu, wd=wd, n1=n1, n2=n2, t=t, hidden=hidden, heads=heads,
+                heads_kv=heads_kv, d_head=d_head, ffn=ffn, block=block, eps=1e-6,
+                seq_ends=list(range(seq_len, t + 1, seq_len)))
+
+
 def chain_matrices(dims, seed: int, div: int = 1):
     """Matrices of a matrix chain (dims divided by `div`), bf16, host: matrix
     i is [d_i, d_(i+1)] with N(0, 1/d_i) entries (N(0, 1) for the first), so

@@ -72,3 +72,40 @@ def test_block_full_size():
     blk.forward()
     torch.cuda.synchronize()
     assert torch.equal(y1, blk.y.bytes())
+
+
+def _run_w1(w):
+    blk = LlamaBlockShare(w["t"], w["hidden"], w["heads"], w["d_head"], w["ffn"], block=w["block"], eps=w["eps"],
+                          heads_kv=w["heads_kv"], seq_ends=w["seq_ends"])
+    blk.load(_device(w))
+    blk.forward()
+    torch.cuda.synchronize()
+    return blk
+
+
+def _oracle_w1(w):
+    f = {k: synth.to_f64(w[k], "bf16") for k in ("x", "n1", "wqkv", "wo", "wg", "wu", "wd", "n2")}
+    return oracle.llama_block(f["x"], f["n1"], f["wqkv"], f["wo"], f["wg"], f["wu"], f["wd"], f["n2"],
+                              heads=w["heads"], d_head=w["d_head"], eps=w["eps"], heads_kv=w["heads_kv"],
+                              seq_ends=w["seq_ends"])
+
+
+def test_w1_block_small_grouped_heads_packed_sequences():
+    # 4 query heads over 2 key/value heads, three packed sequences of 128, 256
+    # and 128 tokens, ragged FFN blocks: every boundary relation
+    w = synth.w1_block(t=512, hidden=512, heads=4, heads_kv=2, ffn=344, block=128, seq_len=128)
+    w["seq_ends"] = [128, 384, 512]
+    blk = _run_w1(w)
+    ref = _oracle_w1(w)
+    for name in ("h1", "qkv", "attn", "x2", "h2", "a", "y"):
+        assert_close(values(getattr(blk, name)), ref[name], rel_fro=CHAIN_REL_FRO, what=name)
+
+
+def test_w1_block_share_full_size():
+    # the benchmarked share of the paper's block: d 4096, 4 of 32 query heads
+    # over 1 of 8 key/value heads, FFN 1792 of 14336, eight packed 1K sequences
+    w = synth.w1_block()
+    blk = _run_w1(w)
+    ref = _oracle_w1(w)
+    for name in ("h1", "qkv", "attn", "x2", "h2", "a", "y"):
+        assert_close(values(getattr(blk, name)), ref[name], rel_fro=CHAIN_REL_FRO, what=name)
