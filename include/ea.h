@@ -247,6 +247,47 @@ int ea_overlay(int32_t rank, const int32_t* nblocks_a, const int64_t* splits_a,
                const int32_t* nblocks_b, const int64_t* splits_b,
                int32_t* nblocks_out, int64_t* splits_out);
 
+/* ---- logical optimization (Section 4) -----------------------------------
+   Chooses a join-agg spec for every abstract operator of a computation over
+   p processors, minimising the communication proxy of Section 4.3, with the
+   dynamic program over output tilings of Section 4.2 (Algorithm "Logical
+   optimization").  A spec decomposes each shardable letter of the operator
+   into near-equal intervals whose counts multiply to p (at most the letter's
+   extent each); it is given by those counts.  Cost of a spec J with input
+   tilings T_k:
+     repartition: + |X_k| for each input k produced by an operator whose
+                  chosen output tiling differs from the tiling J needs
+                  (computation inputs are materialised as J needs: 0);
+     join:        + |X_k| * p / (product of the counts of input k's letters),
+                  the numbers in every function specification's k-th input;
+     aggregation: + (p / (product of the output letters' counts) - 1) * |Y|,
+                  the extra copies of every output block.
+   Operators are listed producers first.  An output consumed once makes a
+   tree edge; an output consumed several times (or by none: a designated
+   output) roots a tree (Section 4.5).  Trees are optimised one at a time,
+   largest first: a tensor from a tree already optimised enters with its
+   chosen tiling (repartition charged), one from a tree not yet optimised
+   as a computation input, whose later tiling choice is charged for the
+   consumers already fixed.  Within a tree the plan is optimal. Host only. */
+#define EA_LOP_MAX_INPUTS 8
+typedef struct ea_lop {
+  const char* spec;        /* the operator's einsum, e.g. "ij,jk->ik"              */
+  const int64_t* extents;  /* extent of every distinct letter of spec, in order of
+                              first appearance (inputs left to right, then output) */
+  const char* shardable;   /* letters that may be split; NULL: every letter      */
+  int32_t input[EA_LOP_MAX_INPUTS]; /* per input of spec: the producing operator's
+                              index (lower than this one's), or -1 for a
+                              computation input                                   */
+} ea_lop;
+/* counts: n_ops x 16 int32 (the interval count of every letter of each
+   operator, letters in order of first appearance; unused entries 0).
+   cost: the chosen plan's total cost under the model above.
+   Errors: EA_ERR_ARG (NULL pointers, p < 1, extents < 1, a bad producer
+   index); EA_ERR_SPEC (bad spec, or a producer's output shape differing from
+   the consumer's input); EA_ERR_UNSUPPORTED (an operator has no spec: p is no
+   product of counts within its shardable extents, or more than 2^20 specs). */
+int ea_logical_plan(int32_t n_ops, const ea_lop* ops, int64_t p, int32_t* counts, int64_t* cost);
+
 /* ---- plan cache --------------------------------------------------------- */
 /* Number of cached plans (all devices). */
 int64_t ea_plan_cache_size(void);

@@ -39,6 +39,7 @@ Pin status (what each function is checked against, in tests/test_oracle_pins.py)
 from __future__ import annotations
 
 import ctypes
+import itertools
 import os
 import subprocess
 
@@ -367,3 +368,96 @@ def llama_block(x, n1, wqkv, wo, wg, wu, wd, n2, heads: int, d_head: int, eps: f
     a = r(silu_mul(matmul(h2, wg), matmul(h2, wu)))
     y = r(add(x2, matmul(a, wd)))
     return dict(h1=h1, qkv=qkv, attn=attn, x2=x2, h2=h2, a=a, y=y)
+
+
+# --------------------------------------------------------------------------
+# logical optimization (Section 4): brute force over every combination of
+# join-agg specs, pure Python (small cases only)
+# --------------------------------------------------------------------------
+def _letters(spec: str):
+    out = []
+    for ch in spec.replace(",", "").replace("->", ""):
+        if ch not in out:
+            out.append(ch)
+    return out
+
+
+def logical_specs(spec: str, extents: dict, p: int, shardable=None):
+    """Every join-agg spec of an operator over p processors (Section 4.2): an
+    interval count per letter, 1 for letters that may not be split, each at
+    most the letter's extent, multiplying to p."""
+    letters = _letters(spec)
+    out = []
+
+    def rec(i, rem, cur):
+        if i == len(letters):
+            if rem == 1:
+                out.append(dict(cur))
+            return
+        l = letters[i]
+        if shardable is not None and l not in shardable:
+            cur[l] = 1
+            rec(i + 1, rem, cur)
+            return
+        for v in range(1, min(rem, extents[l]) + 1):
+            if rem % v == 0:
+                cur[l] = v
+                rec(i + 1, rem // v, cur)
+
+    rec(0, p, {})
+    return out
+
+
+def _intervals(n: int, c: int):
+    pts = [(i * n) // c for i in range(c)] + [n]
+    return [(pts[i], pts[i + 1]) for i in range(c)]
+
+
+def logical_spec_cost(spec: str, extents: dict, counts: dict, input_tilings):
+    """Cost (Section 4.3) of one operator's spec, by its definition: the
+    function specifications are the cells of the interval grid; join adds
+    the numbers in every cell's input blocks, aggregation (m - 1) times each
+    distinct output block's numbers, repartition the whole input tensor for
+    every input whose given tiling (a tuple of counts, None for a
+    computation input) differs from the one the spec needs."""
+    lhs, out = spec.split("->")
+    ins = lhs.split(",")
+    letters = _letters(spec)
+    grids = [_intervals(extents[l], counts[l]) for l in letters]
+    cost = 0
+    out_seen = {}
+    for cell in itertools.product(*grids):
+        iv = dict(zip(letters, cell))
+        for operand in ins:
+            cost += int(np.prod([iv[l][1] - iv[l][0] for l in operand]))
+        key = tuple(iv[l] for l in out)
+        out_seen[key] = out_seen.get(key, 0) + 1
+    for key, m in out_seen.items():
+        cost += (m - 1) * int(np.prod([hi - lo for lo, hi in key]))
+    for operand, t in zip(ins, input_tilings):
+        if t is not None and tuple(t) != tuple(counts[l] for l in operand):
+            cost += int(np.prod([extents[l] for l in operand]))
+    return cost
+
+
+def logical_plan_cost(ops, choice):
+    """Total cost of a plan: ops are (spec, extents, inputs, shardable) with
+    inputs naming producer indices (None: computation input); choice gives
+    each operator's counts."""
+    total = 0
+    for (spec, extents, inputs, _), counts in zip(ops, choice):
+        tilings = []
+        for x in inputs:
+            if x is None:
+                tilings.append(None)
+            else:
+                pspec, _, _, _ = ops[x]
+                tilings.append(tuple(choice[x][l] for l in pspec.split("->")[1]))
+        total += logical_spec_cost(spec, extents, counts, tilings)
+    return total
+
+
+def logical_min_cost(ops, p: int):
+    """The minimum total cost over every combination of specs (exhaustive)."""
+    all_specs = [logical_specs(spec, ext, p, sh) for spec, ext, _, sh in ops]
+    return min(logical_plan_cost(ops, combo) for combo in itertools.product(*all_specs))

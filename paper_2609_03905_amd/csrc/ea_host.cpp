@@ -35,11 +35,10 @@ struct ea_relation {
   int64_t capacity = 0;
 };
 
-namespace {
-
 // ---------------------------------------------------------------------------
-// errors
+// errors (shared with the other host sources through ea_internal.h)
 // ---------------------------------------------------------------------------
+namespace ea {
 thread_local std::string g_err;
 
 int fail(int code, const char* fmt, ...) {
@@ -56,6 +55,9 @@ int ok() {
   g_err.clear();
   return EA_OK;
 }
+}  // namespace ea
+
+namespace {
 
 #define EA_HIP_TRY(expr)                                                              \
   do {                                                                                \
@@ -149,15 +151,12 @@ std::vector<DevBlk> dev_blocks(const ea_relation* r) {
   return v;
 }
 
+}  // namespace
+
 // ---------------------------------------------------------------------------
 // einsum spec
 // ---------------------------------------------------------------------------
-struct Spec {
-  int n_in = 0;
-  int rank[kMaxOps] = {};
-  char let[kMaxOps][kMaxRank] = {};
-};
-
+namespace ea {
 bool is_letter(char ch) { return (ch >= 'a' && ch <= 'z') || (ch >= 'A' && ch <= 'Z'); }
 
 int parse_spec(const char* s, Spec* sp) {
@@ -209,6 +208,9 @@ int find_dim(const Spec& sp, int op, char l) {
     if (sp.let[op][d] == l) return d;
   return -1;
 }
+}  // namespace ea
+
+namespace {
 
 // ---------------------------------------------------------------------------
 // join analysis: letter order, partitions, validation (Section 3.2)

@@ -36,6 +36,21 @@ struct DevBlk {
 // matching by binary search on the operand's split points) and the optional
 // causal predicate holds.
 // ---------------------------------------------------------------------------
+// Host helpers shared by the host sources: the thread's last error message
+// (fail sets it and returns code, ok clears it and returns EA_OK) and the
+// einsum spec parser.
+int fail(int code, const char* fmt, ...);
+int ok();
+
+struct Spec {
+  int n_in = 0;
+  int rank[kMaxOps] = {};
+  char let[kMaxOps][kMaxRank] = {};
+};
+bool is_letter(char ch);
+int parse_spec(const char* s, Spec* sp);
+int find_dim(const Spec& sp, int op, char l);
+
 struct EnumDesc {
   int32_t n_in;
   int32_t n_letters;
