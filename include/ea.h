@@ -288,6 +288,36 @@ typedef struct ea_lop {
    product of counts within its shardable extents, or more than 2^20 specs). */
 int ea_logical_plan(int32_t n_ops, const ea_lop* ops, int64_t p, int32_t* counts, int64_t* cost);
 
+/* ---- exchange programs (Section 5.2; Definition "Closure; validity") -----
+   Text of an ExProg program: declarations, then (after a blank line) a body
+   of actions, statements separated by ';' or new lines.
+     GPUS: 0, 1, 2, 3                      (optional: else every site named)
+     PARTITIONS: G1 {size 2} G2 {0, 3}     (by size, or by members)
+     IN:  A @ 0 (size: 1.0 GB); B @ 1      (atoms; size defaults to 1 GB)
+     OUT: A+B @ 0, 1; C @ G1               (aggregates at sites or partitions)
+     A @ 0 -> 1;  A+B @ 1 -> 2 -> 3;  A+B @ G1
+   An action X @ s [-> D ...] is enabled when aggregates present at s
+   partition X; firing it materialises X at s and at every destination (a
+   chain -> r -> d relays through r; a source list or partition fires at
+   every listed site).  The closure is the least state containing IN that is
+   closed under firing enabled actions; a program is valid when every action
+   is enabled by its closure and every OUT requirement is in it.  Partitions
+   declared by size are valid if some membership works: partitions are
+   disjoint and together cover the GPUs, members of a partition declared by
+   size are drawn from the GPUs no explicit partition holds, memberships
+   tried in lexicographic order.  Host only. */
+/* valid: 1 or 0.  why: for an invalid program, the first OUT requirement
+   missing or the first action never enabled (NUL-terminated, truncated to
+   why_cap).  Errors: EA_ERR_ARG (NULL text or outputs), EA_ERR_SPEC (syntax:
+   unknown site, atom or partition, malformed statement). */
+int ea_exprog_check(const char* text, int32_t* valid, char* why, int64_t why_cap);
+/* A valid body for the declarations of `text` (its body, if any, is ignored):
+   every atom of each OUT aggregate is sent from the site holding it to each
+   target site, then the aggregate is formed locally there.  Writes the
+   declarations plus that body to out (NUL-terminated; *len = its length
+   without the NUL; EA_ERR_CAPACITY if cap is too small, *len still set). */
+int ea_exprog_naive(const char* text, char* out, int64_t cap, int64_t* len);
+
 /* ---- plan cache --------------------------------------------------------- */
 /* Number of cached plans (all devices). */
 int64_t ea_plan_cache_size(void);

@@ -461,3 +461,41 @@ def logical_min_cost(ops, p: int):
     """The minimum total cost over every combination of specs (exhaustive)."""
     all_specs = [logical_specs(spec, ext, p, sh) for spec, ext, _, sh in ops]
     return min(logical_plan_cost(ops, combo) for combo in itertools.product(*all_specs))
+
+
+# --------------------------------------------------------------------------
+# exchange programs (Section 5.2, Definition "Closure; validity"), pure
+# Python on structured programs with fixed sites
+# --------------------------------------------------------------------------
+def exprog_valid(ins, outs, actions):
+    """ins: [(atom, site)]; outs: [(atoms, [sites])]; actions: [(atoms,
+    [source sites], [[hop sites], ...])].  The closure: start from each IN
+    atom at its site; an action at a source site is enabled when some
+    aggregates present there are pairwise disjoint with union its atoms
+    (tried over every subset of the present aggregates); firing adds the
+    aggregate at the source and at every hop's sites.  Valid: every action
+    fires at every source, and every OUT aggregate is at each of its sites."""
+    state = set((frozenset([a]), s) for a, s in ins)
+    pending = [(frozenset(x), s, hops) for x, srcs, hops in actions for s in srcs]
+    fired = [False] * len(pending)
+
+    def enabled(x, s):
+        here = [a for a, t in state if t == s and a <= x]
+        for n in range(1, len(here) + 1):
+            for combo in itertools.combinations(here, n):
+                if sum(len(c) for c in combo) == len(x) and frozenset().union(*combo) == x:
+                    return True
+        return False
+
+    changed = True
+    while changed:
+        changed = False
+        for i, (x, s, hops) in enumerate(pending):
+            if not fired[i] and enabled(x, s):
+                fired[i] = True
+                changed = True
+                state.add((x, s))
+                for hop in hops:
+                    for d in hop:
+                        state.add((x, d))
+    return all(fired) and all((frozenset(x), s) in state for x, sites in outs for s in sites)

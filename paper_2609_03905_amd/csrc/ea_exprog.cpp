@@ -1,0 +1,489 @@
+// ea_exprog.cpp -- exchange programs (Section 5.2): the ExProg text format,
+// the closure and validity of Definition "Closure; validity", memberships of
+// partitions declared by size, and the naive valid program that gathers the
+// atoms of every required aggregate at its targets (Section 5.4).
+#include <algorithm>
+#include <cctype>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "ea_internal.h"
+
+namespace ea {
+namespace {
+
+using Agg = std::vector<int>;  // sorted atom ids
+
+struct Target {
+  bool part = false;
+  int id = 0;  // site, or partition index
+};
+
+struct Action {
+  Agg agg;
+  std::vector<Target> src;
+  std::vector<std::vector<Target>> hops;  // destination lists, in order
+  std::string text;
+};
+
+struct Part {
+  std::string name;
+  int size = 0;
+  bool by_size = false;
+  std::vector<int> members;
+};
+
+struct Prog {
+  std::vector<int> gpus;
+  bool implicit_gpus = false;  // no GPUS declaration: every site named is a GPU
+  std::vector<std::string> atom_name;
+  std::vector<double> atom_bytes;
+  std::map<std::string, int> atom_id;
+  std::vector<Part> parts;
+  std::vector<std::pair<int, int>> ins;  // (atom, site)
+  std::vector<std::pair<Agg, std::vector<Target>>> outs;
+  std::vector<Action> acts;
+  std::string decl_text;  // the declarations, as written
+};
+
+std::string trim(const std::string& s) {
+  size_t a = 0, b = s.size();
+  while (a < b && isspace((unsigned char)s[a])) ++a;
+  while (b > a && isspace((unsigned char)s[b - 1])) --b;
+  return s.substr(a, b - a);
+}
+
+std::vector<std::string> split(const std::string& s, char sep) {
+  std::vector<std::string> out;
+  std::string cur;
+  for (char c : s) {
+    if (c == sep) {
+      out.push_back(cur);
+      cur.clear();
+    } else {
+      cur += c;
+    }
+  }
+  out.push_back(cur);
+  return out;
+}
+
+bool parse_int(const std::string& t, int* v) {
+  const std::string s = trim(t);
+  if (s.empty()) return false;
+  for (char c : s)
+    if (!isdigit((unsigned char)c)) return false;
+  *v = atoi(s.c_str());
+  return true;
+}
+
+int site_of(Prog& p, const std::string& tok, Target* t) {
+  int v;
+  const std::string s = trim(tok);
+  if (parse_int(s, &v)) {
+    if (std::find(p.gpus.begin(), p.gpus.end(), v) == p.gpus.end()) {
+      if (!p.implicit_gpus) return fail(EA_ERR_SPEC, "ExProg: site %d is not among the GPUS", v);
+      p.gpus.push_back(v);
+    }
+    *t = Target{false, v};
+    return EA_OK;
+  }
+  for (size_t i = 0; i < p.parts.size(); ++i)
+    if (p.parts[i].name == s) {
+      *t = Target{true, (int)i};
+      return EA_OK;
+    }
+  return fail(EA_ERR_SPEC, "ExProg: unknown site or partition '%s'", s.c_str());
+}
+
+int targets_of(Prog& p, const std::string& list, std::vector<Target>* out) {
+  out->clear();
+  for (const std::string& tok : split(list, ',')) {
+    Target t;
+    const int e = site_of(p, tok, &t);
+    if (e) return e;
+    out->push_back(t);
+  }
+  return EA_OK;
+}
+
+int agg_of(Prog& p, const std::string& text, Agg* out) {
+  out->clear();
+  for (const std::string& tok : split(text, '+')) {
+    const std::string a = trim(tok);
+    auto it = p.atom_id.find(a);
+    if (it == p.atom_id.end()) return fail(EA_ERR_SPEC, "ExProg: unknown atom '%s'", a.c_str());
+    out->push_back(it->second);
+  }
+  std::sort(out->begin(), out->end());
+  if (std::adjacent_find(out->begin(), out->end()) != out->end())
+    return fail(EA_ERR_SPEC, "ExProg: atom repeated in '%s'", trim(text).c_str());
+  return EA_OK;
+}
+
+double parse_size(const std::string& s) {  // "(size: 1.5 GB)"
+  const size_t c = s.find(':');
+  const std::string body = trim(s.substr(c == std::string::npos ? 0 : c + 1));
+  char* end = nullptr;
+  const double v = strtod(body.c_str(), &end);
+  std::string unit = trim(std::string(end));
+  if (!unit.empty() && unit.back() == ')') unit.pop_back();
+  unit = trim(unit);
+  const double scale = unit == "KB" ? 1e3 : unit == "MB" ? 1e6 : unit == "B" ? 1.0 : 1e9;
+  return v * scale;
+}
+
+const char* kKeys[] = {"GPUS:", "PARTITIONS:", "IN:", "OUT:"};
+
+int key_of(const std::string& line) {
+  const std::string s = trim(line);
+  for (int k = 0; k < 4; ++k)
+    if (s.compare(0, strlen(kKeys[k]), kKeys[k]) == 0) return k;
+  return -1;
+}
+
+int parse(const char* text, Prog* p) {
+  std::string sect[4];
+  std::string body;
+  int cur = -1;
+  bool in_body = false, any_decl = false;
+  std::string decl;
+  for (const std::string& raw : split(text, '\n')) {
+    const std::string line = trim(raw);
+    const int k = key_of(line);
+    if (k >= 0) {
+      cur = k;
+      in_body = false;
+      any_decl = true;
+      sect[k] += " " + line.substr(strlen(kKeys[k])) + ";";
+      decl += raw + "\n";
+      continue;
+    }
+    if (line.empty()) {
+      if (any_decl) in_body = true;
+      cur = -1;
+      continue;
+    }
+    if (cur >= 0 && !in_body) {
+      sect[cur] += " " + line + ";";
+      decl += raw + "\n";
+    } else {
+      body += line + ";";
+    }
+  }
+  p->decl_text = decl;
+  // GPUS (default: every site named anywhere is an error without it)
+  for (const std::string& tok : split(sect[0], ',')) {
+    for (const std::string& t2 : split(tok, ';')) {
+      int v;
+      if (trim(t2).empty()) continue;
+      if (!parse_int(t2, &v)) return fail(EA_ERR_SPEC, "ExProg: bad GPU '%s'", trim(t2).c_str());
+      p->gpus.push_back(v);
+    }
+  }
+  p->implicit_gpus = p->gpus.empty();
+  // PARTITIONS: name {size n} | name {a, b, ...}
+  {
+    std::string s = sect[1];
+    size_t i = 0;
+    while (true) {
+      const size_t lb = s.find('{', i);
+      if (lb == std::string::npos) break;
+      const size_t rb = s.find('}', lb);
+      if (rb == std::string::npos) return fail(EA_ERR_SPEC, "ExProg: unclosed partition");
+      std::string name = trim(s.substr(i, lb - i));
+      while (!name.empty() && name.front() == ';') name = trim(name.substr(1));
+      const std::string inner = trim(s.substr(lb + 1, rb - lb - 1));
+      Part pt;
+      pt.name = name;
+      if (name.empty()) return fail(EA_ERR_SPEC, "ExProg: unnamed partition");
+      if (inner.compare(0, 4, "size") == 0) {
+        pt.by_size = true;
+        if (!parse_int(inner.substr(4), &pt.size) || pt.size < 1)
+          return fail(EA_ERR_SPEC, "ExProg: partition %s: bad size", name.c_str());
+      } else {
+        for (const std::string& tok : split(inner, ',')) {
+          int v;
+          if (!parse_int(tok, &v)) return fail(EA_ERR_SPEC, "ExProg: partition %s: bad member", name.c_str());
+          pt.members.push_back(v);
+        }
+        pt.size = (int)pt.members.size();
+      }
+      p->parts.push_back(pt);
+      i = rb + 1;
+    }
+    for (const Part& pt : p->parts)
+      for (int m : pt.members) {
+        Target t;
+        const int e = site_of(*p, std::to_string(m), &t);
+        if (e) return e;
+      }
+  }
+  // IN: atom @ site (size: ...)
+  for (const std::string& st : split(sect[2], ';')) {
+    std::string s = trim(st);
+    if (s.empty()) continue;
+    double bytes = 1e9;
+    const size_t lp = s.find('(');
+    if (lp != std::string::npos) {
+      bytes = parse_size(s.substr(lp + 1));
+      s = trim(s.substr(0, lp));
+    }
+    const size_t at = s.find('@');
+    if (at == std::string::npos) return fail(EA_ERR_SPEC, "ExProg: IN '%s' has no '@'", s.c_str());
+    const std::string name = trim(s.substr(0, at));
+    if (name.empty() || name.find('+') != std::string::npos)
+      return fail(EA_ERR_SPEC, "ExProg: IN '%s' must place one atom", s.c_str());
+    Target t;
+    int e = site_of(*p, s.substr(at + 1), &t);
+    if (e) return e;
+    if (t.part) return fail(EA_ERR_SPEC, "ExProg: IN places atoms at GPUs");
+    if (p->atom_id.count(name)) return fail(EA_ERR_SPEC, "ExProg: atom %s placed twice", name.c_str());
+    p->atom_id[name] = (int)p->atom_name.size();
+    p->atom_name.push_back(name);
+    p->atom_bytes.push_back(bytes);
+    p->ins.push_back({p->atom_id[name], t.id});
+  }
+  // OUT: aggregate @ targets
+  for (const std::string& st : split(sect[3], ';')) {
+    const std::string s = trim(st);
+    if (s.empty()) continue;
+    const size_t at = s.find('@');
+    if (at == std::string::npos) return fail(EA_ERR_SPEC, "ExProg: OUT '%s' has no '@'", s.c_str());
+    Agg a;
+    std::vector<Target> ts;
+    int e = agg_of(*p, s.substr(0, at), &a);
+    if (!e) e = targets_of(*p, s.substr(at + 1), &ts);
+    if (e) return e;
+    p->outs.push_back({a, ts});
+  }
+  // body: X @ sources [-> destinations ...]
+  for (const std::string& st : split(body, ';')) {
+    const std::string s = trim(st);
+    if (s.empty()) continue;
+    Action act;
+    act.text = s;
+    std::vector<std::string> parts;
+    size_t i = 0;
+    while (true) {
+      const size_t ar = s.find("->", i);
+      parts.push_back(s.substr(i, ar == std::string::npos ? std::string::npos : ar - i));
+      if (ar == std::string::npos) break;
+      i = ar + 2;
+    }
+    const size_t at = parts[0].find('@');
+    if (at == std::string::npos) return fail(EA_ERR_SPEC, "ExProg: action '%s' has no '@'", s.c_str());
+    int e = agg_of(*p, parts[0].substr(0, at), &act.agg);
+    if (!e) e = targets_of(*p, parts[0].substr(at + 1), &act.src);
+    for (size_t h = 1; !e && h < parts.size(); ++h) {
+      std::vector<Target> d;
+      e = targets_of(*p, parts[h], &d);
+      act.hops.push_back(d);
+    }
+    if (e) return e;
+    p->acts.push_back(act);
+  }
+  // partitions: disjoint, together covering the GPUs
+  int total = 0;
+  std::set<int> seen;
+  for (const Part& pt : p->parts) {
+    total += pt.size;
+    for (int m : pt.members)
+      if (!seen.insert(m).second) return fail(EA_ERR_SPEC, "ExProg: site %d in two partitions", m);
+  }
+  if (!p->parts.empty() && total != (int)p->gpus.size())
+    return fail(EA_ERR_SPEC, "ExProg: partitions hold %d sites, not the %d GPUS", total, (int)p->gpus.size());
+  std::sort(p->gpus.begin(), p->gpus.end());
+  return EA_OK;
+}
+
+std::vector<int> sites(const Prog& p, const std::vector<Target>& ts, const std::vector<std::vector<int>>& mem) {
+  std::vector<int> out;
+  for (const Target& t : ts) {
+    if (!t.part) out.push_back(t.id);
+    else out.insert(out.end(), mem[(size_t)t.id].begin(), mem[(size_t)t.id].end());
+  }
+  return out;
+}
+
+// do aggregates present at a site partition X (an exact cover by subsets)?
+bool covers(const std::set<Agg>& here, const Agg& x) {
+  if (here.count(x)) return true;
+  std::vector<const Agg*> cand;
+  for (const Agg& a : here)
+    if (std::includes(x.begin(), x.end(), a.begin(), a.end())) cand.push_back(&a);
+  std::vector<char> used(x.size(), 0);
+  auto pos = [&](int atom) { return (size_t)(std::lower_bound(x.begin(), x.end(), atom) - x.begin()); };
+  auto rec = [&](auto&& self) -> bool {
+    size_t first = 0;
+    while (first < x.size() && used[first]) ++first;
+    if (first == x.size()) return true;
+    for (const Agg* a : cand) {
+      if (!std::binary_search(a->begin(), a->end(), x[first])) continue;
+      bool free_all = true;
+      for (int at : *a) free_all &= !used[pos(at)];
+      if (!free_all) continue;
+      for (int at : *a) used[pos(at)] = 1;
+      if (self(self)) return true;
+      for (int at : *a) used[pos(at)] = 0;
+    }
+    return false;
+  };
+  return rec(rec);
+}
+
+// closure and validity for one membership of the partitions
+bool check(const Prog& p, const std::vector<std::vector<int>>& mem, std::string* why) {
+  std::map<int, std::set<Agg>> state;
+  for (const auto& in : p.ins) state[in.second].insert(Agg{in.first});
+  // (action, source site) pairs; fired when enabled, to a fixed point
+  std::vector<std::pair<int, int>> todo;
+  for (size_t a = 0; a < p.acts.size(); ++a)
+    for (int s : sites(p, p.acts[a].src, mem)) todo.push_back({(int)a, s});
+  std::vector<char> fired(todo.size(), 0);
+  for (bool changed = true; changed;) {
+    changed = false;
+    for (size_t i = 0; i < todo.size(); ++i) {
+      if (fired[i]) continue;
+      const Action& act = p.acts[(size_t)todo[i].first];
+      if (!covers(state[todo[i].second], act.agg)) continue;
+      fired[i] = 1;
+      changed = true;
+      state[todo[i].second].insert(act.agg);
+      for (const auto& hop : act.hops)
+        for (int d : sites(p, hop, mem)) state[d].insert(act.agg);
+    }
+  }
+  for (size_t i = 0; i < todo.size(); ++i)
+    if (!fired[i]) {
+      *why = "action '" + p.acts[(size_t)todo[i].first].text + "' is never enabled at site " +
+             std::to_string(todo[i].second);
+      return false;
+    }
+  for (const auto& req : p.outs)
+    for (int s : sites(p, req.second, mem))
+      if (!state[s].count(req.first)) {
+        std::string name;
+        for (int a : req.first) name += (name.empty() ? "" : "+") + p.atom_name[(size_t)a];
+        *why = "OUT " + name + " is not materialised at site " + std::to_string(s);
+        return false;
+      }
+  return true;
+}
+
+// memberships of the partitions declared by size, lexicographic order; fn
+// returns true to stop
+template <class F>
+void memberships(const Prog& p, F&& fn) {
+  std::vector<std::vector<int>> mem(p.parts.size());
+  std::vector<int> free;
+  std::set<int> taken;
+  for (size_t i = 0; i < p.parts.size(); ++i)
+    if (!p.parts[i].by_size) {
+      mem[i] = p.parts[i].members;
+      taken.insert(p.parts[i].members.begin(), p.parts[i].members.end());
+    }
+  for (int g : p.gpus)
+    if (!taken.count(g)) free.push_back(g);
+  std::vector<char> used(free.size(), 0);
+  bool stop = false;
+  auto rec = [&](auto&& self, size_t part) -> void {
+    if (stop) return;
+    while (part < p.parts.size() && !p.parts[part].by_size) ++part;
+    if (part == p.parts.size()) {
+      stop = fn(mem);
+      return;
+    }
+    // choose size-many unused free sites in increasing order
+    std::vector<int>& m = mem[part];
+    auto pick = [&](auto&& pk, size_t from) -> void {
+      if (stop) return;
+      if ((int)m.size() == p.parts[part].size) {
+        self(self, part + 1);
+        return;
+      }
+      for (size_t j = from; j < free.size(); ++j) {
+        if (used[j]) continue;
+        used[j] = 1;
+        m.push_back(free[j]);
+        pk(pk, j + 1);
+        m.pop_back();
+        used[j] = 0;
+        if (stop) return;
+      }
+    };
+    pick(pick, 0);
+  };
+  rec(rec, 0);
+}
+
+}  // namespace
+}  // namespace ea
+
+using namespace ea;
+
+extern "C" int ea_exprog_check(const char* text, int32_t* valid, char* why, int64_t why_cap) {
+  if (!text || !valid) return fail(EA_ERR_ARG, "ea_exprog_check: NULL argument");
+  Prog p;
+  int e = parse(text, &p);
+  if (e) return e;
+  std::string first_why;
+  bool ok_any = false;
+  memberships(p, [&](const std::vector<std::vector<int>>& mem) {
+    std::string w;
+    if (check(p, mem, &w)) {
+      ok_any = true;
+      return true;
+    }
+    if (first_why.empty()) first_why = w;
+    return false;
+  });
+  *valid = ok_any ? 1 : 0;
+  if (why && why_cap > 0) {
+    const std::string w = ok_any ? std::string() : first_why;
+    const size_t n = std::min<size_t>(w.size(), (size_t)why_cap - 1);
+    memcpy(why, w.data(), n);
+    why[n] = 0;
+  }
+  return ok();
+}
+
+extern "C" int ea_exprog_naive(const char* text, char* out, int64_t cap, int64_t* len) {
+  if (!text || !len) return fail(EA_ERR_ARG, "ea_exprog_naive: NULL argument");
+  Prog p;
+  int e = parse(text, &p);
+  if (e) return e;
+  std::vector<std::vector<int>> first;
+  memberships(p, [&](const std::vector<std::vector<int>>& mem) {
+    first = mem;
+    return true;
+  });
+  std::string body;
+  std::set<std::string> seen;
+  auto emit = [&](const std::string& a) {
+    if (seen.insert(a).second) body += a + "\n";
+  };
+  std::vector<int> home(p.atom_name.size(), -1);
+  for (const auto& in : p.ins) home[(size_t)in.first] = in.second;
+  for (const auto& req : p.outs) {
+    std::string name;
+    for (int a : req.first) name += (name.empty() ? "" : "+") + p.atom_name[(size_t)a];
+    for (int t : sites(p, req.second, first)) {
+      for (int a : req.first)
+        if (home[(size_t)a] != t)
+          emit(p.atom_name[(size_t)a] + " @ " + std::to_string(home[(size_t)a]) + " -> " + std::to_string(t));
+      if (req.first.size() > 1) emit(name + " @ " + std::to_string(t));
+    }
+  }
+  const std::string prog = p.decl_text + "\n" + body;
+  *len = (int64_t)prog.size();
+  if (!out || cap < (int64_t)prog.size() + 1)
+    return fail(EA_ERR_CAPACITY, "ea_exprog_naive: %lld bytes needed", (long long)prog.size() + 1);
+  memcpy(out, prog.data(), prog.size());
+  out[prog.size()] = 0;
+  return ok();
+}

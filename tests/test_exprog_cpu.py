@@ -1,0 +1,106 @@
+"""Exchange programs (Section 5.2) on the CPU: the paper's example programs
+are valid under Definition "Closure; validity" and stop being valid when an
+action they need is removed; the preamble of Example "Generating a preamble"
+needs a body, which the naive program provides; the native checker agrees
+with the oracle's literal closure on random programs."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_03905_amd import ea, exprog
+
+with open(os.path.join(os.path.dirname(__file__), "golden", "exprog_examples.json")) as f:
+    EX = json.load(f)
+
+
+@pytest.mark.parametrize("name", ["swap", "doubling", "v100"])
+def test_paper_examples_are_valid(name):
+    assert exprog.check(EX[name]) == (True, "")
+
+
+@pytest.mark.parametrize("name,drop", [("swap", "B @ 1 -> 0"), ("doubling", "C+D @ 2 -> 0"),
+                                       ("v100", "E+F @ 4 -> 0")])
+def test_removing_a_needed_action_invalidates(name, drop):
+    text = EX[name]
+    assert drop in text
+    bad = text.replace(drop + ";", "").replace(drop, "")
+    valid, why = exprog.check(bad)
+    assert not valid and why
+
+
+def test_v100_groups_must_follow_the_pillars():
+    # with the partitions fixed to the machine's sockets instead, the body
+    # (which aggregates across the 0-4, 1-5, 2-6, 3-7 pairs) is invalid; with
+    # the groups the paper names it is valid
+    sock = EX["v100"].replace("G1 {size 4} G2 {size 4}", "G1 {0, 1, 2, 3} G2 {4, 5, 6, 7}")
+    assert not exprog.check(sock)[0]
+    g1, g2 = EX["v100_groups"]
+    named = EX["v100"].replace("G1 {size 4} G2 {size 4}",
+                               "G1 {%s} G2 {%s}" % (", ".join(map(str, g1)), ", ".join(map(str, g2))))
+    assert exprog.check(named) == (True, "")
+
+
+def test_preamble_needs_a_body_and_the_naive_program_is_valid():
+    valid, why = exprog.check(EX["preamble"])
+    assert not valid and "X1+Y1" in why
+    prog = exprog.naive(EX["preamble"])
+    assert prog.startswith(EX["preamble"])
+    assert exprog.check(prog) == (True, "")
+    for name in ("swap", "doubling", "v100"):
+        decl = EX[name].split("\n\n")[0] + "\n"
+        assert exprog.check(exprog.naive(decl)) == (True, "")
+
+
+def test_syntax_errors():
+    for bad in ("IN: A @ 0\nOUT: B @ 0\n",            # unknown atom
+                "GPUS: 0, 1\nIN: A @ 2\nOUT: A @ 0\n",  # site not among the GPUS
+                "IN: A @ 0\nOUT: A @ G1\n",            # unknown partition
+                "GPUS: 0, 1\nPARTITIONS: G1 {size 3}\nIN: A @ 0\nOUT: A @ G1\n"):  # partitions do not cover
+        with pytest.raises(ea.EAError) as e:
+            exprog.check(bad)
+        assert e.value.code == -5
+
+
+def _render(n_sites, ins, outs, actions):
+    names = {a: f"A{a}" for a, _ in ins}
+    agg = lambda xs: "+".join(names[a] for a in sorted(xs))
+    text = "GPUS: " + ", ".join(map(str, range(n_sites))) + "\n"
+    text += "IN: " + "; ".join(f"{names[a]} @ {s}" for a, s in ins) + "\n"
+    text += "OUT: " + "; ".join(f"{agg(x)} @ " + ", ".join(map(str, ss)) for x, ss in outs) + "\n\n"
+    for x, srcs, hops in actions:
+        text += f"{agg(x)} @ " + ", ".join(map(str, srcs)) + "".join(" -> " + ", ".join(map(str, h)) for h in hops) + "\n"
+    return text
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_checker_matches_the_literal_closure(seed):
+    rng = np.random.default_rng(seed)
+    n_sites, n_atoms = int(rng.integers(2, 5)), int(rng.integers(2, 6))
+    ins = [(a, int(rng.integers(0, n_sites))) for a in range(n_atoms)]
+
+    def rand_agg():
+        k = int(rng.integers(1, n_atoms + 1))
+        return frozenset(int(x) for x in rng.choice(n_atoms, k, replace=False))
+
+    def rand_sites():
+        return sorted(set(int(x) for x in rng.choice(n_sites, int(rng.integers(1, n_sites + 1)))))
+
+    outs = [(rand_agg(), rand_sites()) for _ in range(int(rng.integers(1, 3)))]
+    actions = []
+    for _ in range(int(rng.integers(0, 8)) if seed % 3 else 0):  # seed % 3 == 0: the gather body alone
+        hops = [rand_sites() for _ in range(int(rng.integers(0, 3)))]
+        actions.append((rand_agg(), rand_sites(), hops))
+    if seed % 3 != 2:  # a gather-everything body, valid on its own
+        for x, ss in outs:
+            for s in ss:
+                for a in x:
+                    src = dict(ins)[a]
+                    if src != s:
+                        actions.append((frozenset([a]), [src], [[s]]))
+                if len(x) > 1:
+                    actions.append((x, [s], []))
+    text = _render(n_sites, ins, outs, actions)
+    assert exprog.check(text)[0] == oracle.exprog_valid(ins, outs, actions), text
