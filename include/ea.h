@@ -317,6 +317,16 @@ int ea_exprog_check(const char* text, int32_t* valid, char* why, int64_t why_cap
    declarations plus that body to out (NUL-terminated; *len = its length
    without the NUL; EA_ERR_CAPACITY if cap is too small, *len still set). */
 int ea_exprog_naive(const char* text, char* out, int64_t cap, int64_t* len);
+/* Completion time (seconds) of a valid program on a full point-to-point mesh
+   (every GPU pair linked, as xGMI connects an MI355X node): an action starts
+   once its aggregate's parts are present at its source; it aggregates them
+   locally (reads the parts, writes the aggregate, at hbm_gbs GB/s; nothing
+   when the aggregate is present whole), then sends it along each hop, one
+   transfer per destination on that pair's directed link (link_gbs GB/s).
+   Stages sharing a GPU's memory or a directed link share its bandwidth
+   equally.  An aggregate's size is its largest atom's.  Errors: EA_ERR_ARG
+   (bad arguments, or an invalid program), EA_ERR_SPEC (syntax). */
+int ea_exprog_simulate(const char* text, double link_gbs, double hbm_gbs, double* seconds);
 
 /* ---- plan cache --------------------------------------------------------- */
 /* Number of cached plans (all devices). */

@@ -1,7 +1,10 @@
 // ea_exprog.cpp -- exchange programs (Section 5.2): the ExProg text format,
 // the closure and validity of Definition "Closure; validity", memberships of
-// partitions declared by size, and the naive valid program that gathers the
-// atoms of every required aggregate at its targets (Section 5.4).
+// partitions declared by size, the naive valid program that gathers the
+// atoms of every required aggregate at its targets (Section 5.4), and a
+// simulator of a full point-to-point mesh (every GPU pair linked, as xGMI
+// connects an 8-GPU MI355X node) that gives a valid program its completion
+// time.
 #include <algorithm>
 #include <cctype>
 #include <cstdlib>
@@ -311,11 +314,17 @@ std::vector<int> sites(const Prog& p, const std::vector<Target>& ts, const std::
 }
 
 // do aggregates present at a site partition X (an exact cover by subsets)?
-bool covers(const std::set<Agg>& here, const Agg& x) {
-  if (here.count(x)) return true;
+// Larger parts are tried first; the cover found goes to *cover if given.
+bool covers(const std::set<Agg>& here, const Agg& x, std::vector<const Agg*>* cover = nullptr) {
+  if (here.count(x)) {
+    if (cover) cover->assign(1, &*here.find(x));
+    return true;
+  }
   std::vector<const Agg*> cand;
   for (const Agg& a : here)
     if (std::includes(x.begin(), x.end(), a.begin(), a.end())) cand.push_back(&a);
+  std::stable_sort(cand.begin(), cand.end(), [](const Agg* a, const Agg* b) { return a->size() > b->size(); });
+  std::vector<const Agg*> chosen;
   std::vector<char> used(x.size(), 0);
   auto pos = [&](int atom) { return (size_t)(std::lower_bound(x.begin(), x.end(), atom) - x.begin()); };
   auto rec = [&](auto&& self) -> bool {
@@ -328,12 +337,16 @@ bool covers(const std::set<Agg>& here, const Agg& x) {
       for (int at : *a) free_all &= !used[pos(at)];
       if (!free_all) continue;
       for (int at : *a) used[pos(at)] = 1;
+      chosen.push_back(a);
       if (self(self)) return true;
+      chosen.pop_back();
       for (int at : *a) used[pos(at)] = 0;
     }
     return false;
   };
-  return rec(rec);
+  const bool ok_cover = rec(rec);
+  if (ok_cover && cover) *cover = chosen;
+  return ok_cover;
 }
 
 // closure and validity for one membership of the partitions
@@ -421,10 +434,176 @@ void memberships(const Prog& p, F&& fn) {
   rec(rec, 0);
 }
 
+// Completion time of a valid program on a full mesh: dataflow semantics
+// (an action starts once its aggregate's parts are present at its source;
+// every eligible action proceeds concurrently).  An action is a pipeline of
+// stages: the local aggregation of its parts (reading them and writing the
+// aggregate at the GPU's memory bandwidth; none when the aggregate is
+// present as one piece), then each hop's transfers, one per destination,
+// each on the directed link between the two GPUs.  Stages that share a
+// resource (a GPU's memory, a directed link) share its bandwidth equally.
+// An aggregate's size is its largest atom's.
+double simulate(const Prog& p, const std::vector<std::vector<int>>& mem, double link_bps, double hbm_bps) {
+  struct Task {
+    int act, site;              // action and source site
+    int stage = 0;              // 0 aggregation, 1.. hop transfers
+    std::vector<int> from, to;  // current hop: transfers (from[i] -> to[i])
+    std::vector<double> left;   // bytes left per transfer (stage >= 1), or [0]: the aggregation
+    bool started = false, done = false;
+  };
+  std::map<int, std::set<Agg>> state;
+  for (const auto& in : p.ins) state[in.second].insert(Agg{in.first});
+  auto size_of = [&](const Agg& a) {
+    double m = 0;
+    for (int x : a) m = std::max(m, p.atom_bytes[(size_t)x]);
+    return m;
+  };
+  std::vector<Task> tasks;
+  for (size_t a = 0; a < p.acts.size(); ++a)
+    for (int s : sites(p, p.acts[a].src, mem)) {
+      Task t;
+      t.act = (int)a;
+      t.site = s;
+      tasks.push_back(t);
+    }
+  // the aggregation reads the parts of one cover (larger parts first) and
+  // writes the aggregate; nothing when it is present as one piece
+  auto parts_bytes = [&](const Agg& x, int s) {
+    if (state[s].count(x)) return 0.0;
+    std::vector<const Agg*> cover;
+    covers(state[s], x, &cover);
+    double bytes = size_of(x);
+    for (const Agg* a : cover) bytes += size_of(*a);
+    return bytes;
+  };
+  auto start_hop = [&](Task& t, int hop) {
+    const Action& act = p.acts[(size_t)t.act];
+    t.stage = hop + 1;
+    t.from.clear();
+    t.to.clear();
+    t.left.clear();
+    const std::vector<int> srcs = hop == 0 ? std::vector<int>{t.site} : sites(p, act.hops[(size_t)hop - 1], mem);
+    for (int f : srcs)
+      for (int d : sites(p, act.hops[(size_t)hop], mem))
+        if (d != f) {
+          t.from.push_back(f);
+          t.to.push_back(d);
+          t.left.push_back(size_of(act.agg));
+        }
+  };
+  double now = 0;
+  for (int guard = 0; guard < 1 << 22; ++guard) {
+    // start every eligible action
+    for (Task& t : tasks) {
+      if (t.started) continue;
+      const Action& act = p.acts[(size_t)t.act];
+      if (!covers(state[t.site], act.agg)) continue;
+      t.started = true;
+      t.stage = 0;
+      t.left = {parts_bytes(act.agg, t.site)};
+    }
+    // advance stages that have nothing left
+    bool moved = true;
+    while (moved) {
+      moved = false;
+      for (Task& t : tasks) {
+        if (!t.started || t.done) continue;
+        bool empty = true;
+        for (double b : t.left) empty &= b <= 0;
+        if (!empty) continue;
+        const Action& act = p.acts[(size_t)t.act];
+        if (t.stage == 0) state[t.site].insert(act.agg);
+        else
+          for (int d : t.to) state[d].insert(act.agg);
+        if (t.stage < (int)act.hops.size()) {
+          start_hop(t, t.stage);
+        } else {
+          t.done = true;
+        }
+        moved = true;
+      }
+    }
+    // active resource users: GPU memory (stage 0) and directed links
+    std::map<std::pair<int, int>, int> users;  // (from, to) link; (-1 - gpu, 0) memory
+    for (const Task& t : tasks) {
+      if (!t.started || t.done) continue;
+      if (t.stage == 0) {
+        if (t.left[0] > 0) ++users[{-1 - t.site, 0}];
+      } else {
+        for (size_t i = 0; i < t.to.size(); ++i)
+          if (t.left[i] > 0) ++users[{t.from[i], t.to[i]}];
+      }
+    }
+    if (users.empty()) {
+      bool all_done = true;
+      for (const Task& t : tasks) all_done &= t.done;
+      if (all_done) return now;
+      bool any_new = false;  // something may have become eligible
+      for (const Task& t : tasks)
+        if (!t.started && covers(state[t.site], p.acts[(size_t)t.act].agg)) any_new = true;
+      if (!any_new) return -1;  // stuck: not a valid program
+      continue;
+    }
+    auto rate = [&](const std::pair<int, int>& r) {
+      return (r.first < 0 ? hbm_bps : link_bps) / users[r];
+    };
+    double dt = 1e300;
+    for (const Task& t : tasks) {
+      if (!t.started || t.done) continue;
+      if (t.stage == 0) {
+        if (t.left[0] > 0) dt = std::min(dt, t.left[0] / rate({-1 - t.site, 0}));
+      } else {
+        for (size_t i = 0; i < t.to.size(); ++i)
+          if (t.left[i] > 0) dt = std::min(dt, t.left[i] / rate({t.from[i], t.to[i]}));
+      }
+    }
+    for (Task& t : tasks) {
+      if (!t.started || t.done) continue;
+      if (t.stage == 0) {
+        if (t.left[0] > 0) t.left[0] = std::max(0.0, t.left[0] - dt * rate({-1 - t.site, 0}));
+      } else {
+        for (size_t i = 0; i < t.to.size(); ++i)
+          if (t.left[i] > 0) t.left[i] = std::max(0.0, t.left[i] - dt * rate({t.from[i], t.to[i]}));
+      }
+    }
+    // finish the stage whose remainder is within rounding of zero
+    for (Task& t : tasks)
+      for (double& b : t.left)
+        if (b > 0 && b < 1e-6) b = 0;
+    now += dt;
+  }
+  return -1;
+}
+
 }  // namespace
 }  // namespace ea
 
 using namespace ea;
+
+extern "C" int ea_exprog_simulate(const char* text, double link_gbs, double hbm_gbs, double* seconds) {
+  if (!text || !seconds || !(link_gbs > 0) || !(hbm_gbs > 0)) return fail(EA_ERR_ARG, "ea_exprog_simulate: bad arguments");
+  Prog p;
+  int e = parse(text, &p);
+  if (e) return e;
+  std::vector<std::vector<int>> chosen;
+  std::string why;
+  bool found = false;
+  memberships(p, [&](const std::vector<std::vector<int>>& mem) {
+    std::string w;
+    if (check(p, mem, &w)) {
+      chosen = mem;
+      found = true;
+      return true;
+    }
+    if (why.empty()) why = w;
+    return false;
+  });
+  if (!found) return fail(EA_ERR_ARG, "ea_exprog_simulate: the program is not valid: %s", why.c_str());
+  const double t = simulate(p, chosen, link_gbs * 1e9, hbm_gbs * 1e9);
+  if (t < 0) return fail(EA_ERR_ARG, "ea_exprog_simulate: the program stalls");
+  *seconds = t;
+  return ok();
+}
 
 extern "C" int ea_exprog_check(const char* text, int32_t* valid, char* why, int64_t why_cap) {
   if (!text || !valid) return fail(EA_ERR_ARG, "ea_exprog_check: NULL argument");

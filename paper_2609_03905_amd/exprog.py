@@ -26,3 +26,16 @@ def naive(text: str) -> str:
     buf = ctypes.create_string_buffer(n.value + 1)
     ea._check(ea.lib().ea_exprog_naive(text.encode(), buf, len(buf), ctypes.byref(n)))
     return buf.value.decode()
+
+
+# MI355X node: every GPU pair on its own xGMI link (about 153 GB/s per link
+# and direction), HBM3E at about 8 TB/s
+XGMI_LINK_GBS = 153.0
+HBM_GBS = 8000.0
+
+
+def simulate(text: str, link_gbs: float = XGMI_LINK_GBS, hbm_gbs: float = HBM_GBS) -> float:
+    """Completion time in seconds of a valid program on a full xGMI mesh."""
+    t = ctypes.c_double()
+    ea._check(ea.lib().ea_exprog_simulate(text.encode(), float(link_gbs), float(hbm_gbs), ctypes.byref(t)))
+    return t.value

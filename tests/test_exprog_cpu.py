@@ -104,3 +104,49 @@ def test_checker_matches_the_literal_closure(seed):
                     actions.append((x, [s], []))
     text = _render(n_sites, ins, outs, actions)
     assert exprog.check(text)[0] == oracle.exprog_valid(ins, outs, actions), text
+
+
+# ---- the full-mesh simulator: closed forms on links of L GB/s and memory of
+# H GB/s, 1 GB atoms unless sized
+L, H = 100.0, 1000.0
+
+
+def _sim(text):
+    return exprog.simulate(text, L, H)
+
+
+def test_simulator_swap_and_doubling_closed_forms():
+    # swap: both transfers on their own links (1/L), then an aggregation of two
+    # parts at each GPU (read 2, write 1: 3/H)
+    assert _sim(EX["swap"]) == pytest.approx(1 / L + 3 / H, rel=1e-9)
+    # doubling: two rounds of (aggregate if needed, transfer), then the final
+    # aggregation of two parts: 1/L + (3/H + 1/L) + 3/H
+    assert _sim(EX["doubling"]) == pytest.approx(2 / L + 6 / H, rel=1e-9)
+
+
+def test_simulator_links_multicast_relay_and_sizes():
+    base = "IN: A @ 0; B @ 0 (size: 0.5 GB)\nOUT: A @ 1, 2, 3\n\n"
+    # a multicast uses one link per destination on a full mesh
+    assert _sim(base + "A @ 0 -> 1, 2, 3") == pytest.approx(1 / L, rel=1e-9)
+    # two transfers on one directed link share it
+    two = "IN: A @ 0; B @ 0\nOUT: A @ 1; B @ 1\n\nA @ 0 -> 1; B @ 0 -> 1"
+    assert _sim(two) == pytest.approx(2 / L, rel=1e-9)
+    # a relay is two transfers in a row; a half-size atom takes half the time
+    assert _sim("IN: A @ 0\nOUT: A @ 2\n\nA @ 0 -> 1 -> 2") == pytest.approx(2 / L, rel=1e-9)
+    assert _sim("IN: B @ 0 (size: 0.5 GB)\nOUT: B @ 1\n\nB @ 0 -> 1") == pytest.approx(0.5 / L, rel=1e-9)
+
+
+def test_simulator_topology_changes_the_best_program():
+    # on a full mesh every GPU gathers the other three atoms at once (1/L,
+    # then 4 parts read + 1 written: 5/H), faster than recursive doubling's
+    # two rounds
+    decl = EX["doubling"].split("\n\n")[0] + "\n"
+    gather = _sim(exprog.naive(decl))
+    assert gather == pytest.approx(1 / L + 5 / H, rel=1e-9)
+    assert gather < _sim(EX["doubling"])
+
+
+def test_simulator_rejects_invalid_programs():
+    with pytest.raises(ea.EAError) as e:
+        _sim("IN: A @ 0\nOUT: A @ 1\n\n")
+    assert e.value.code == -1
