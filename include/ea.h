@@ -317,6 +317,29 @@ int ea_exprog_check(const char* text, int32_t* valid, char* why, int64_t why_cap
    declarations plus that body to out (NUL-terminated; *len = its length
    without the NUL; EA_ERR_CAPACITY if cap is too small, *len still set). */
 int ea_exprog_naive(const char* text, char* out, int64_t cap, int64_t* len);
+/* Preamble of the exchange program that delivers one input of an operator
+   (Section 5.3).  The producer's output is tiled by prod_nblocks/prod_splits
+   (per dim nblocks[d] + 1 split points); its n_prod function specifications
+   each leave one unaggregated copy of output block prod_block[i] at GPU
+   prod_gpu[i].  The consumer's join-agg spec needs the input tiled by
+   cons_nblocks/cons_splits; its n_cons function specifications each read
+   block cons_block[j].  Atoms are the cells of the overlay of the two
+   tilings, numbered from 1 in row-major order.  Writes:
+     GPUS: 0, ..., n_gpus - 1
+     PARTITIONS: S1 {size 1} ... Sn {size 1}     (one per consumer specification)
+     IN:  <copy><atom> @ <gpu>; ...              (copy X, Y, Z, W, ... by the order
+                                                  of the producer specs holding it)
+     OUT: <copies of atom a, joined by +> @ <the S of every spec reading a>; ...
+   IN lists producer specs in order, each with its atoms; OUT lists atoms in
+   order.  elem_bytes > 0 adds each atom's size.  Host only.  Errors:
+   EA_ERR_ARG (bad counts or indices, n_cons != n_gpus since the size-one
+   partitions must cover the GPUs, more than 26 copies of a block),
+   EA_ERR_PARTITION (split lists that do not tile one shape), EA_ERR_CAPACITY
+   (*len still set). */
+int ea_exprog_preamble(int32_t rank, const int32_t* prod_nblocks, const int64_t* prod_splits, int32_t n_prod,
+                       const int64_t* prod_block, const int32_t* prod_gpu, const int32_t* cons_nblocks,
+                       const int64_t* cons_splits, int32_t n_cons, const int64_t* cons_block, int32_t n_gpus,
+                       int64_t elem_bytes, char* out, int64_t cap, int64_t* len);
 /* Completion time (seconds) of a valid program on a full point-to-point mesh
    (every GPU pair linked, as xGMI connects an MI355X node): an action starts
    once its aggregate's parts are present at its source; it aggregates them

@@ -8,6 +8,7 @@
 #include <algorithm>
 #include <cctype>
 #include <cstdlib>
+#include <cstdio>
 #include <cstring>
 #include <map>
 #include <set>
@@ -664,5 +665,130 @@ extern "C" int ea_exprog_naive(const char* text, char* out, int64_t cap, int64_t
     return fail(EA_ERR_CAPACITY, "ea_exprog_naive: %lld bytes needed", (long long)prog.size() + 1);
   memcpy(out, prog.data(), prog.size());
   out[prog.size()] = 0;
+  return ok();
+}
+
+extern "C" int ea_exprog_preamble(int32_t rank, const int32_t* prod_nblocks, const int64_t* prod_splits,
+                                  int32_t n_prod, const int64_t* prod_block, const int32_t* prod_gpu,
+                                  const int32_t* cons_nblocks, const int64_t* cons_splits, int32_t n_cons,
+                                  const int64_t* cons_block, int32_t n_gpus, int64_t elem_bytes, char* out,
+                                  int64_t cap, int64_t* len) {
+  if (rank < 1 || rank > kMaxRank || !prod_nblocks || !prod_splits || !cons_nblocks || !cons_splits || !len ||
+      n_prod < 1 || n_cons < 1 || n_gpus < 1 || !prod_block || !prod_gpu || !cons_block)
+    return fail(EA_ERR_ARG, "ea_exprog_preamble: bad arguments");
+  // partitions cover the GPUs (Section 5.2): one consumer specification per GPU
+  if (n_cons != n_gpus)
+    return fail(EA_ERR_ARG, "ea_exprog_preamble: %d consumer specifications for %d GPUs", n_cons, n_gpus);
+  // the two tilings and their overlay (per dim: the union of split points)
+  std::vector<std::vector<int64_t>> ps(rank), cs(rank), os(rank);
+  for (int d = 0, pi = 0, ci = 0; d < rank; ++d) {
+    if (prod_nblocks[d] < 1 || cons_nblocks[d] < 1) return fail(EA_ERR_ARG, "ea_exprog_preamble: dim %d has no blocks", d);
+    ps[d].assign(prod_splits + pi, prod_splits + pi + prod_nblocks[d] + 1);
+    cs[d].assign(cons_splits + ci, cons_splits + ci + cons_nblocks[d] + 1);
+    pi += prod_nblocks[d] + 1;
+    ci += cons_nblocks[d] + 1;
+    for (const auto* v : {&ps[d], &cs[d]})
+      for (size_t i = 0; i + 1 < v->size(); ++i)
+        if ((*v)[i] >= (*v)[i + 1] || (*v)[0] != 0) return fail(EA_ERR_PARTITION, "ea_exprog_preamble: dim %d split points", d);
+    if (ps[d].back() != cs[d].back()) return fail(EA_ERR_PARTITION, "ea_exprog_preamble: dim %d extents differ", d);
+    std::set<int64_t> u(ps[d].begin(), ps[d].end());
+    u.insert(cs[d].begin(), cs[d].end());
+    os[d].assign(u.begin(), u.end());
+  }
+  int64_t n_pblocks = 1, n_cblocks = 1, n_atoms = 1;
+  for (int d = 0; d < rank; ++d) {
+    n_pblocks *= (int64_t)ps[d].size() - 1;
+    n_cblocks *= (int64_t)cs[d].size() - 1;
+    n_atoms *= (int64_t)os[d].size() - 1;
+  }
+  // block coordinates -> the overlay cells inside, in row-major order
+  auto cells_of = [&](const std::vector<std::vector<int64_t>>& t, int64_t b) {
+    int64_t rem = b;
+    std::vector<std::pair<int64_t, int64_t>> rng(rank);  // overlay cell index range per dim
+    for (int d = rank - 1; d >= 0; --d) {
+      const int64_t n = (int64_t)t[d].size() - 1, c = rem % n;
+      rem /= n;
+      const int64_t lo = std::lower_bound(os[d].begin(), os[d].end(), t[d][c]) - os[d].begin();
+      const int64_t hi = std::lower_bound(os[d].begin(), os[d].end(), t[d][c + 1]) - os[d].begin();
+      rng[d] = {lo, hi};
+    }
+    std::vector<int64_t> out_cells;
+    std::vector<int64_t> idx(rank);
+    for (int d = 0; d < rank; ++d) idx[d] = rng[d].first;
+    while (true) {
+      int64_t a = 0;
+      for (int d = 0; d < rank; ++d) a = a * ((int64_t)os[d].size() - 1) + idx[d];
+      out_cells.push_back(a);
+      int d = rank - 1;
+      while (d >= 0 && ++idx[d] == rng[d].second) {
+        idx[d] = rng[d].first;
+        --d;
+      }
+      if (d < 0) break;
+    }
+    return out_cells;
+  };
+  auto atom_elems = [&](int64_t a) {
+    int64_t n = 1, rem = a;
+    for (int d = rank - 1; d >= 0; --d) {
+      const int64_t k = (int64_t)os[d].size() - 1, c = rem % k;
+      rem /= k;
+      n *= os[d][c + 1] - os[d][c];
+    }
+    return n;
+  };
+  // copies of every atom: (copy letter, producer spec) in spec order
+  const char* kCopy = "XYZWVUTSRQPONMLKJIHGFEDCBA";
+  std::vector<std::vector<int>> copies((size_t)n_atoms);  // producer spec indices holding a copy
+  std::vector<int> seen_per_block((size_t)n_pblocks, 0);
+  std::vector<int> copy_of_spec((size_t)n_prod);
+  for (int i = 0; i < n_prod; ++i) {
+    if (prod_block[i] < 0 || prod_block[i] >= n_pblocks || prod_gpu[i] < 0 || prod_gpu[i] >= n_gpus)
+      return fail(EA_ERR_ARG, "ea_exprog_preamble: producer spec %d: block or GPU out of range", i);
+    copy_of_spec[(size_t)i] = seen_per_block[(size_t)prod_block[i]]++;
+    if (copy_of_spec[(size_t)i] >= 26) return fail(EA_ERR_ARG, "ea_exprog_preamble: more than 26 copies of a block");
+    for (int64_t a : cells_of(ps, prod_block[i])) copies[(size_t)a].push_back(i);
+  }
+  auto name = [&](int spec, int64_t atom) { return std::string(1, kCopy[copy_of_spec[(size_t)spec]]) + std::to_string(atom + 1); };
+  std::string t = "GPUS: ";
+  for (int gi = 0; gi < n_gpus; ++gi) t += (gi ? ", " : "") + std::to_string(gi);
+  t += "\nPARTITIONS:";
+  for (int j = 0; j < n_cons; ++j) t += " S" + std::to_string(j + 1) + " {size 1}";
+  t += "\nIN: ";
+  bool first = true;
+  for (int i = 0; i < n_prod; ++i)
+    for (int64_t a : cells_of(ps, prod_block[i])) {
+      t += (first ? "" : "; ") + name(i, a) + " @ " + std::to_string(prod_gpu[i]);
+      if (elem_bytes > 0) {
+        char buf[64];
+        snprintf(buf, sizeof(buf), " (size: %.9g GB)", (double)(atom_elems(a) * elem_bytes) / 1e9);
+        t += buf;
+      }
+      first = false;
+    }
+  // the consumer specs reading each atom
+  std::vector<std::vector<int>> readers((size_t)n_atoms);
+  for (int j = 0; j < n_cons; ++j) {
+    if (cons_block[j] < 0 || cons_block[j] >= n_cblocks)
+      return fail(EA_ERR_ARG, "ea_exprog_preamble: consumer spec %d: block out of range", j);
+    for (int64_t a : cells_of(cs, cons_block[j])) readers[(size_t)a].push_back(j);
+  }
+  t += "\nOUT: ";
+  first = true;
+  for (int64_t a = 0; a < n_atoms; ++a) {
+    if (readers[(size_t)a].empty()) continue;
+    if (copies[(size_t)a].empty()) return fail(EA_ERR_ARG, "ea_exprog_preamble: atom %lld has no copy", (long long)a + 1);
+    std::string agg;
+    for (int i : copies[(size_t)a]) agg += (agg.empty() ? "" : "+") + name(i, a);
+    t += (first ? "" : "; ") + agg + " @ ";
+    for (size_t k = 0; k < readers[(size_t)a].size(); ++k)
+      t += (k ? ", S" : "S") + std::to_string(readers[(size_t)a][k] + 1);
+    first = false;
+  }
+  t += "\n";
+  *len = (int64_t)t.size();
+  if (!out || cap < (int64_t)t.size() + 1) return fail(EA_ERR_CAPACITY, "ea_exprog_preamble: %lld bytes needed", (long long)t.size() + 1);
+  memcpy(out, t.data(), t.size());
+  out[t.size()] = 0;
   return ok();
 }

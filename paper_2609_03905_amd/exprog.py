@@ -39,3 +39,29 @@ def simulate(text: str, link_gbs: float = XGMI_LINK_GBS, hbm_gbs: float = HBM_GB
     t = ctypes.c_double()
     ea._check(ea.lib().ea_exprog_simulate(text.encode(), float(link_gbs), float(hbm_gbs), ctypes.byref(t)))
     return t.value
+
+
+def preamble(prod_partition, prod_specs, cons_partition, cons_blocks, n_gpus: int, elem_bytes: int = 0) -> str:
+    """Preamble of the exchange program delivering one input (Section 5.3):
+    prod_partition / cons_partition are the producer output's and the
+    consumer's required tilings (split lists per dim); prod_specs lists the
+    producer's function specifications as (output block index, GPU);
+    cons_blocks the block each consumer specification reads."""
+    rank = len(prod_partition)
+    i32, i64 = ctypes.c_int32, ctypes.c_int64
+    arr = lambda t, xs: (t * max(1, len(xs)))(*[int(x) for x in xs])
+    pn = arr(i32, [len(sp) - 1 for sp in prod_partition])
+    psp = arr(i64, [x for sp in prod_partition for x in sp])
+    cn = arr(i32, [len(sp) - 1 for sp in cons_partition])
+    csp = arr(i64, [x for sp in cons_partition for x in sp])
+    pb = arr(i64, [b for b, _ in prod_specs])
+    pg = arr(i32, [g for _, g in prod_specs])
+    cb = arr(i64, cons_blocks)
+    n = ctypes.c_int64()
+    args = [rank, pn, psp, len(prod_specs), pb, pg, cn, csp, len(cons_blocks), cb, int(n_gpus), int(elem_bytes)]
+    rc = ea.lib().ea_exprog_preamble(*args, None, 0, ctypes.byref(n))
+    if rc not in (ea.OK, -4):
+        ea._check(rc)
+    buf = ctypes.create_string_buffer(n.value + 1)
+    ea._check(ea.lib().ea_exprog_preamble(*args, buf, len(buf), ctypes.byref(n)))
+    return buf.value.decode()

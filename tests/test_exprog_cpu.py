@@ -150,3 +150,116 @@ def test_simulator_rejects_invalid_programs():
     with pytest.raises(ea.EAError) as e:
         _sim("IN: A @ 0\nOUT: A @ 1\n\n")
     assert e.value.code == -1
+
+
+# ---- preamble generation (Section 5.3) ----------------------------------
+
+def _norm(text):
+    return " ".join(text.replace(";", " ; ").split())
+
+
+def test_preamble_matches_the_paper_example():
+    """Section 5.3, Example "Generating a preamble": the 256x256 product C of
+    the matmul example, row-split in two with F11, F12, F21, F22 on GPUs
+    0..3, consumed by a softmax over four 64-row blocks."""
+    t = exprog.preamble([[0, 128, 256], [0, 256]], [(0, 0), (0, 1), (1, 2), (1, 3)],
+                        [[0, 64, 128, 192, 256], [0, 256]], [0, 1, 2, 3], 4)
+    assert _norm(t) == _norm(EX["preamble"])
+    assert exprog.check(exprog.naive(t)) == (True, "")
+
+
+def _parse_preamble(text):
+    sec = {}
+    for line in text.strip().splitlines():
+        k, v = line.split(":", 1)
+        sec[k.strip()] = v.strip()
+    ins = {}
+    for item in filter(None, (x.strip() for x in sec["IN"].split(";"))):
+        name, rest = item.split("@")
+        gpu = rest.split("(")[0].strip()
+        size = float(rest.split("size:")[1].split("GB")[0]) if "size:" in rest else None
+        ins[name.strip()] = (int(gpu), size)
+    outs = {}
+    for item in filter(None, (x.strip() for x in sec["OUT"].split(";"))):
+        agg, dst = item.split("@")
+        outs[frozenset(agg.strip().split("+"))] = sorted(int(s.strip()[1:]) for s in dst.split(","))
+    return ins, outs
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_preamble_atoms_against_elementwise_grouping(seed):
+    """Atoms are the nonempty intersections of a producer block with a
+    consumer block; grouped element by element on a small 2-D tensor."""
+    rng = np.random.default_rng(seed)
+    shape = (int(rng.integers(3, 9)), int(rng.integers(3, 9)))
+
+    def tiling():
+        return [[0] + sorted(rng.choice(np.arange(1, n), int(rng.integers(0, min(3, n - 1) + 1)),
+                                        replace=False).tolist()) + [n] for n in shape]
+
+    pt, ct = tiling(), tiling()
+    npb = (len(pt[0]) - 1) * (len(pt[1]) - 1)
+    ncb = (len(ct[0]) - 1) * (len(ct[1]) - 1)
+    cons = [b for b in range(ncb) for _ in range(int(rng.integers(1, 3)))]
+    n_gpus = len(cons)
+    prod = [(b, int(rng.integers(0, n_gpus))) for b in range(npb) for _ in range(int(rng.integers(1, 3)))]
+    t = exprog.preamble(pt, prod, ct, cons, n_gpus, elem_bytes=4)
+    ins, outs = _parse_preamble(t)
+
+    # brute force: (producer block, consumer block) of every element
+    def block_of(tl, i, j):
+        bi = int(np.searchsorted(tl[0], i, side="right")) - 1
+        bj = int(np.searchsorted(tl[1], j, side="right")) - 1
+        return bi * (len(tl[1]) - 1) + bj
+
+    groups = {}
+    for i in range(shape[0]):
+        for j in range(shape[1]):
+            groups.setdefault((block_of(pt, i, j), block_of(ct, i, j)), []).append((i, j))
+    assert len(outs) == len(groups)
+    copies_of_block = {}
+    for s, (b, g) in enumerate(prod):
+        copies_of_block.setdefault(b, []).append((s, g))
+    letters = "XYZWVU"
+    expected_in = {}
+    for (pb, cb), cells in groups.items():
+        for c, (s, g) in enumerate(copies_of_block[pb]):
+            expected_in.setdefault(letters[c], []).append((g, len(cells) * 4 / 1e9, pb, cb))
+    # every OUT item aggregates all copies of one atom, delivered to its readers
+    matched = set()
+    for agg, dst in outs.items():
+        letters_here = sorted(a[0] for a in agg)
+        idx = {a[1:] for a in agg}
+        assert len(idx) == 1
+        atom = idx.pop()
+        gpu_size = [ins[a] for a in agg]
+        cand = [(pb, cb) for (pb, cb), cells in groups.items()
+                if len(copies_of_block[pb]) == len(agg)
+                and sorted(g for _, g in copies_of_block[pb]) == sorted(g for g, _ in gpu_size)
+                and all(abs(sz - len(cells) * 4 / 1e9) < 1e-15 for _, sz in gpu_size)
+                and dst == sorted(k + 1 for k, b in enumerate(cons) if b == cb)
+                and (pb, cb) not in matched]
+        assert cand, (agg, dst)
+        matched.add(cand[0])
+        assert letters_here == sorted(letters[:len(agg)])
+    assert len(matched) == len(groups)
+    # each copy of a producer block is cut into atoms that sum to the block
+    for s, (b, g) in enumerate(prod):
+        cells = sum(len(v) for (pb, _), v in groups.items() if pb == b)
+        assert cells > 0
+    assert sum(sz for _, sz in ins.values()) == pytest.approx(
+        sum(len(v) * 4 / 1e9 * len(copies_of_block[pb]) for (pb, _), v in groups.items()), rel=1e-12)
+    assert exprog.check(exprog.naive(t)) == (True, "")
+
+
+def test_preamble_rejects_mismatched_tilings_and_bad_indices():
+    with pytest.raises(ea.EAError):
+        exprog.preamble([[0, 4]], [(0, 0)], [[0, 5]], [0], 1)
+    with pytest.raises(ea.EAError):
+        exprog.preamble([[0, 4]], [(1, 0)], [[0, 4]], [0], 1)
+    with pytest.raises(ea.EAError):
+        exprog.preamble([[0, 4]], [(0, 2)], [[0, 4]], [0], 2)
+    with pytest.raises(ea.EAError):
+        exprog.preamble([[0, 2, 2, 4]], [(0, 0)], [[0, 4]], [0], 1)
+    with pytest.raises(ea.EAError):
+        exprog.preamble([[0, 4]], [(0, 0)], [[0, 4]], [0], 2)
