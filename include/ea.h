@@ -317,6 +317,23 @@ int ea_exprog_check(const char* text, int32_t* valid, char* why, int64_t why_cap
    declarations plus that body to out (NUL-terminated; *len = its length
    without the NUL; EA_ERR_CAPACITY if cap is too small, *len still set). */
 int ea_exprog_naive(const char* text, char* out, int64_t cap, int64_t* len);
+/* Body synthesis (Section 5.4).  Memberships of partitions declared by size
+   are fixed first: the naive program is costed under each, in lexicographic
+   order (the first 5040), and the cheapest is kept.  From its naive body, a
+   seeded simulated-annealing search applies the paper's transformations
+   (multicast fission and fusion, relay introduction and elimination,
+   aggregation pushdown and pullup, source substitution) and action
+   deletion; each candidate must be valid under Definition "Closure;
+   validity" and is costed by ea_exprog_simulate's model.  Any body in
+   text is ignored.  Writes the best program found: declarations with the
+   chosen memberships written out and atom sizes in bytes, then the body;
+   *seconds is its simulated time (never above the naive program's for that
+   membership).  Deterministic for a given seed.  Host only.  Errors:
+   EA_ERR_ARG (bad arguments, no membership under which OUT can be met),
+   EA_ERR_SPEC (a syntax error), EA_ERR_CAPACITY (*len and *seconds still
+   set). */
+int ea_exprog_synthesize(const char* text, double link_gbs, double hbm_gbs, int32_t iters, uint64_t seed, char* out,
+                         int64_t cap, int64_t* len, double* seconds);
 /* Preamble of the exchange program that delivers one input of an operator
    (Section 5.3).  The producer's output is tiled by prod_nblocks/prod_splits
    (per dim nblocks[d] + 1 split points); its n_prod function specifications

@@ -7,6 +7,8 @@
 // time.
 #include <algorithm>
 #include <cctype>
+#include <cmath>
+#include <cstdint>
 #include <cstdlib>
 #include <cstdio>
 #include <cstring>
@@ -350,8 +352,10 @@ bool covers(const std::set<Agg>& here, const Agg& x, std::vector<const Agg*>* co
   return ok_cover;
 }
 
-// closure and validity for one membership of the partitions
-bool check(const Prog& p, const std::vector<std::vector<int>>& mem, std::string* why) {
+// closure and validity for one membership of the partitions; the closure
+// goes to *closure if given
+bool check(const Prog& p, const std::vector<std::vector<int>>& mem, std::string* why,
+           std::map<int, std::set<Agg>>* closure = nullptr) {
   std::map<int, std::set<Agg>> state;
   for (const auto& in : p.ins) state[in.second].insert(Agg{in.first});
   // (action, source site) pairs; fired when enabled, to a fixed point
@@ -372,6 +376,7 @@ bool check(const Prog& p, const std::vector<std::vector<int>>& mem, std::string*
         for (int d : sites(p, hop, mem)) state[d].insert(act.agg);
     }
   }
+  if (closure) *closure = state;
   for (size_t i = 0; i < todo.size(); ++i)
     if (!fired[i]) {
       *why = "action '" + p.acts[(size_t)todo[i].first].text + "' is never enabled at site " +
@@ -576,6 +581,258 @@ double simulate(const Prog& p, const std::vector<std::vector<int>>& mem, double 
   return -1;
 }
 
+// ---- body synthesis (Section 5.4) ----------------------------------------
+// Bodies are searched with concrete sites: an action is an aggregate, one
+// source GPU and its hops' destination GPUs.
+struct FAct {
+  Agg agg;
+  int src = 0;
+  std::vector<std::vector<int>> hops;
+  bool operator==(const FAct& o) const { return agg == o.agg && src == o.src && hops == o.hops; }
+};
+
+std::string agg_name(const Prog& p, const Agg& a) {
+  std::string n;
+  for (int x : a) n += (n.empty() ? "" : "+") + p.atom_name[(size_t)x];
+  return n;
+}
+
+std::string render_act(const Prog& p, const FAct& f) {
+  std::string t = agg_name(p, f.agg) + " @ " + std::to_string(f.src);
+  for (const auto& h : f.hops) {
+    t += " ->";
+    for (size_t i = 0; i < h.size(); ++i) t += (i ? ", " : " ") + std::to_string(h[i]);
+  }
+  return t;
+}
+
+Prog with_body(const Prog& base, const std::vector<FAct>& body) {
+  Prog q = base;
+  q.acts.clear();
+  for (const FAct& f : body) {
+    Action a;
+    a.agg = f.agg;
+    a.src = {Target{false, f.src}};
+    for (const auto& h : f.hops) {
+      std::vector<Target> ts;
+      for (int d : h) ts.push_back(Target{false, d});
+      a.hops.push_back(ts);
+    }
+    a.text = render_act(base, f);
+    q.acts.push_back(a);
+  }
+  return q;
+}
+
+// the naive valid program (Section 5.4): the atoms of every required
+// aggregate go from their IN site to each target, which aggregates locally
+std::vector<FAct> naive_body(const Prog& p, const std::vector<std::vector<int>>& mem) {
+  std::vector<FAct> body;
+  auto add = [&](const FAct& f) {
+    if (std::find(body.begin(), body.end(), f) == body.end()) body.push_back(f);
+  };
+  std::vector<int> home(p.atom_name.size(), -1);
+  for (const auto& in : p.ins) home[(size_t)in.first] = in.second;
+  for (const auto& req : p.outs)
+    for (int t : sites(p, req.second, mem)) {
+      for (int a : req.first)
+        if (home[(size_t)a] != t) add(FAct{Agg{a}, home[(size_t)a], {{t}}});
+      if (req.first.size() > 1) add(FAct{req.first, t, {}});
+    }
+  return body;
+}
+
+// declarations with the memberships fixed and sizes kept exactly
+std::string render_decls(const Prog& p, const std::vector<std::vector<int>>& mem) {
+  std::string t = "GPUS: ";
+  for (size_t i = 0; i < p.gpus.size(); ++i) t += (i ? ", " : "") + std::to_string(p.gpus[i]);
+  t += "\n";
+  if (!p.parts.empty()) {
+    t += "PARTITIONS:";
+    for (size_t i = 0; i < p.parts.size(); ++i) {
+      t += " " + p.parts[i].name + " {";
+      for (size_t j = 0; j < mem[i].size(); ++j) t += (j ? ", " : "") + std::to_string(mem[i][j]);
+      t += "}";
+    }
+    t += "\n";
+  }
+  t += "IN: ";
+  for (size_t i = 0; i < p.ins.size(); ++i) {
+    char buf[64];
+    snprintf(buf, sizeof(buf), " (size: %.17g B)", p.atom_bytes[(size_t)p.ins[i].first]);
+    t += (i ? "; " : "") + p.atom_name[(size_t)p.ins[i].first] + " @ " + std::to_string(p.ins[i].second) + buf;
+  }
+  t += "\nOUT: ";
+  for (size_t i = 0; i < p.outs.size(); ++i) {
+    t += (i ? "; " : "") + agg_name(p, p.outs[i].first) + " @ ";
+    for (size_t j = 0; j < p.outs[i].second.size(); ++j) {
+      const Target& g = p.outs[i].second[j];
+      t += (j ? ", " : "") + (g.part ? p.parts[(size_t)g.id].name : std::to_string(g.id));
+    }
+  }
+  return t + "\n";
+}
+
+struct Rng {  // splitmix64
+  uint64_t s;
+  uint64_t next() {
+    uint64_t z = (s += 0x9e3779b97f4a7c15ull);
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    return z ^ (z >> 31);
+  }
+  int below(int n) { return n <= 1 ? 0 : (int)(next() % (uint64_t)n); }
+  double unit() { return (double)(next() >> 11) * (1.0 / 9007199254740992.0); }
+};
+
+// One random transformation of Section 5.4 applied to body; false when the
+// drawn move does not apply.  Validity is checked by the caller.
+bool transform(const Prog& p, const std::map<int, std::set<Agg>>& closure, std::vector<FAct>& b, Rng& rng) {
+  if (b.empty()) return false;
+  const int kind = rng.below(8);
+  const int i = rng.below((int)b.size());
+  FAct& a = b[(size_t)i];
+  const int ng = (int)p.gpus.size();
+  auto single_hop = [](const FAct& f) { return f.hops.size() == 1; };
+  switch (kind) {
+    case 0: {  // multicast fission: X @ s -> D1 u D2  =>  X @ s -> D1; X @ s -> D2
+      if (!single_hop(a) || a.hops[0].size() < 2) return false;
+      std::vector<int> d1, d2;
+      for (int d : a.hops[0]) (rng.below(2) ? d1 : d2).push_back(d);
+      if (d1.empty() || d2.empty()) return false;
+      FAct other{a.agg, a.src, {d2}};
+      a.hops[0] = d1;
+      b.push_back(other);
+      return true;
+    }
+    case 1: {  // multicast fusion (the reverse)
+      if (!single_hop(a)) return false;
+      for (size_t j = 0; j < b.size(); ++j)
+        if ((int)j != i && single_hop(b[j]) && b[j].agg == a.agg && b[j].src == a.src) {
+          for (int d : b[j].hops[0])
+            if (std::find(a.hops[0].begin(), a.hops[0].end(), d) == a.hops[0].end()) a.hops[0].push_back(d);
+          std::sort(a.hops[0].begin(), a.hops[0].end());
+          b.erase(b.begin() + (long)j);
+          return true;
+        }
+      return false;
+    }
+    case 2: {  // relay introduction: X @ s -> d  =>  X @ s -> r -> d
+      if (!single_hop(a) || ng < 3) return false;
+      const int d = a.hops[0][(size_t)rng.below((int)a.hops[0].size())];
+      const int r = p.gpus[(size_t)rng.below(ng)];
+      if (r == a.src || r == d) return false;
+      FAct relay{a.agg, a.src, {{r}, {d}}};
+      if (a.hops[0].size() == 1) {
+        a = relay;
+      } else {
+        a.hops[0].erase(std::find(a.hops[0].begin(), a.hops[0].end(), d));
+        b.push_back(relay);
+      }
+      return true;
+    }
+    case 3: {  // relay elimination: X @ s -> r -> d  =>  X @ s -> d
+      if (a.hops.size() != 2 || a.hops[0].size() != 1) return false;
+      a.hops = {a.hops[1]};
+      return true;
+    }
+    case 4: {  // aggregation pushdown: X @ r -> s; Y @ r -> s  =>  X+Y @ r -> s
+      if (!single_hop(a) || a.hops[0].size() != 1) return false;
+      for (size_t j = 0; j < b.size(); ++j) {
+        const FAct& o = b[j];
+        if ((int)j == i || !single_hop(o) || o.hops[0] != a.hops[0] || o.src != a.src) continue;
+        Agg u;
+        std::set_union(a.agg.begin(), a.agg.end(), o.agg.begin(), o.agg.end(), std::back_inserter(u));
+        if (u.size() != a.agg.size() + o.agg.size()) continue;  // not disjoint
+        a.agg = u;
+        b.erase(b.begin() + (long)j);
+        return true;
+      }
+      return false;
+    }
+    case 5: {  // aggregation pullup: X+Y @ r -> s  =>  X @ r -> s; Y @ r -> s; X+Y @ s
+      if (!single_hop(a) || a.hops[0].size() != 1 || a.agg.size() < 2) return false;
+      Agg x, y;
+      for (int at : a.agg) (rng.below(2) ? x : y).push_back(at);
+      if (x.empty() || y.empty()) return false;
+      const FAct local{a.agg, a.hops[0][0], {}};
+      const FAct fy{y, a.src, a.hops};
+      a.agg = x;
+      b.push_back(fy);
+      if (std::find(b.begin(), b.end(), local) == b.end()) b.push_back(local);
+      return true;
+    }
+    case 6: {  // source substitution: draw X from another site holding it
+      if (a.hops.empty()) return false;
+      std::vector<int> holders;
+      for (const auto& kv : closure)
+        if (kv.first != a.src && kv.second.count(a.agg)) holders.push_back(kv.first);
+      if (holders.empty()) return false;
+      const int s2 = holders[(size_t)rng.below((int)holders.size())];
+      a.src = s2;
+      for (auto& h : a.hops) h.erase(std::remove(h.begin(), h.end(), s2), h.end());
+      a.hops.erase(std::remove_if(a.hops.begin(), a.hops.end(), [](const std::vector<int>& h) { return h.empty(); }),
+                   a.hops.end());
+      return true;
+    }
+    default:  // deletion of an action (guarded by validity)
+      b.erase(b.begin() + i);
+      return true;
+  }
+}
+
+// Search from the naive program of the best membership: seeded simulated
+// annealing over the transformations, every candidate checked for validity
+// and costed by the simulator.  Returns the best cost, or -1.
+double synthesize(const Prog& p, double link_bps, double hbm_bps, int iters, uint64_t seed,
+                  std::vector<std::vector<int>>* mem_out, std::vector<FAct>* body_out) {
+  const int kMaxMemberships = 5040;
+  double best = -1;
+  int tried = 0;
+  memberships(p, [&](const std::vector<std::vector<int>>& mem) {
+    const std::vector<FAct> nb = naive_body(p, mem);
+    const Prog q = with_body(p, nb);
+    std::string why;
+    if (check(q, mem, &why)) {
+      const double c = simulate(q, mem, link_bps, hbm_bps);
+      if (c >= 0 && (best < 0 || c < best)) {
+        best = c;
+        *mem_out = mem;
+        *body_out = nb;
+      }
+    }
+    return ++tried >= kMaxMemberships;
+  });
+  if (best < 0) return -1;
+  const std::vector<std::vector<int>> mem = *mem_out;
+  Rng rng{seed};
+  std::vector<FAct> cur = *body_out;
+  double cur_cost = best;
+  std::map<int, std::set<Agg>> closure;
+  std::string why;
+  check(with_body(p, cur), mem, &why, &closure);
+  for (int it = 0; it < iters; ++it) {
+    const double temp = 0.02 * best * (1.0 - (double)it / iters);
+    std::vector<FAct> cand = cur;
+    if (!transform(p, closure, cand, rng)) continue;
+    const Prog q = with_body(p, cand);
+    std::map<int, std::set<Agg>> cl;
+    if (!check(q, mem, &why, &cl)) continue;
+    const double c = simulate(q, mem, link_bps, hbm_bps);
+    if (c < 0) continue;
+    if (c <= cur_cost || (temp > 0 && rng.unit() < std::exp((cur_cost - c) / temp))) {
+      cur = cand;
+      cur_cost = c;
+      closure = cl;
+      if (c < best - 1e-15 || (c <= best && cand.size() < body_out->size())) {
+        best = c;
+        *body_out = cand;
+      }
+    }
+  }
+  return best;
+}
+
 }  // namespace
 }  // namespace ea
 
@@ -643,26 +900,33 @@ extern "C" int ea_exprog_naive(const char* text, char* out, int64_t cap, int64_t
     return true;
   });
   std::string body;
-  std::set<std::string> seen;
-  auto emit = [&](const std::string& a) {
-    if (seen.insert(a).second) body += a + "\n";
-  };
-  std::vector<int> home(p.atom_name.size(), -1);
-  for (const auto& in : p.ins) home[(size_t)in.first] = in.second;
-  for (const auto& req : p.outs) {
-    std::string name;
-    for (int a : req.first) name += (name.empty() ? "" : "+") + p.atom_name[(size_t)a];
-    for (int t : sites(p, req.second, first)) {
-      for (int a : req.first)
-        if (home[(size_t)a] != t)
-          emit(p.atom_name[(size_t)a] + " @ " + std::to_string(home[(size_t)a]) + " -> " + std::to_string(t));
-      if (req.first.size() > 1) emit(name + " @ " + std::to_string(t));
-    }
-  }
+  for (const FAct& f : naive_body(p, first)) body += render_act(p, f) + "\n";
   const std::string prog = p.decl_text + "\n" + body;
   *len = (int64_t)prog.size();
   if (!out || cap < (int64_t)prog.size() + 1)
     return fail(EA_ERR_CAPACITY, "ea_exprog_naive: %lld bytes needed", (long long)prog.size() + 1);
+  memcpy(out, prog.data(), prog.size());
+  out[prog.size()] = 0;
+  return ok();
+}
+
+extern "C" int ea_exprog_synthesize(const char* text, double link_gbs, double hbm_gbs, int32_t iters, uint64_t seed,
+                                    char* out, int64_t cap, int64_t* len, double* seconds) {
+  if (!text || !len || !seconds || !(link_gbs > 0) || !(hbm_gbs > 0) || iters < 0)
+    return fail(EA_ERR_ARG, "ea_exprog_synthesize: bad arguments");
+  Prog p;
+  int e = parse(text, &p);
+  if (e) return e;
+  std::vector<std::vector<int>> mem;
+  std::vector<FAct> body;
+  const double t = synthesize(p, link_gbs * 1e9, hbm_gbs * 1e9, iters, seed, &mem, &body);
+  if (t < 0) return fail(EA_ERR_ARG, "ea_exprog_synthesize: no membership admits the naive program");
+  std::string prog = render_decls(p, mem) + "\n";
+  for (const FAct& f : body) prog += render_act(p, f) + "\n";
+  *len = (int64_t)prog.size();
+  *seconds = t;
+  if (!out || cap < (int64_t)prog.size() + 1)
+    return fail(EA_ERR_CAPACITY, "ea_exprog_synthesize: %lld bytes needed", (long long)prog.size() + 1);
   memcpy(out, prog.data(), prog.size());
   out[prog.size()] = 0;
   return ok();

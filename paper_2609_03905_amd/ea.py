@@ -72,6 +72,8 @@ def lib() -> ctypes.CDLL:
         L.ea_exprog_check.argtypes = [ctypes.c_char_p, P(i32), ctypes.c_char_p, i64]
         L.ea_exprog_naive.argtypes = [ctypes.c_char_p, ctypes.c_char_p, i64, P(i64)]
         L.ea_exprog_simulate.argtypes = [ctypes.c_char_p, ctypes.c_double, ctypes.c_double, P(ctypes.c_double)]
+        L.ea_exprog_synthesize.argtypes = [ctypes.c_char_p, ctypes.c_double, ctypes.c_double, i32, ctypes.c_uint64,
+                                           ctypes.c_char_p, i64, P(i64), P(ctypes.c_double)]
         L.ea_exprog_preamble.argtypes = [i32, P(i32), P(i64), i32, P(i64), P(i32), P(i32), P(i64), i32, P(i64), i32,
                                          i64, ctypes.c_char_p, i64, P(i64)]
         L.ea_plan_cache_size.restype = i64

@@ -65,3 +65,20 @@ def preamble(prod_partition, prod_specs, cons_partition, cons_blocks, n_gpus: in
     buf = ctypes.create_string_buffer(n.value + 1)
     ea._check(ea.lib().ea_exprog_preamble(*args, buf, len(buf), ctypes.byref(n)))
     return buf.value.decode()
+
+
+def synthesize(text: str, link_gbs: float = XGMI_LINK_GBS, hbm_gbs: float = HBM_GBS, iters: int = 2000,
+               seed: int = 0):
+    """Body synthesis (Section 5.4) for the declarations in text: returns
+    (program, simulated seconds).  The search starts from the naive program
+    under the cheapest membership and applies the paper's transformations,
+    keeping only valid programs."""
+    n = ctypes.c_int64()
+    t = ctypes.c_double()
+    args = [text.encode(), float(link_gbs), float(hbm_gbs), int(iters), int(seed) & (2**64 - 1)]
+    rc = ea.lib().ea_exprog_synthesize(*args, None, 0, ctypes.byref(n), ctypes.byref(t))
+    if rc not in (ea.OK, -4):
+        ea._check(rc)
+    buf = ctypes.create_string_buffer(n.value + 1)
+    ea._check(ea.lib().ea_exprog_synthesize(*args, buf, len(buf), ctypes.byref(n), ctypes.byref(t)))
+    return buf.value.decode(), t.value

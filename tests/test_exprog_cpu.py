@@ -4,6 +4,7 @@ action they need is removed; the preamble of Example "Generating a preamble"
 needs a body, which the naive program provides; the native checker agrees
 with the oracle's literal closure on random programs."""
 import json
+import re
 import os
 
 import numpy as np
@@ -263,3 +264,109 @@ def test_preamble_rejects_mismatched_tilings_and_bad_indices():
         exprog.preamble([[0, 2, 2, 4]], [(0, 0)], [[0, 4]], [0], 1)
     with pytest.raises(ea.EAError):
         exprog.preamble([[0, 4]], [(0, 0)], [[0, 4]], [0], 2)
+
+
+# ---- body synthesis (Section 5.4) ----------------------------------------
+
+def _parse_concrete(text):
+    """A synthesized program (memberships written out, concrete sites in the
+    body) as the oracle's (ins, outs, actions)."""
+    decl, body = text.split("\n\n", 1)
+    sec = {}
+    for line in decl.splitlines():
+        k, v = line.split(":", 1)
+        sec[k.strip()] = v
+    parts = {}
+    for name, members in re.findall(r"(\w+)\s*\{([^}]*)\}", sec.get("PARTITIONS", "")):
+        parts[name] = [int(m) for m in members.split(",")]
+
+    def sites(s):
+        out = []
+        for tok in s.split(","):
+            tok = tok.strip()
+            out += parts[tok] if tok in parts else [int(tok)]
+        return out
+
+    ins = [(a.split("@")[0].strip(), int(a.split("@")[1].split("(")[0])) for a in sec["IN"].split(";")]
+    outs = [(tuple(o.split("@")[0].strip().split("+")), sites(o.split("@")[1])) for o in sec["OUT"].split(";")]
+    acts = []
+    for line in filter(None, (x.strip() for x in body.splitlines())):
+        hops = line.split("->")
+        agg, src = hops[0].split("@")
+        acts.append((tuple(agg.strip().split("+")), sites(src), [sites(h) for h in hops[1:]]))
+    return ins, outs, acts
+
+
+def _synth_ok(decl, iters=1500, seed=0):
+    prog, t = exprog.synthesize(decl, L, H, iters=iters, seed=seed)
+    assert exprog.check(prog) == (True, "")
+    assert oracle.exprog_valid(*_parse_concrete(prog))
+    # the written program reproduces the reported time
+    assert _sim(prog) == pytest.approx(t, rel=1e-12)
+    return prog, t
+
+
+def test_synthesis_relays_around_one_contended_link():
+    """Four 1 GB atoms from GPU 0 to GPU 1 on a 4-GPU mesh.  The naive body
+    shares link 0->1 (4/L).  GPU 1 has three incoming links for 4 GB, so some
+    link carries 2 GB and 2/L is a lower bound; two relays reach it."""
+    decl = "GPUS: 0, 1, 2, 3\nIN: A @ 0; B @ 0; C @ 0; D @ 0\nOUT: A @ 1; B @ 1; C @ 1; D @ 1\n"
+    assert _sim(exprog.naive(decl)) == pytest.approx(4 / L, rel=1e-9)
+    prog, t = _synth_ok(decl)
+    assert t == pytest.approx(2 / L, rel=1e-9)
+    assert any(line.count("->") == 2 for line in prog.splitlines())
+
+
+def test_synthesis_pushes_aggregation_below_the_transfer():
+    """X+Y required at GPU 1 with X and Y at GPU 0 and no relay: the naive
+    body sends both (2/L) then aggregates (3/H).  GPU 1 must receive at least
+    one aggregate-sized piece and somebody must aggregate, so 1/L + 3/H is a
+    lower bound; aggregation pushdown reaches it."""
+    decl = "GPUS: 0, 1\nIN: X @ 0; Y @ 0\nOUT: X+Y @ 1\n"
+    assert _sim(exprog.naive(decl)) == pytest.approx(2 / L + 3 / H, rel=1e-9)
+    prog, t = _synth_ok(decl)
+    assert t == pytest.approx(1 / L + 3 / H, rel=1e-9)
+    assert "X+Y @ 0 -> 1" in prog
+
+
+def test_synthesis_chooses_the_memberships_of_the_paper_preamble():
+    """Section 5.3's preamble: each S_j must sit at a GPU holding one copy of
+    its atom (GPUs 0, 1 for atoms 1, 2; GPUs 2, 3 for atoms 3, 4), receive the
+    other copy (1/L) and aggregate two parts (3/H), the lower bound."""
+    prog, t = _synth_ok(EX["preamble"])
+    assert t == pytest.approx(1 / L + 3 / H, rel=1e-9)
+    members = dict(re.findall(r"(S\d)\s*\{(\d+)\}", prog))
+    assert {members["S1"], members["S2"]} == {"0", "1"}
+    assert {members["S3"], members["S4"]} == {"2", "3"}
+
+
+@pytest.mark.parametrize("name", ["swap", "doubling", "v100"])
+def test_synthesis_never_worse_than_naive_on_the_paper_examples(name):
+    decl = EX[name].split("\n\n")[0] + "\n"
+    _, t = _synth_ok(decl)
+    assert t <= _sim(exprog.naive(decl)) * (1 + 1e-12)
+    # deterministic for a seed
+    assert exprog.synthesize(decl, L, H, iters=300, seed=7) == exprog.synthesize(decl, L, H, iters=300, seed=7)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_synthesis_on_random_preambles(seed):
+    """Random exchange problems (atoms of random sizes at random GPUs,
+    aggregates required at random sites): every program the search returns is
+    valid under the oracle's literal closure and no slower than the naive
+    body under the same memberships."""
+    rng = np.random.default_rng(100 + seed)
+    n_gpus = int(rng.integers(2, 6))
+    n_atoms = int(rng.integers(1, 6))
+    ins = [(f"A{i}", int(rng.integers(0, n_gpus)), float(rng.choice([0.25, 0.5, 1.0, 2.0]))) for i in range(n_atoms)]
+    outs = []
+    for _ in range(int(rng.integers(1, 4))):
+        k = int(rng.integers(1, n_atoms + 1))
+        atoms = sorted(rng.choice(n_atoms, k, replace=False).tolist())
+        dst = sorted(rng.choice(n_gpus, int(rng.integers(1, n_gpus + 1)), replace=False).tolist())
+        outs.append(("+".join(f"A{a}" for a in atoms), dst))
+    decl = ("GPUS: " + ", ".join(map(str, range(n_gpus))) + "\nIN: "
+            + "; ".join(f"{a} @ {g} (size: {s} GB)" for a, g, s in ins) + "\nOUT: "
+            + "; ".join(f"{x} @ " + ", ".join(map(str, d)) for x, d in outs) + "\n")
+    prog, t = _synth_ok(decl, iters=800, seed=seed)
+    assert t <= _sim(exprog.naive(decl)) * (1 + 1e-12)
