@@ -10,22 +10,23 @@
 // in ascending key-block order.
 //
 // Work unit = (group, 128-row query tile, a run of the group's tuples).  A
-// workgroup is 4 waves x 32 query rows; two workgroups share a CU, so one's
-// loads overlap the other's MFMAs.  Per 128-key chunk:
+// workgroup holds two groups of 4 waves x 32 query rows; one group's loads
+// overlap the other's MFMAs.  Per 64-key chunk:
 //   * K and V chunks [key][d] (bf16, 256-byte rows) go straight from global
 //     memory into LDS (global_load_lds_dwordx4), their 16-byte chunks
 //     XOR-swizzled per key row so that the fragment reads below spread over
-//     all banks;
+//     all banks; each wave then converts the V pieces it loaded to fp16 in
+//     place (exact for values in fp16's normal range);
 //   * S^T = K Q^T on bf16 MFMA 32x32x16 (Q^T from registers), so each lane
 //     holds the scores of one query: the row max and sum need one exchange
 //     between lanes l and l^32;
 //   * the scale (log2 domain) is one FMA ahead of exp2; the causal mask is
 //     applied only on chunks that reach past a query of the wave;
-//   * P = 2^(S - m) is carried as a bf16 pair P_hi + P_lo (about 16
-//     significant bits) and O^T += V^T P_hi^T + V^T P_lo^T runs on bf16 MFMA;
-//     the V^T operand (8 keys of one d per lane) comes from two transposing
-//     LDS reads (ds_read_b64_tr_b16) of the [key][d] chunk, with the MFMA's k
-//     order matched to the accumulator layout of S^T.
+//   * P = 2^(S - m), in [0, 1], is rounded to fp16 and O^T += V^T P^T runs
+//     on fp16 MFMA 32x32x16; the V^T operand (8 keys of one d per lane)
+//     comes from two transposing LDS reads (ds_read_b64_tr_b16) of the
+//     [key][d] chunk, with the MFMA's k order matched to the accumulator
+//     layout of S^T.
 // A group whose tuples are split across units writes partial (m, l, O) to the
 // plan's scratch; the last unit to arrive (device-scope counter, no waiting)
 // merges the partials in tuple order and stores the output block rows.
