@@ -40,20 +40,44 @@ METRIC = "join-agg TFLOP/s (%MFMA peak), norm/repartition GB/s (%HBM), ms per LL
 
 
 def _events_ms(fn, n, warm=3):
-    """Average duration of fn() over n back-to-back launches, measured with
-    HIP events on the current stream (the stream libea launches on)."""
+    """Average GPU duration of fn() over n back-to-back launches, measured
+    with HIP events on the current stream (the stream libea launches on).
+    The launches are queued behind a bounded spin kernel, so the events see
+    them run back to back even where one host call takes longer than its
+    kernel; the spin is doubled until the start event is still pending once
+    every launch is queued."""
     import torch
 
     for _ in range(warm):
         fn()
-    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    spin = 1 << 22
+    for _ in range(6):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        torch.cuda._sleep(spin)
+        s.record()
+        for _ in range(n):
+            fn()
+        e.record()
+        queued_in_time = not s.query()
+        e.synchronize()
+        if queued_in_time:
+            break
+        spin *= 2
+    return s.elapsed_time(e) / n
+
+
+def _host_us_per_call(fn, n):
+    """Host time of one call of fn() (marshalling, plan lookup, launch)."""
+    import torch
+
     torch.cuda.synchronize()
-    s.record()
+    t0 = time.perf_counter()
     for _ in range(n):
         fn()
-    e.record()
-    e.synchronize()
-    return s.elapsed_time(e) / n
+    t = (time.perf_counter() - t0) / n * 1e6
+    torch.cuda.synchronize()
+    return t
 
 
 def _profiled_traffic(kernel: str):
@@ -424,7 +448,7 @@ def main():
     comps = {}
     for name, c in wl["comps"].items():
         ms = _events_ms(c["fn"], max(args.steps, 20))
-        d = {"ms": round(ms, 5)}
+        d = {"ms": round(ms, 5), "host_us": round(_host_us_per_call(c["fn"], 20), 2)}
         if "flops" in c:
             d["tflops"] = c["flops"] / ms / 1e9
             d["frac_mfma_peak"] = d["tflops"] / PEAK_BF16_TFLOPS
