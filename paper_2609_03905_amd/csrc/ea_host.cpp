@@ -943,6 +943,12 @@ int build_rows(const Spec& sp, const ea_relation* const* ops, const OpInfo& oi, 
       tasks.push_back(t);
     }
   }
+  // causal softmax: a row's loads grow with its query position, so the
+  // longest rows go first and the shortest fill the tail
+  if (oi.kind == K_SOFTMAX && oi.causal && qd >= 0)
+    std::stable_sort(tasks.begin(), tasks.end(), [](const RowTask& a, const RowTask& b) {
+      return (int64_t)a.qlo + a.row0 % std::max(a.qext, 1) > (int64_t)b.qlo + b.row0 % std::max(b.qext, 1);
+    });
   ex->work = img->put_vec(tasks);
   ex->n_work = (int64_t)tasks.size();
   return EA_OK;
