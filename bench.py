@@ -1,6 +1,6 @@
 """Throughput of one GPU's share of the block join-agg hot path on MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload block|qkv|attention|reductions|repartition]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload block|qkv|attention|packed_gqa|reductions|repartition|w1_block|w1_1k|w1_8k|w1_128k|w1_128x1k|chains]
 
 Default workload "block": one GPU's share of a LLaMA-65B-shape transformer
 block (hidden 8192, 8 of 64 heads of dim 128, SwiGLU FFN 2752 = 22016/8,
@@ -243,11 +243,13 @@ def packed_gqa_workload():
                         "causal": True, "dtype": "bf16", "buffer_sets": len(rot.sets)}, cpu=None)
 
 
-def w1_block_workload():
+def w1_block_workload(t=8192, seq_len=1024):
+    """One GPU's 8-way head share of the paper's W1 block on t tokens packed
+    as sequences of seq_len (seq_len == t: one sequence)."""
     import synth
     from paper_2609_03905_amd.block import LlamaBlockShare
 
-    w = synth.w1_block()
+    w = synth.w1_block(t=t, seq_len=seq_len)
     blk = LlamaBlockShare(w["t"], w["hidden"], w["heads"], w["d_head"], w["ffn"], block=w["block"], eps=w["eps"],
                           heads_kv=w["heads_kv"], seq_ends=w["seq_ends"])
     blk.load({k: _dev(w[k]) for k in ("x", "n1", "n2", "wqkv", "wo", "wg", "wu", "wd")})
@@ -255,9 +257,13 @@ def w1_block_workload():
     stages = blk.stages()
     comps = {name: dict(fn=fn, **work[name]) for name, fn in stages}
     flops = sum(c.get("flops", 0) for c in comps.values())
-    return dict(step=blk.forward, flops=flops, comps=comps, dominant="swiglu_gemm",
-                config={"workload": "w1_block_share", "hidden": 4096, "heads_q": "4 of 32", "heads_kv": "1 of 8",
-                        "d_head": 128, "ffn": "1792 of 14336", "tokens": 8192, "sequences": "8 x 1024 packed",
+    n_seq = t // seq_len
+    dominant = max(("swiglu_gemm", "attention"), key=lambda k: comps[k]["flops"])
+    name = "w1_block_share" if (t, seq_len) == (8192, 1024) else f"w1_block_share_{n_seq}x{seq_len}"
+    return dict(step=blk.forward, flops=flops, comps=comps, dominant=dominant,
+                config={"workload": name, "hidden": 4096, "heads_q": "4 of 32", "heads_kv": "1 of 8",
+                        "d_head": 128, "ffn": "1792 of 14336", "tokens": t,
+                        "sequences": f"{n_seq} x {seq_len} packed" if n_seq > 1 else f"one of {seq_len}",
                         "block": 512, "dtype": "bf16", "chain": [n for n, _ in stages]},
                 cpu=None)
 
@@ -409,7 +415,9 @@ def cpu_baseline_qkv(target_s: float = 12.0):
 
 
 WORKLOADS = {"block": block_workload, "qkv": qkv_workload, "attention": attention_workload,
-             "packed_gqa": packed_gqa_workload, "w1_block": w1_block_workload, "chains": chains_workload,
+             "packed_gqa": packed_gqa_workload, "w1_block": w1_block_workload, "w1_1k": lambda: w1_block_workload(1024, 1024),
+             "w1_8k": lambda: w1_block_workload(8192, 8192), "w1_128k": lambda: w1_block_workload(131072, 131072),
+             "w1_128x1k": lambda: w1_block_workload(131072, 1024), "chains": chains_workload,
              "reductions": reductions_workload,
              "repartition": repartition_workload}
 

@@ -370,6 +370,50 @@ def llama_block(x, n1, wqkv, wo, wg, wu, wd, n2, heads: int, d_head: int, eps: f
     return dict(h1=h1, qkv=qkv, attn=attn, x2=x2, h2=h2, a=a, y=y)
 
 
+def llama_block_rows(x, n1, wqkv, wo, wg, wu, wd, n2, heads: int, d_head: int, eps: float, rows,
+                     heads_kv: int | None = None, seq_ends=None):
+    """Rows `rows` of llama_block's boundary relations, for sequences too long
+    for the whole chain in fp64 on the CPU.  h1 and qkv are computed for the
+    tokens the rows read (from the start of the earliest row's sequence to
+    the last row).  Attention is then evaluated only at the sampled query
+    rows: query t of head h takes the softmax of its scaled scores against
+    the keys of key/value head h // (heads // heads_kv) from the start of
+    its sequence through t, and returns the weighted sum of their values
+    (Section 3.2, Example "Flash attention"; the per-row formula that
+    attention_ex evaluates at every row).  The remaining stages are
+    row-wise.  The same bf16 rounding is applied at every relation boundary.
+    Returns a dict of [len(rows), ...] fp64 arrays, rows in ascending order."""
+    r = rne_bf16
+    x = _f64(x)
+    T = x.shape[0]
+    hkv = heads if heads_kv is None else heads_kv
+    group = heads // hkv
+    hd, kvd = heads * d_head, hkv * d_head
+    ends = np.asarray(seq_ends if seq_ends is not None else [T], dtype=np.int64)
+    rows = np.unique(np.asarray(rows, dtype=np.int64))
+    starts = np.array([int(ends[ends <= t].max()) if np.any(ends <= t) else 0 for t in rows], dtype=np.int64)
+    lo, hi = int(starts.min()), int(rows.max()) + 1
+    h1 = r(rmsnorm(x[lo:hi], n1, eps))
+    qkv = r(matmul(h1, wqkv))
+    scale = 1.0 / np.sqrt(d_head)
+    o = np.empty((len(rows), hd))
+    for i, (t, s0) in enumerate(zip(rows, starts)):
+        for h in range(heads):
+            m = h // group
+            qv = qkv[t - lo, h * d_head:(h + 1) * d_head]
+            kk = qkv[s0 - lo:t - lo + 1, hd + m * d_head:hd + (m + 1) * d_head]
+            vv = qkv[s0 - lo:t - lo + 1, hd + kvd + m * d_head:hd + kvd + (m + 1) * d_head]
+            sc = (kk @ qv) * scale
+            pr = np.exp(sc - sc.max())
+            o[i, h * d_head:(h + 1) * d_head] = (pr @ vv) / pr.sum()
+    attn = r(o)
+    x2 = r(add(x[rows], matmul(attn, wo)))
+    h2 = r(rmsnorm(x2, n2, eps))
+    a = r(silu_mul(matmul(h2, wg), matmul(h2, wu)))
+    y = r(add(x2, matmul(a, wd)))
+    return dict(h1=h1[rows - lo], qkv=qkv[rows - lo], attn=attn, x2=x2, h2=h2, a=a, y=y)
+
+
 # --------------------------------------------------------------------------
 # logical optimization (Section 4): brute force over every combination of
 # join-agg specs, pure Python (small cases only)

@@ -7,7 +7,7 @@ import torch
 
 import oracle
 import synth
-from helpers import assert_close, values
+from helpers import assert_close, download, values
 from paper_2609_03905_amd.block import LlamaBlockShare
 
 pytestmark = pytest.mark.gpu
@@ -109,3 +109,80 @@ def test_w1_block_share_full_size():
     ref = _oracle_w1(w)
     for name in ("h1", "qkv", "attn", "x2", "h2", "a", "y"):
         assert_close(values(getattr(blk, name)), ref[name], rel_fro=CHAIN_REL_FRO, what=name)
+
+
+# ---- the other W1 token workloads: single 1K, 8K and 128K sequences, and
+# 128 packed 1K sequences (4 of 32 query heads over 1 of 8 key/value heads,
+# FFN 1792 of 14336, d 4096)
+
+_W1_INPUTS = {}
+
+
+def _w1(t, seq_ends):
+    if t not in _W1_INPUTS:
+        _W1_INPUTS.clear()
+        _W1_INPUTS[t] = synth.w1_block(t=t)
+    w = dict(_W1_INPUTS[t])
+    w["seq_ends"] = list(seq_ends)
+    return w
+
+
+def _rows_f64(rel, rows):
+    return synth.to_f64(download(rel)[rows], rel.dtype)
+
+
+def _check_w1_rows(w, rows):
+    blk = _run_w1(w)
+    f = {k: synth.to_f64(w[k], "bf16") for k in ("x", "n1", "wqkv", "wo", "wg", "wu", "wd", "n2")}
+    ref = oracle.llama_block_rows(f["x"], f["n1"], f["wqkv"], f["wo"], f["wg"], f["wu"], f["wd"], f["n2"],
+                                  heads=w["heads"], d_head=w["d_head"], eps=w["eps"], rows=rows,
+                                  heads_kv=w["heads_kv"], seq_ends=w["seq_ends"])
+    rows = np.unique(np.asarray(rows))
+    for name in ("h1", "qkv", "attn", "x2", "h2", "a", "y"):
+        assert_close(_rows_f64(getattr(blk, name), rows), ref[name], rel_fro=CHAIN_REL_FRO, what=name)
+    return blk
+
+
+def test_w1_block_single_1k_sequence():
+    w = _w1(1024, [1024])
+    blk = _run_w1(w)
+    ref = _oracle_w1(w)
+    for name in ("h1", "qkv", "attn", "x2", "h2", "a", "y"):
+        assert_close(values(getattr(blk, name)), ref[name], rel_fro=CHAIN_REL_FRO, what=name)
+
+
+def _sample_rows(t, seed, extra):
+    rng = np.random.default_rng(seed)
+    return sorted(set(extra) | set(rng.integers(0, t, 24).tolist()))
+
+
+def test_w1_block_single_8k_sequence_sampled_rows():
+    print("w1 8K single sequence", flush=True)
+    _check_w1_rows(_w1(8192, [8192]), _sample_rows(8192, 81, [0, 1, 127, 128, 511, 512, 4095, 8190, 8191]))
+
+
+def test_w1_block_single_128k_sequence_sampled_rows():
+    # 131072 tokens: activations of 1 GiB per [T, 4096] relation; rows late in
+    # the sequence attend over up to 128K keys (1024 key blocks per query tile)
+    print("w1 128K single sequence", flush=True)
+    t = 131072
+    _check_w1_rows(_w1(t, [t]), _sample_rows(t, 128, [0, 511, 512, 65535, 65536, t - 129, t - 128, t - 1]))
+
+
+def test_w1_block_128_packed_1k_sequences_sampled_sequences():
+    # 128 packed 1K sequences: rows of a sequence equal the block run on that
+    # sequence alone, so three whole sequences are checked against the oracle
+    print("w1 128 x 1K packed sequences", flush=True)
+    t = 131072
+    w = _w1(t, range(1024, t + 1, 1024))
+    blk = _run_w1(w)
+    f = {k: synth.to_f64(w[k], "bf16") for k in ("n1", "wqkv", "wo", "wg", "wu", "wd", "n2")}
+    for j in (0, 77, 127):
+        rows = np.arange(j * 1024, (j + 1) * 1024)
+        x = synth.to_f64(w["x"][rows], "bf16")
+        ref = oracle.llama_block(x, f["n1"], f["wqkv"], f["wo"], f["wg"], f["wu"], f["wd"], f["n2"],
+                                 heads=w["heads"], d_head=w["d_head"], eps=w["eps"], heads_kv=w["heads_kv"],
+                                 seq_ends=[1024])
+        for name in ("h1", "qkv", "attn", "x2", "h2", "a", "y"):
+            assert_close(_rows_f64(getattr(blk, name), rows), ref[name], rel_fro=CHAIN_REL_FRO,
+                         what=f"sequence {j} {name}")

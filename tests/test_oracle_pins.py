@@ -471,3 +471,30 @@ def test_llama_block_grouped_heads_and_packed_sequences():
     first = oracle.llama_block(f["x"][:20], f["n1"], wqkv, *rest, heads=4, d_head=16, eps=1e-6, heads_kv=2,
                                seq_ends=[20])
     np.testing.assert_array_equal(packed["y"][:20], first["y"])
+
+
+@pytest.mark.parametrize("seq_ends", [None, [20, 48], [7, 31, 48]])
+def test_llama_block_rows_equals_the_whole_chain_at_its_rows(seq_ends):
+    # the sampled-rows block (attention written out per query row) against the
+    # whole-chain oracle at the same rows, grouped heads, packed or single
+    # sequence; boundaries round to bf16 on both sides, so an element may
+    # differ by one bf16 step where fp64 summation order moves a value across
+    # a rounding boundary
+    w = synth.llama_block(t=48, hidden=64, heads=4, d_head=16, ffn=40)
+    f = {k: synth.to_f64(w[k], "bf16") for k in ("x", "wqkv", "wo", "wg", "wu", "wd", "n1", "n2")}
+    wqkv = f["wqkv"][:, :4 * 16 + 2 * 2 * 16]
+    args = (f["x"], f["n1"], wqkv, f["wo"], f["wg"], f["wu"], f["wd"], f["n2"])
+    full = oracle.llama_block(*args, heads=4, d_head=16, eps=1e-6, heads_kv=2, seq_ends=seq_ends)
+    rows = [0, 5, 19, 20, 21, 33, 47]
+    part = oracle.llama_block_rows(*args, heads=4, d_head=16, eps=1e-6, rows=rows, heads_kv=2, seq_ends=seq_ends)
+    for name in ("h1", "qkv", "attn", "x2", "h2", "a", "y"):
+        ref = full[name][rows]
+        got = part[name]
+        assert got.shape == ref.shape
+        close = np.isclose(got, ref, rtol=2.0 ** -7, atol=1e-30)
+        assert close.all(), name
+        assert np.mean(got == ref) > 0.98, name
+    if seq_ends is None:
+        # a history shifted by one token changes the row: the comparison can fail
+        bad = oracle.llama_block_rows(f["x"][1:], *args[1:], heads=4, d_head=16, eps=1e-6, rows=[10], heads_kv=2)
+        assert not np.allclose(bad["attn"], full["attn"][[10]])
