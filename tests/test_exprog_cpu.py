@@ -3,6 +3,7 @@ are valid under Definition "Closure; validity" and stop being valid when an
 action they need is removed; the preamble of Example "Generating a preamble"
 needs a body, which the naive program provides; the native checker agrees
 with the oracle's literal closure on random programs."""
+import ctypes
 import json
 import re
 import os
@@ -370,3 +371,24 @@ def test_synthesis_on_random_preambles(seed):
             + "; ".join(f"{x} @ " + ", ".join(map(str, d)) for x, d in outs) + "\n")
     prog, t = _synth_ok(decl, iters=800, seed=seed)
     assert t <= _sim(exprog.naive(decl)) * (1 + 1e-12)
+
+
+def test_synthesis_argument_and_capacity_errors():
+    decl = "GPUS: 0, 1\nIN: A @ 0\nOUT: A @ 1\n"
+    with pytest.raises(ea.EAError) as e:
+        exprog.synthesize(decl, 0.0, H)
+    assert e.value.code == -1
+    with pytest.raises(ea.EAError) as e:
+        exprog.synthesize(decl, L, H, iters=-1)
+    assert e.value.code == -1
+    with pytest.raises(ea.EAError) as e:
+        exprog.synthesize("GPUS: 0, 1\nIN: A @ 0\nOUT: A @ 7\n", L, H)
+    assert e.value.code == -5  # site 7 is not among the GPUS
+    # zero iterations return the naive program under the best membership
+    prog, t = exprog.synthesize(decl, L, H, iters=0)
+    assert t == pytest.approx(1 / L, rel=1e-9) and "A @ 0 -> 1" in prog
+    # the capacity error still reports the needed length
+    n = ctypes.c_int64()
+    sec = ctypes.c_double()
+    rc = ea.lib().ea_exprog_synthesize(decl.encode(), L, H, 0, 0, None, 0, ctypes.byref(n), ctypes.byref(sec))
+    assert rc == -4 and n.value == len(prog) and sec.value == pytest.approx(t)
