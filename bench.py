@@ -364,20 +364,18 @@ def repartition_workload():
 # ---------------------------------------------------------------------------
 def _adaptive(run, first, cap, target_s):
     """Grow the sample (rows of the workload) until one run takes about a
-    third of target_s, or the whole workload; if the whole workload is
-    faster than that, repeat it until about 10 s are spent.  Returns (rows,
-    repetitions, seconds of the timed repetitions)."""
+    third of target_s, or the whole workload; then time as many runs of it
+    as cover at least 10 s.  Returns (rows, repetitions, seconds of the
+    timed repetitions)."""
     n = first
     while True:
         t0 = time.perf_counter()
         run(n)
         dt = time.perf_counter() - t0
-        if dt >= target_s / 3:
-            return n, 1, dt
-        if n >= cap:
+        if dt >= target_s / 3 or n >= cap:
             break
         n = min(cap, max(2 * n, int(n * target_s / 3 / max(dt, 1e-3))))
-    reps = max(1, int(10.0 / max(dt, 1e-3)))
+    reps = max(1, -int(-10.0 // max(dt, 1e-3)))
     t0 = time.perf_counter()
     for _ in range(reps):
         run(n)
