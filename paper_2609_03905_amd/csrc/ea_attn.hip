@@ -52,6 +52,7 @@ struct KvMeta {
   int32_t klo, kext;   // key interval of the block
 };
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLazyMax = 8.0f;  // log2 of the largest P the lazy running max allows
 // LDS byte offset of the epilogue's per-wave row staging: past the area the
 // two groups' (m, l, O) merge uses (16384 + 512 floats)
 constexpr int kEpiStageOffset = 68 * 1024;
@@ -115,8 +116,9 @@ __device__ __forceinline__ uint2 tr_read(const uint16_t* p) {
   return __builtin_bit_cast(uint2, v);
 }
 
-// 2^x on the transcendental unit; arguments here are <= 0, and results
-// below the normal range contribute nothing next to the 1 of the row maximum.
+// 2^x on the transcendental unit; arguments here are at most kLazyMax, and
+// results below the normal range contribute nothing next to the at least 1
+// of the row's largest term.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
@@ -256,7 +258,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
         mx = fmaxf(mx, sv);
       }
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m, mx * sc);
+    // The running max moves only when a score passes it by more than
+    // kLazyMax (log2 domain).  O / l is the same for any m the two share, P
+    // stays at most 2^kLazyMax (exact range and precision in fp16), and the
+    // rescale of O below is skipped on most chunks.
+    const float cand = mx * sc;
+    const float m_new = cand > m + kLazyMax ? cand : m;
     const float m_use = m_new == -INFINITY ? 0.0f : m_new;
     float rs = 0.0f;
 #pragma unroll
