@@ -919,7 +919,7 @@ int build_rows(const Spec& sp, const ea_relation* const* ops, const OpInfo& oi, 
   int64_t n_groups = 1;
   for (int d = 0; d < r - 1; ++d) n_groups *= y->nb[d];
   int32_t c[kMaxRank] = {};
-  const int rows_per_task = 4;
+  const int rows_per_task = kRowsPerTask;  // the row kernels' wavefronts per workgroup
   const int qd = r - 2;
   for (int64_t g = 0; g < n_groups; ++g) {
     int64_t rem = g;

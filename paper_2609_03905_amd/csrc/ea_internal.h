@@ -243,6 +243,7 @@ struct AttnUnit {
   int32_t weight;      // expected tuple count (host-side ordering only)
 };
 
+constexpr int kRowsPerTask = 4;  // RMSNorm/softmax row tasks: rows per workgroup, one per wavefront
 constexpr int kAttnMaxUnitTuples = 32;  // key blocks per attention work unit (LDS table size)
 
 // Per-unit block metadata, resolved once per plan from the GPU-built tuple

@@ -21,7 +21,7 @@ namespace ea {
 
 namespace {
 
-constexpr int kThreads = 256;  // 4 rows per workgroup, one per wavefront
+constexpr int kThreads = 64 * kRowsPerTask;  // one row per wavefront
 constexpr int kMaxSeg = 64;    // segments per row on the register path
 constexpr int kMaxK = 16;      // 16-byte chunks per lane on the register path
 
