@@ -244,7 +244,7 @@ struct AttnUnit {
 };
 
 constexpr int kRowsPerTask = 4;  // RMSNorm/softmax row tasks: rows per workgroup, one per wavefront
-constexpr int kAttnMaxUnitTuples = 32;  // key blocks per attention work unit (LDS table size)
+constexpr int kAttnMaxUnitTuples = 64;  // key blocks per attention work unit (LDS table size)
 
 // Per-unit block metadata, resolved once per plan from the GPU-built tuple
 // table (attention prep kernel), so that the attention kernel reaches its
