@@ -26,15 +26,28 @@
  * the last element of the last block (ea_layout_nbytes).  Padding bytes are
  * never read for results and never written.
  *
- * Plans.  ea_joinagg / ea_repartition resolve their join (or overlay) once per
- * configuration -- spec, ops, dtypes and partitions, not data pointers -- and
- * keep the resulting tuple table in a library-owned device buffer (a plan).
- * The first call for a configuration allocates that buffer, uploads block
- * tables, runs the GPU join enumerator on the caller's stream and waits for
- * it; later calls only enqueue kernels and never synchronize.  Plans live
- * until ea_plan_cache_clear() or process exit.  Two calls that share a plan
- * must not run concurrently on different streams (an attention plan holds a
- * scratch area for its key-split partial results).
+ * Plans.  A join is resolved once per configuration -- spec, ops, dtypes,
+ * partitions and parameters, not data pointers -- into a plan: library-owned
+ * device tables (block tables, the GPU-built tuple table, the kernel's work
+ * list).  Plans are built only by the planning calls ea_joinagg_workspace,
+ * ea_repartition_plan and ea_join_tuples: they allocate the plan's device
+ * memory, run the GPU join enumerator on the given stream and wait for it.
+ * ea_joinagg and ea_repartition never allocate and never synchronize: they
+ * find the plan (EA_ERR_NOPLAN if none was built on the current device) and
+ * enqueue kernels.  A plan is immutable once built, so calls that share one
+ * may run concurrently on different streams.  Plans live until
+ * ea_plan_cache_clear() or process exit.
+ *
+ * Workspace.  Key-split join-aggs (a block GEMM or attention whose output
+ * tiles are cut into several runs of tuples to fill the GPU) exchange partial
+ * results through a caller-owned device workspace, of the size that
+ * ea_joinagg_workspace reports (0: none needed).  Its first
+ * EA_WS_COUNTER_BYTES bytes hold arrival counters: they must be zero before
+ * the workspace's first use (allocate it zeroed), and every call leaves them
+ * zero again, so one workspace serves any sequence of calls, of any
+ * configuration, on one stream.  The bytes after them hold partial results and
+ * need no initial value.  Calls that may overlap in time (different streams)
+ * need different workspaces.
  *
  * Streams are hipStream_t passed as void*; NULL is the default stream.
  *
@@ -68,6 +81,11 @@ extern "C" {
                                 /* partition not the one the inputs induce    */
 #define EA_ERR_UNSUPPORTED (-7) /* valid request outside what is implemented  */
 #define EA_ERR_HIP (-8)         /* a HIP runtime call or kernel failed        */
+#define EA_ERR_NOPLAN (-9)      /* configuration not planned on this device:  */
+                                /* call the planning entry point first        */
+
+/* Bytes at the start of a join-agg workspace that hold arrival counters. */
+#define EA_WS_COUNTER_BYTES 262144
 
 /* ---- element types --------------------------------------------------- */
 #define EA_F32 0
@@ -119,7 +137,7 @@ typedef struct ea_params {
      (fused residual): same shape and partition as the output.  Used by the
      einsum path (EA_JOIN_MUL / EA_JOIN_ADD).  NULL = none.                  */
   const ea_relation* residual;
-  /* EA_OP_ATTENTION, grouped-query attention (Section 3.2, Example "Flash
+  /* EA_OP_ATTENTION, grouped-query attention (Section 3.3, Example "Flash
      attention"): query heads per key-value head.  0 or 1: Q, K and V share
      every batch letter.  G > 1: K and V name their head letter apart from
      Q's ("bhqd,bgkd,bgkd->bhqd"), Q's head extent is G times theirs, and
@@ -203,16 +221,36 @@ int ea_relation_block(const ea_relation* rel, int64_t b, int64_t* lo, int64_t* h
      positive finite number; d must be a single block of extent 128; q and k
      block extents multiples of 128; the causal rule needs q and k of the
      same extent; bf16 data.  Scores and softmax in f32; for the P.V product
-     P (in [0, 1]) is rounded to fp16 and V is converted to fp16, so V values
-     must lie within the fp16 range; fp32 accumulation.
+     P (in [0, 2^8]: the running max may lag the true one by up to 8 in
+     the log2 domain) is rounded to fp16 and V is converted to fp16, so V
+     values must lie within the fp16 range; fp32 accumulation.
    EA_OP_SWIGLU, agg SUM: in = (X "tj", W1 "jk", W2 "jk"), out "tk" =
      silu(X W1) * (X W2), silu(g) = g / (1 + e^-g); bf16 data.
    Errors: EA_ERR_ARG, EA_ERR_SPEC, EA_ERR_DTYPE, EA_ERR_JOIN,
-   EA_ERR_UNSUPPORTED, EA_ERR_HIP.  Asynchronous on `stream` after the
-   first call of a configuration. */
+   EA_ERR_UNSUPPORTED, EA_ERR_HIP; EA_ERR_NOPLAN when the configuration was
+   not planned on the current device (ea_joinagg_workspace); EA_ERR_CAPACITY
+   when ws_bytes is below what the plan needs; EA_ERR_ARG for a missing or
+   unaligned workspace the plan needs.
+   workspace: caller-owned device memory, 256-byte aligned, of at least the
+   bytes ea_joinagg_workspace reports (NULL and 0 if it reports 0); see
+   "Workspace" above for its contents.  Asynchronous on `stream`: never
+   allocates, never synchronizes. */
 int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in,
                const ea_relation* const* in, ea_relation* out,
-               const ea_params* params, void* stream);
+               const ea_params* params, void* workspace, int64_t ws_bytes, void* stream);
+
+/* Plan a join-agg configuration (the join of Section 3.2 step 1, resolved
+   once as a compiled program would) and report the workspace its
+   ea_joinagg calls need.  Arguments as ea_joinagg; relation data may be
+   NULL.  The first call of a configuration on a device allocates the plan,
+   runs the GPU join enumerator on `stream` and waits for it; later calls only
+   look the plan up.  *ws_bytes: 0 when no workspace is needed, else at least
+   EA_WS_COUNTER_BYTES.  Errors as ea_joinagg's validation, plus
+   EA_ERR_UNSUPPORTED for a plan with more split keys than the counter area
+   holds. */
+int ea_joinagg_workspace(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in,
+                         const ea_relation* const* in, const ea_relation* out,
+                         const ea_params* params, int64_t* ws_bytes, void* stream);
 
 /* ---- the join alone (Section 3.2 step 1, Section 3.3) -------------------
    Writes the plan's GPU-built tuple table into caller device buffers:
@@ -222,7 +260,8 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in,
    for RMSNORM and SOFTMAX).  Order: group-major, then the remaining letters'
    block coordinates in order of first appearance across the inputs.
    Causal (params->causal) drops a tuple iff its key block starts after its
-   last query position.  Synchronizes `stream`.  Errors as ea_joinagg, plus
+   last query position.  Plans the configuration like ea_joinagg_workspace
+   and synchronizes `stream`.  Errors as ea_joinagg, plus
    EA_ERR_CAPACITY when cap or gcap is too small (counts still written). */
 int ea_join_tuples(const char* spec, int32_t join_op, int32_t n_in,
                    const ea_relation* const* in, const ea_relation* out,
@@ -233,8 +272,16 @@ int ea_join_tuples(const char* spec, int32_t join_op, int32_t n_in,
 /* ---- repartition (Section 5.3: overlay atoms, decompose, recompose) ------
    dst receives src's dense tensor under dst's partition.  Same rank, shape
    and dtype (EA_ERR_ARG otherwise); src and dst memory must not overlap.
-   Bit-exact byte movement.  Asynchronous on `stream`. */
+   Bit-exact byte movement.  Asynchronous on `stream`: never allocates, never
+   synchronizes.  EA_ERR_NOPLAN if ea_repartition_plan has not planned this
+   pair of partitions (with this shape and dtype) on the current device. */
 int ea_repartition(const ea_relation* src, ea_relation* dst, void* stream);
+/* Plan a repartition: its overlay boxes (Section 5.3) in a library-owned
+   device table.  Relation data may be NULL.  The first call for a pair of
+   partitions allocates the table, uploads it on `stream` and waits; later
+   calls only look it up.  Errors: EA_ERR_ARG (rank, shape or dtype differ),
+   EA_ERR_UNSUPPORTED, EA_ERR_HIP. */
+int ea_repartition_plan(const ea_relation* src, const ea_relation* dst, void* stream);
 /* ea_repartition with an output store policy (EA_STORE_CACHED or
    EA_STORE_STREAM; other values: EA_ERR_ARG).  ea_repartition is
    ea_repartition_ex(src, dst, EA_STORE_CACHED, stream). */

@@ -202,7 +202,7 @@ def join(spec: str, partitions, group: str | None = None, causal: tuple[str, str
     group: letters whose block coordinates form the group key (default: the
     output letters).  causal: (q_letter, k_letter) keeps a tuple iff some q
     position of its q block is at or after some k position of its k block.
-    Attention predicates (Section 3.2, Example "Flash attention"):
+    Attention predicates (Section 3.3, Example "Flash attention"):
     positions (q_letter, k_letter) with seq_ends, the ends of packed
     sequences, keep a tuple iff some q position and some k position of its
     blocks lie in one sequence (and satisfy causal order, if causal);
@@ -300,7 +300,7 @@ def attention(q, k, v, causal: bool, scale: float) -> np.ndarray:
 def attention_ex(q, k, v, causal: bool, scale: float, seq_ends=None) -> np.ndarray:
     """Attention with grouped-query heads (k, v [B, Hkv, S, D], query head h
     reading key/value head h // (Hq // Hkv)) and packed sequences ending at
-    seq_ends (None: one sequence); Section 3.2, Example "Flash attention"."""
+    seq_ends (None: one sequence); Section 3.3, Example "Flash attention"."""
     q, k, v = _f64(q), _f64(k), _f64(v)
     B, Hq, S, D = q.shape
     Hkv = k.shape[1]
@@ -370,6 +370,34 @@ def llama_block(x, n1, wqkv, wo, wg, wu, wd, n2, heads: int, d_head: int, eps: f
     return dict(h1=h1, qkv=qkv, attn=attn, x2=x2, h2=h2, a=a, y=y)
 
 
+def attention_rows(q, k, v, rows, scale: float, seq_ends=None) -> np.ndarray:
+    """Causal attention evaluated at the query positions ``rows`` only.
+
+    q [Hq, S, D]; k and v [Hkv, S, D], query head h reading key/value head
+    h // (Hq // Hkv); seq_ends: ends of packed sequences along S (None: one
+    sequence).  Query t of head h takes the softmax of its scaled scores
+    against the keys of its own sequence at positions <= t and returns the
+    weighted sum of their values (Section 3.3, Example "Flash attention";
+    the per-row formula attention_ex evaluates at every row).  Ends at or
+    below 0 are ignored, so a window that starts inside the tokens can pass
+    ends shifted by its start.  Returns [len(rows), Hq, D]."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    Hq, S, D = q.shape
+    group = Hq // k.shape[0]
+    rows = np.asarray(rows, dtype=np.int64)
+    ends = np.asarray(seq_ends if seq_ends is not None else [S], dtype=np.int64)
+    o = np.empty((len(rows), Hq, D))
+    for i, t in enumerate(rows):
+        before = ends[ends <= t]
+        s0 = int(before.max()) if before.size and before.max() > 0 else 0
+        for h in range(Hq):
+            m = h // group
+            sc = (k[m, s0:t + 1] @ q[h, t]) * scale
+            pr = np.exp(sc - sc.max())
+            o[i, h] = (pr @ v[m, s0:t + 1]) / pr.sum()
+    return o
+
+
 def llama_block_rows(x, n1, wqkv, wo, wg, wu, wd, n2, heads: int, d_head: int, eps: float, rows,
                      heads_kv: int | None = None, seq_ends=None):
     """Rows `rows` of llama_block's boundary relations, for sequences too long
@@ -379,7 +407,7 @@ def llama_block_rows(x, n1, wqkv, wo, wg, wu, wd, n2, heads: int, d_head: int, e
     rows: query t of head h takes the softmax of its scaled scores against
     the keys of key/value head h // (heads // heads_kv) from the start of
     its sequence through t, and returns the weighted sum of their values
-    (Section 3.2, Example "Flash attention"; the per-row formula that
+    (Section 3.3, Example "Flash attention"; the per-row formula that
     attention_ex evaluates at every row).  The remaining stages are
     row-wise.  The same bf16 rounding is applied at every relation boundary.
     Returns a dict of [len(rows), ...] fp64 arrays, rows in ascending order."""
@@ -387,7 +415,6 @@ def llama_block_rows(x, n1, wqkv, wo, wg, wu, wd, n2, heads: int, d_head: int, e
     x = _f64(x)
     T = x.shape[0]
     hkv = heads if heads_kv is None else heads_kv
-    group = heads // hkv
     hd, kvd = heads * d_head, hkv * d_head
     ends = np.asarray(seq_ends if seq_ends is not None else [T], dtype=np.int64)
     rows = np.unique(np.asarray(rows, dtype=np.int64))
@@ -395,17 +422,14 @@ def llama_block_rows(x, n1, wqkv, wo, wg, wu, wd, n2, heads: int, d_head: int, e
     lo, hi = int(starts.min()), int(rows.max()) + 1
     h1 = r(rmsnorm(x[lo:hi], n1, eps))
     qkv = r(matmul(h1, wqkv))
-    scale = 1.0 / np.sqrt(d_head)
-    o = np.empty((len(rows), hd))
-    for i, (t, s0) in enumerate(zip(rows, starts)):
-        for h in range(heads):
-            m = h // group
-            qv = qkv[t - lo, h * d_head:(h + 1) * d_head]
-            kk = qkv[s0 - lo:t - lo + 1, hd + m * d_head:hd + (m + 1) * d_head]
-            vv = qkv[s0 - lo:t - lo + 1, hd + kvd + m * d_head:hd + kvd + (m + 1) * d_head]
-            sc = (kk @ qv) * scale
-            pr = np.exp(sc - sc.max())
-            o[i, h * d_head:(h + 1) * d_head] = (pr @ vv) / pr.sum()
+
+    def heads_of(cols, n):  # [n, hi - lo, d_head]
+        return cols.reshape(hi - lo, n, d_head).transpose(1, 0, 2)
+
+    q = heads_of(qkv[:, 0:hd], heads)
+    k = heads_of(qkv[:, hd:hd + kvd], hkv)
+    v = heads_of(qkv[:, hd + kvd:hd + 2 * kvd], hkv)
+    o = attention_rows(q, k, v, rows - lo, 1.0 / np.sqrt(d_head), seq_ends=ends - lo).reshape(len(rows), hd)
     attn = r(o)
     x2 = r(add(x[rows], matmul(attn, wo)))
     h2 = r(rmsnorm(x2, n2, eps))

@@ -263,7 +263,7 @@ static int tuple_cmp(const void* a, const void* b) {
 }
 
 /* Sequence of position x among packed sequences ending at ends[0..n): the
-   number of ends at or below x (Section 3.2, Example "Flash attention"). */
+   number of ends at or below x (Section 3.3, Example "Flash attention"). */
 static int64_t seq_index(const int64_t* ends, int64_t n, int64_t x) {
   int64_t s = 0;
   while (s < n && ends[s] <= x) ++s;

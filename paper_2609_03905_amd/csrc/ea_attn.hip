@@ -22,7 +22,7 @@
 //     between lanes l and l^32;
 //   * the scale (log2 domain) is one FMA ahead of exp2; the causal mask is
 //     applied only on chunks that reach past a query of the wave;
-//   * P = 2^(S - m), in [0, 1], is rounded to fp16 and O^T += V^T P^T runs
+//   * P = 2^(S - m), in [0, 2^8] (m lags the true max by at most 8), is rounded to fp16 and O^T += V^T P^T runs
 //     on fp16 MFMA 32x32x16; the V^T operand (8 keys of one d per lane)
 //     comes from two transposing LDS reads (ds_read_b64_tr_b16) of the
 //     [key][d] chunk, with the MFMA's k order matched to the accumulator
@@ -518,7 +518,8 @@ __global__ __launch_bounds__(64) void attn_prep_kernel(const AttnArgs p) {
     um.qoff = qb.off;
     um.ooff = p.blk_o[p.tuples[(int64_t)gb * 4 + 0]].off;
     um.q_lo = qb.lo[p.q_dim];
-    um.nt = min(te - tb, kAttnMaxUnitTuples);  // the plan sizes units to fit; a guard on the record
+    um.nt = min(te - tb, kAttnMaxUnitTuples);
+    if (te - tb > kAttnMaxUnitTuples) *p.overflow = 1;  // the host refuses the plan
   }
   for (int t = lane; t < te - tb && t < kAttnMaxUnitTuples; t += 64) {
     const int32_t* tp = p.tuples + (int64_t)(tb + t) * 4;

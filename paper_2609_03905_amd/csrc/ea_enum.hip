@@ -8,7 +8,7 @@
 // (lo, hi) must be one of the operand's intervals (binary search on its split
 // points, then an exact comparison of both bounds).  A matched candidate that
 // passes the optional predicates (causal; grouped-query heads; packed
-// sequences, Section 3.2 Example "Flash attention") becomes a tuple
+// sequences, Section 3.3 Example "Flash attention") becomes a tuple
 // (output block, input blocks...).  Kept tuples are compacted with a
 // workgroup prefix sum, so the table comes out grouped by output key with no
 // sort, and the CSR group offsets fall out of the same scan.

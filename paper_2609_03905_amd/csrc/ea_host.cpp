@@ -303,8 +303,9 @@ struct RowLayout {
 struct Plan {
   int device = 0;
   Kind kind = K_GENERIC;
-  char* dmem = nullptr;
+  char* dmem = nullptr;   // tables of the join and the work list
   size_t dbytes = 0;
+  char* dmem2 = nullptr;  // attention: work units and their block records
   // join
   int n_in = 0;
   int64_t n_groups = 0, tuple_cap = 0;
@@ -322,17 +323,21 @@ struct Plan {
   // rows
   RowLayout rows;
   AttnUnitMeta* attn_meta = nullptr;
-  // attention scratch
-  float* part_o = nullptr;
-  float* part_ml = nullptr;
-  int32_t* counters = nullptr;
+  // Caller workspace of split keys: arrival counters at the start of the
+  // counter area, partial results after the area (attention: O partials,
+  // then (m, l) partials at ws_part_ml).
+  int64_t ws_counters = 0;
+  int64_t ws_partial_bytes = 0;
+  size_t ws_part_ml = 0;
+  int64_t ws_bytes() const { return ws_counters || ws_partial_bytes ? kWsCounterBytes + ws_partial_bytes : 0; }
   ~Plan() {
-    if (dmem) {
+    if (dmem || dmem2) {
       int cur = 0;
       if (hipGetDevice(&cur) == hipSuccess) {
         (void)hipSetDevice(device);
         (void)hipDeviceSynchronize();
-        (void)hipFree(dmem);
+        if (dmem) (void)hipFree(dmem);
+        if (dmem2) (void)hipFree(dmem2);
         (void)hipSetDevice(cur);
       }
     }
@@ -354,16 +359,17 @@ void key_rel(std::ostringstream& k, const ea_relation* r) {
   }
 }
 
-// Allocate the plan's device buffer (image + extra zeroed scratch) and upload.
-int plan_upload(Plan* p, const Image& img, size_t extra, size_t* extra_off, hipStream_t s) {
-  const size_t base = (size_t)align256((int64_t)img.bytes.size());
-  p->dbytes = base + extra;
-  EA_HIP_TRY(hipGetDevice(&p->device));
-  EA_HIP_TRY(hipMalloc((void**)&p->dmem, p->dbytes));
-  EA_HIP_TRY(hipMemcpyAsync(p->dmem, img.bytes.data(), img.bytes.size(), hipMemcpyHostToDevice, s));
-  if (extra) EA_HIP_TRY(hipMemsetAsync(p->dmem + base, 0, extra, s));
-  if (extra_off) *extra_off = base;
+// Allocate a device buffer for a plan image and upload the image into it.
+int upload_image(const Image& img, char** mem, hipStream_t s) {
+  EA_HIP_TRY(hipMalloc((void**)mem, std::max<size_t>(img.bytes.size(), 256)));
+  EA_HIP_TRY(hipMemcpyAsync(*mem, img.bytes.data(), img.bytes.size(), hipMemcpyHostToDevice, s));
   return EA_OK;
+}
+
+int plan_upload(Plan* p, const Image& img, hipStream_t s) {
+  p->dbytes = img.bytes.size();
+  EA_HIP_TRY(hipGetDevice(&p->device));
+  return upload_image(img, &p->dmem, s);
 }
 
 // Build the enumerator description and reserve the tuple table.
@@ -685,11 +691,7 @@ int classify(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation*
 // ---------------------------------------------------------------------------
 struct Extra {
   size_t desc = 0, work = 0;
-  size_t scratch_bytes = 0;
   int64_t n_work = 0;
-  // attention scratch layout (offsets inside the scratch area)
-  size_t part_o = 0, part_ml = 0, counters = 0;
-  size_t meta = 0;  // attention: per-unit block metadata (filled at plan time)
 };
 
 int build_generic(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation* const* ops,
@@ -954,41 +956,32 @@ int build_rows(const Spec& sp, const ea_relation* const* ops, const OpInfo& oi, 
   return EA_OK;
 }
 
-int build_attention(const ea_relation* const* ops, const OpInfo& oi, const JoinInfo& ji, int causal, Image* img,
-                    Extra* ex) {
-  // Work units: per group (b.., q block) and per 128-row query tile, the
-  // group's tuples (key blocks) split into runs of at most `chunk` tuples.
-  // Tuple counts per group are known on the host from the causal rule.
-  const ea_relation* Q = ops[0];
-  const ea_relation* K = ops[1];
-  const int r = Q->rank;
-  (void)ji;
-  int64_t n_groups = Q->nblocks;  // group letters are all of Q's letters; d is one block
+// Work units of an attention plan.  Per group (b.., q block) and per 128-row
+// query tile, the group's tuples (the key blocks the GPU join kept) are split
+// into runs of at most kAttnMaxUnitTuples; the last unit of a split tile to
+// finish merges the partials.  Tuple counts come from the GPU-built group
+// offsets (goff), so the units follow the join's own predicates.
+struct AttnPlanInfo {
   std::vector<AttnUnit> units;
-  int32_t slot = 0, counter = 0;
-  int32_t c[kMaxRank];
-  // tuples of every (group, 128-row tile): the key blocks the causal and
-  // sequence rules keep (the GPU join's predicates; grouped-query heads keep
-  // one key/value head per query head, so they do not change the count).
-  // It sizes the split, which holds at most kAttnMaxUnitTuples per unit; the
-  // kernel reads its tuple range from the GPU-built group offsets
+  int32_t slots = 0, counters = 0;
+};
+
+int attention_units(const ea_relation* Q, const std::vector<int32_t>& goff, AttnPlanInfo* info) {
+  const int r = Q->rank;
+  const int64_t n_groups = Q->nblocks;  // group letters are all of Q's letters; d is one block
+  if ((int64_t)goff.size() != n_groups + 1) return fail(EA_ERR_HIP, "internal: attention group count mismatch");
   struct TileWork {
     int64_t g, q0;
     int n_t;
   };
   std::vector<TileWork> tiles;
+  int32_t c[kMaxRank];
   for (int64_t g = 0; g < n_groups; ++g) {
     block_coords(Q, g, c);
-    const int64_t q_lo = Q->splits[r - 2][c[r - 2]];
-    const int64_t q_hi = Q->splits[r - 2][c[r - 2] + 1];
-    const std::vector<int64_t>& ends = oi.seq_ends;
-    auto seq_of = [&](int64_t x) { return std::upper_bound(ends.begin(), ends.end(), x) - ends.begin(); };
-    int n_t = 0;
-    for (int kb = 0; kb < K->nb[r - 2]; ++kb) {
-      const int64_t k_lo = K->splits[r - 2][kb];
-      if ((!causal || k_lo <= q_hi - 1) && (ends.empty() || seq_of(k_lo) == seq_of(q_lo))) ++n_t;
-    }
-    for (int64_t q0 = 0; q0 < q_hi - q_lo; q0 += 128) tiles.push_back(TileWork{g, q0, n_t});
+    const int64_t q_ext = Q->splits[r - 2][c[r - 2] + 1] - Q->splits[r - 2][c[r - 2]];
+    const int n_t = goff[(size_t)g + 1] - goff[(size_t)g];
+    if (n_t < 0) return fail(EA_ERR_HIP, "internal: GPU join group offsets decrease at group %lld", (long long)g);
+    for (int64_t q0 = 0; q0 < q_ext; q0 += 128) tiles.push_back(TileWork{g, q0, n_t});
   }
   // key blocks per unit (the online-softmax partial): the run that minimises
   // waves of units over the 256 CUs x (longest unit + half a key block per
@@ -1013,6 +1006,7 @@ int build_attention(const ea_relation* const* ops, const OpInfo& oi, const JoinI
       chunk = cc;
     }
   }
+  int32_t slot = 0, counter = 0;
   for (const TileWork& t : tiles) {
     const int parts = std::max(1, (t.n_t + chunk - 1) / chunk);
     for (int p = 0; p < parts; ++p) {
@@ -1022,6 +1016,8 @@ int build_attention(const ea_relation* const* ops, const OpInfo& oi, const JoinI
       u.part = p;
       u.n_parts = parts;
       u.weight = (t.n_t * (p + 1)) / parts - (t.n_t * p) / parts;
+      if (u.weight > kAttnMaxUnitTuples)
+        return fail(EA_ERR_HIP, "internal: attention unit of %d key blocks exceeds %d", u.weight, kAttnMaxUnitTuples);
       if (parts > 1) {
         u.slot = slot + p;
         u.first_slot = slot;
@@ -1031,7 +1027,7 @@ int build_attention(const ea_relation* const* ops, const OpInfo& oi, const JoinI
         u.first_slot = -1;
         u.counter = -1;
       }
-      units.push_back(u);
+      info->units.push_back(u);
     }
     if (parts > 1) {
       slot += parts;
@@ -1039,23 +1035,22 @@ int build_attention(const ea_relation* const* ops, const OpInfo& oi, const JoinI
     }
   }
   // heaviest units first so that the long runs start early
-  std::stable_sort(units.begin(), units.end(),
+  std::stable_sort(info->units.begin(), info->units.end(),
                    [](const AttnUnit& a, const AttnUnit& b) { return a.weight > b.weight; });
-  ex->work = img->put_vec(units);
-  ex->n_work = (int64_t)units.size();
-  ex->meta = img->put_zero(units.size() * sizeof(AttnUnitMeta));
-  ex->part_o = 0;
-  ex->part_ml = (size_t)slot * 128 * 128 * sizeof(float);
-  ex->counters = ex->part_ml + (size_t)slot * 128 * 2 * sizeof(float);
-  ex->scratch_bytes = ex->counters + (size_t)std::max(counter, 1) * sizeof(int32_t);
-  (void)oi;
+  info->slots = slot;
+  info->counters = counter;
   return EA_OK;
 }
 
 // Look up or create the plan of a join-agg call.
+// Look up the plan of a join-agg configuration.  With build set, a missing
+// plan is created: its tables are uploaded, the GPU join enumerator runs on
+// stream s and the host waits for it (and, for attention, sizes the work
+// units from the GPU's group offsets).  Without build, a missing plan is
+// EA_ERR_NOPLAN: the enqueue path never allocates or synchronizes.
 int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int32_t agg_op,
-                     const ea_relation* const* ops, const ea_params* prm, const OpInfo& oi, hipStream_t s,
-                     Plan** out) {
+                     const ea_relation* const* ops, const ea_params* prm, const OpInfo& oi, bool build,
+                     hipStream_t s, Plan** out) {
   int dev = 0;
   EA_HIP_TRY(hipGetDevice(&dev));
   std::ostringstream k;
@@ -1072,6 +1067,9 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
     *out = it->second.get();
     return EA_OK;
   }
+  if (!build)
+    return fail(EA_ERR_NOPLAN, "join-agg '%s' is not planned on device %d: call ea_joinagg_workspace first", spec_str,
+                dev);
   JoinInfo ji;
   int e = analyze_join(sp, ops, oi.group, &ji);
   if (e) return e;
@@ -1091,36 +1089,44 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
       ex.work = img.put_vec(gi.units);
       ex.n_work = (int64_t)gi.units.size();
       p->gemm_parts = gi.parts;
-      ex.part_o = 0;  // partial sums of split tiles, then their counters
-      ex.counters = (size_t)gi.slots * kGemmTM * kGemmTN * sizeof(float);
-      ex.scratch_bytes = gi.slots ? ex.counters + (size_t)gi.counters * sizeof(int32_t) : 0;
+      p->ws_counters = gi.counters;  // fp32 partial tiles of split keys in the workspace
+      p->ws_partial_bytes = (int64_t)gi.slots * kGemmTM * kGemmTN * (int64_t)sizeof(float);
       break;
     }
     case K_RMSNORM:
     case K_SOFTMAX: e = build_rows(sp, ops, oi, &img, &ex, &p->rows); break;
-    case K_ATTENTION: e = build_attention(ops, oi, ji, oi.causal, &img, &ex); break;
+    case K_ATTENTION: break;  // work units follow the GPU join (below)
     default: e = fail(EA_ERR_UNSUPPORTED, "internal: unknown plan kind");
   }
   if (e) return e;
-  size_t scratch_base = 0;
-  e = plan_upload(p.get(), img, ex.scratch_bytes, &scratch_base, s);
+  e = plan_upload(p.get(), img, s);
   if (e) return e;
   p->d_desc = ex.desc ? p->dmem + ex.desc : nullptr;
   p->d_work = p->dmem + ex.work;
   p->n_work = ex.n_work;
-  if (oi.kind == K_GEMM && ex.scratch_bytes) {
-    p->part_o = (float*)(p->dmem + scratch_base + ex.part_o);
-    p->counters = (int32_t*)(p->dmem + scratch_base + ex.counters);
-  }
-  if (oi.kind == K_ATTENTION) {
-    p->part_o = (float*)(p->dmem + scratch_base + ex.part_o);
-    p->part_ml = (float*)(p->dmem + scratch_base + ex.part_ml);
-    p->counters = (int32_t*)(p->dmem + scratch_base + ex.counters);
-  }
   e = finish_join(p.get(), js, sp.n_in + 1, s);
   if (e) return e;
   if (oi.kind == K_ATTENTION) {
-    p->attn_meta = (AttnUnitMeta*)(p->dmem + ex.meta);
+    // units from the GPU-built group offsets (the join has completed)
+    std::vector<int32_t> goff((size_t)p->n_groups + 1);
+    EA_HIP_TRY(hipMemcpyAsync(goff.data(), p->d_goff, goff.size() * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    EA_HIP_TRY(hipStreamSynchronize(s));
+    AttnPlanInfo ai;
+    e = attention_units(ops[0], goff, &ai);
+    if (e) return e;
+    Image img2;
+    const size_t uoff = img2.put_vec(ai.units);
+    const size_t moff = img2.put_zero(ai.units.size() * sizeof(AttnUnitMeta));
+    const size_t foff = img2.put_zero(sizeof(int32_t));
+    e = upload_image(img2, &p->dmem2, s);
+    if (e) return e;
+    p->d_work = p->dmem2 + uoff;
+    p->n_work = (int64_t)ai.units.size();
+    p->attn_meta = (AttnUnitMeta*)(p->dmem2 + moff);
+    const int64_t slots = ai.slots;
+    p->ws_counters = ai.counters;
+    p->ws_part_ml = (size_t)slots * 128 * 128 * sizeof(float);
+    p->ws_partial_bytes = slots ? (int64_t)p->ws_part_ml + slots * 128 * 2 * (int64_t)sizeof(float) : 0;
     AttnArgs a;
     memset(&a, 0, sizeof(a));
     a.tuples = p->d_tuples;
@@ -1134,9 +1140,17 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
     a.q_dim = oi.q_dim;
     a.k_dim = oi.k_dim;
     a.meta = p->attn_meta;
+    a.overflow = (int32_t*)(p->dmem2 + foff);
     EA_HIP_TRY(launch_attention_prep(a, s));
+    int32_t overflow = 0;
+    EA_HIP_TRY(hipMemcpyAsync(&overflow, a.overflow, sizeof(int32_t), hipMemcpyDeviceToHost, s));
     EA_HIP_TRY(hipStreamSynchronize(s));
+    if (overflow)
+      return fail(EA_ERR_HIP, "internal: an attention unit holds more than %d key blocks", kAttnMaxUnitTuples);
   }
+  if (p->ws_counters * (int64_t)sizeof(int32_t) > kWsCounterBytes)
+    return fail(EA_ERR_UNSUPPORTED, "plan needs %lld split-key counters, above the workspace's %lld",
+                (long long)p->ws_counters, (long long)(kWsCounterBytes / (int64_t)sizeof(int32_t)));
   *out = p.get();
   cache()[key] = std::move(p);
   return EA_OK;
@@ -1150,7 +1164,7 @@ int check_rel(const ea_relation* r, const char* what, bool need_data) {
 
 // Common front half of ea_joinagg / ea_join_tuples: validation + plan.
 int prepare(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, const ea_relation* const* in,
-            const ea_relation* out, const ea_params* prm, bool need_data, hipStream_t s, Spec* sp,
+            const ea_relation* out, const ea_params* prm, bool need_data, bool build, hipStream_t s, Spec* sp,
             OpInfo* oi, Plan** plan) {
   if (!spec) return fail(EA_ERR_ARG, "NULL spec");
   if (n_in < 1 || n_in > kMaxIn || !in) return fail(EA_ERR_ARG, "n_in %d outside [1, %d] or NULL inputs", n_in, kMaxIn);
@@ -1182,7 +1196,14 @@ int prepare(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, con
   e = analyze_join(*sp, ops, oi->group, &ji);
   if (e) return e;
   if (!plan) return EA_OK;
-  return get_joinagg_plan(spec, *sp, join_op, agg_op, ops, prm, *oi, s, plan);
+  return get_joinagg_plan(spec, *sp, join_op, agg_op, ops, prm, *oi, build, s, plan);
+}
+
+// Validate a run of a planned join-agg and find its plan (never building it).
+int lookup_run(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, const ea_relation* const* in,
+               const ea_relation* out, const ea_params* params, hipStream_t s, OpInfo* oi, Plan** plan) {
+  Spec sp;
+  return prepare(spec, join_op, agg_op, n_in, in, out, params, true, false, s, &sp, oi, plan);
 }
 
 }  // namespace
@@ -1337,7 +1358,7 @@ int ea_join_tuples(const char* spec, int32_t join_op, int32_t n_in, const ea_rel
   Spec sp;
   OpInfo oi;
   Plan* plan = nullptr;
-  int e = prepare(spec, join_op, agg, n_in, in, out, params, false, s, &sp, &oi, &plan);
+  int e = prepare(spec, join_op, agg, n_in, in, out, params, false, true, s, &sp, &oi, &plan);
   if (e) return e;
   int32_t count = 0;
   EA_HIP_TRY(hipMemcpyAsync(&count, plan->d_count, sizeof(int32_t), hipMemcpyDeviceToHost, s));
@@ -1360,14 +1381,15 @@ int ea_join_tuples(const char* spec, int32_t join_op, int32_t n_in, const ea_rel
   return ok();
 }
 
-int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, const ea_relation* const* in,
-               ea_relation* out, const ea_params* params, void* stream) {
-  hipStream_t s = (hipStream_t)stream;
-  Spec sp;
-  OpInfo oi;
-  Plan* plan = nullptr;
-  int e = prepare(spec, join_op, agg_op, n_in, in, out, params, true, s, &sp, &oi, &plan);
-  if (e) return e;
+}  // extern "C"
+
+namespace {
+
+// Enqueue the kernels of a planned join-agg on stream s.  ws: the split-key
+// workspace (counters at its start, partial results from kWsCounterBytes),
+// at least plan->ws_bytes() bytes, or null when the plan needs none.
+int run_planned(const Plan* plan, int32_t join_op, int32_t n_in, const ea_relation* const* in, ea_relation* out,
+                const ea_params* params, const OpInfo& oi, char* ws, hipStream_t s) {
   const ea_relation* res = params ? params->residual : nullptr;
   switch (plan->kind) {
     case K_GENERIC: {
@@ -1420,8 +1442,8 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
         for (int i = 0; i < n_in; ++i) small &= max_block_bytes(in[i]) < (int64_t(1) << 32);
         a.direct = k32 && per_unit <= kGemmMaxTuples && small;
       }
-      a.partials = plan->part_o;
-      a.counters = plan->counters;
+      a.partials = (float*)(ws + kWsCounterBytes);
+      a.counters = (int32_t*)ws;
       EA_HIP_TRY(launch_gemm(a, s));
       break;
     }
@@ -1481,9 +1503,9 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
       a.q_dim = oi.q_dim;
       a.k_dim = oi.k_dim;
       a.scale = params->scale;
-      a.part_o = plan->part_o;
-      a.part_ml = plan->part_ml;
-      a.counters = plan->counters;
+      a.part_o = (float*)(ws + kWsCounterBytes);
+      a.part_ml = (float*)(ws + kWsCounterBytes + plan->ws_part_ml);
+      a.counters = (int32_t*)ws;
       a.dt_o = out->dtype;
       a.meta = plan->attn_meta;
       EA_HIP_TRY(launch_attention(a, s));
@@ -1492,6 +1514,45 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
     default:
       return fail(EA_ERR_UNSUPPORTED, "internal: plan kind %d", (int)plan->kind);
   }
+  return EA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+
+int ea_joinagg_workspace(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in,
+                         const ea_relation* const* in, const ea_relation* out, const ea_params* params,
+                         int64_t* ws_bytes, void* stream) {
+  if (!ws_bytes) return fail(EA_ERR_ARG, "NULL ws_bytes");
+  *ws_bytes = 0;
+  Spec sp;
+  OpInfo oi;
+  Plan* plan = nullptr;
+  int e = prepare(spec, join_op, agg_op, n_in, in, out, params, false, true, (hipStream_t)stream, &sp, &oi, &plan);
+  if (e) return e;
+  *ws_bytes = plan->ws_bytes();
+  return ok();
+}
+
+int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, const ea_relation* const* in,
+               ea_relation* out, const ea_params* params, void* workspace, int64_t ws_bytes, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  OpInfo oi;
+  Plan* plan = nullptr;
+  int e = lookup_run(spec, join_op, agg_op, n_in, in, out, params, s, &oi, &plan);
+  if (e) return e;
+  const int64_t need = plan->ws_bytes();
+  if (need) {
+    if (!workspace) return fail(EA_ERR_ARG, "this join-agg needs a workspace of %lld bytes", (long long)need);
+    if ((uintptr_t)workspace % 256) return fail(EA_ERR_ARG, "workspace must be 256-byte aligned");
+    if (ws_bytes < need)
+      return fail(EA_ERR_CAPACITY, "workspace of %lld bytes below the %lld this join-agg needs", (long long)ws_bytes,
+                  (long long)need);
+  }
+  e = run_planned(plan, join_op, n_in, in, out, params, oi, need ? (char*)workspace : nullptr, s);
+  if (e) return e;
   return ok();
 }
 
@@ -1499,21 +1560,28 @@ int ea_repartition(const ea_relation* src, ea_relation* dst, void* stream) {
   return ea_repartition_ex(src, dst, EA_STORE_CACHED, stream);
 }
 
-int ea_repartition_ex(const ea_relation* src, ea_relation* dst, int32_t store, void* stream) {
-  hipStream_t s = (hipStream_t)stream;
-  if (store != EA_STORE_CACHED && store != EA_STORE_STREAM) return fail(EA_ERR_ARG, "store must be EA_STORE_CACHED or EA_STORE_STREAM");
+}  // extern "C"
+
+namespace {
+
+int check_repartition(const ea_relation* src, const ea_relation* dst, bool need_data) {
   if (!src || !dst) return fail(EA_ERR_ARG, "NULL relation");
-  if (!src->data || !dst->data) return fail(EA_ERR_ARG, "relation has no data");
+  if (need_data && (!src->data || !dst->data)) return fail(EA_ERR_ARG, "relation has no data");
   if (src->rank != dst->rank || src->dtype != dst->dtype)
     return fail(EA_ERR_ARG, "source and destination differ in rank or dtype");
   for (int d = 0; d < src->rank; ++d)
     if (src->shape[d] != dst->shape[d]) return fail(EA_ERR_ARG, "source and destination differ in shape");
-  {
+  if (need_data) {
     const char* a0 = (const char*)src->data;
     const char* b0 = (const char*)dst->data;
     if (a0 < b0 + dst->nbytes && b0 < a0 + src->nbytes)
       return fail(EA_ERR_ARG, "source and destination memory overlap");
   }
+  return EA_OK;
+}
+
+// The plan of a repartition (its overlay boxes), built when `build` is set.
+int get_repartition_plan(const ea_relation* src, const ea_relation* dst, bool build, hipStream_t s, Plan** out) {
   int dev = 0;
   EA_HIP_TRY(hipGetDevice(&dev));
   std::ostringstream k;
@@ -1526,6 +1594,8 @@ int ea_repartition_ex(const ea_relation* src, ea_relation* dst, int32_t store, v
     std::lock_guard<std::mutex> lk(g_cache_mu);
     auto it = cache().find(key);
     if (it != cache().end()) plan = it->second.get();
+    if (!plan && !build)
+      return fail(EA_ERR_NOPLAN, "repartition is not planned on device %d: call ea_repartition_plan first", dev);
     if (!plan) {
       // Overlay (Section 5.3): cut every dim at the union of both partitions'
       // split points.  A box = the intersection of one source block and one
@@ -1626,7 +1696,7 @@ int ea_repartition_ex(const ea_relation* src, ea_relation* dst, int32_t store, v
       const size_t toff = img.put_vec(tasks);
       auto p = std::make_unique<Plan>();
       p->kind = K_REPART;
-      int e = plan_upload(p.get(), img, 0, nullptr, s);
+      int e = plan_upload(p.get(), img, s);
       if (e) return e;
       EA_HIP_TRY(hipStreamSynchronize(s));
       p->d_work = p->dmem + toff;
@@ -1635,6 +1705,31 @@ int ea_repartition_ex(const ea_relation* src, ea_relation* dst, int32_t store, v
       cache()[key] = std::move(p);
     }
   }
+  *out = plan;
+  return EA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ea_repartition_plan(const ea_relation* src, const ea_relation* dst, void* stream) {
+  int e = check_repartition(src, dst, false);
+  if (e) return e;
+  Plan* plan = nullptr;
+  e = get_repartition_plan(src, dst, true, (hipStream_t)stream, &plan);
+  if (e) return e;
+  return ok();
+}
+
+int ea_repartition_ex(const ea_relation* src, ea_relation* dst, int32_t store, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  if (store != EA_STORE_CACHED && store != EA_STORE_STREAM) return fail(EA_ERR_ARG, "store must be EA_STORE_CACHED or EA_STORE_STREAM");
+  int e = check_repartition(src, dst, true);
+  if (e) return e;
+  Plan* plan = nullptr;
+  e = get_repartition_plan(src, dst, false, s, &plan);
+  if (e) return e;
   EA_HIP_TRY(launch_repartition((const RepTask*)plan->d_work, plan->n_work, (const char*)src->data,
                                 (char*)dst->data, store == EA_STORE_STREAM, s));
   return ok();

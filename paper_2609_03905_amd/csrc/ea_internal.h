@@ -1,9 +1,11 @@
 // ea_internal.h -- structures shared by libea's host code and its HIP kernels.
 //
-// A plan is one library-owned device buffer holding everything a join-agg or
-// repartition needs besides the relations' data: the enumerator description,
-// the split points, per-operand block tables, the GPU-built tuple table with
-// its CSR group offsets, the kernel's work list and any scratch space.
+// A plan is library-owned device memory holding what a join-agg or
+// repartition needs besides the relations' data and the caller's workspace:
+// the enumerator description, the split points, per-operand block tables, the
+// GPU-built tuple table with its CSR group offsets and the kernel's work list.
+// It is immutable once built, so calls sharing it may run concurrently on
+// several streams, each with its own workspace.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -18,6 +20,9 @@ constexpr int kMaxRank = EA_MAX_RANK;
 constexpr int kMaxIn = EA_MAX_INPUTS;
 constexpr int kMaxOps = EA_MAX_INPUTS + 1;  // inputs, then the output
 constexpr int kMaxLetters = 16;
+// A join-agg workspace: arrival counters of split keys in its first
+// kWsCounterBytes (zero between calls), partial results after them.
+constexpr int64_t kWsCounterBytes = EA_WS_COUNTER_BYTES;
 
 // One block of a relation: byte offset from the relation base, and its
 // sub-tensor type as (lo, extent) per dim.
@@ -230,7 +235,8 @@ hipError_t launch_softmax(const RowArgs& a, hipStream_t s);
 // Causal attention with key-split online-softmax aggregation.
 // A unit is (group, query tile of 128 rows, a run of the group's tuples).
 // Units of one (group, tile) that split its tuples write partial (m, l, O)
-// to scratch; the last unit to finish merges them in tuple order.
+// to the caller's workspace; the last unit to finish merges them in tuple
+// order.
 // ---------------------------------------------------------------------------
 struct AttnUnit {
   int32_t group;
@@ -281,6 +287,7 @@ struct AttnArgs {
   int32_t* counters;     // one per split (group, tile); zero between calls
   int32_t dt_o;
   AttnUnitMeta* meta;    // one per unit (written by the prep kernel at plan time)
+  int32_t* overflow;     // prep kernel: set to 1 if a unit exceeds kAttnMaxUnitTuples
 };
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);

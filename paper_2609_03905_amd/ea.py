@@ -19,7 +19,9 @@ LIB_PATH = os.path.join(_HERE, "libea.so")
 # ---- codes (mirror include/ea.h) ------------------------------------------
 OK = 0
 ERR_NAMES = {-1: "EA_ERR_ARG", -2: "EA_ERR_DTYPE", -3: "EA_ERR_PARTITION", -4: "EA_ERR_CAPACITY",
-             -5: "EA_ERR_SPEC", -6: "EA_ERR_JOIN", -7: "EA_ERR_UNSUPPORTED", -8: "EA_ERR_HIP"}
+             -5: "EA_ERR_SPEC", -6: "EA_ERR_JOIN", -7: "EA_ERR_UNSUPPORTED", -8: "EA_ERR_HIP",
+             -9: "EA_ERR_NOPLAN"}
+WS_COUNTER_BYTES = 262144  # EA_WS_COUNTER_BYTES: the counter area at the start of a workspace
 F32, BF16, F16 = 0, 1, 2
 DTYPES = {"f32": F32, "bf16": BF16, "f16": F16}
 ELEM_SIZE = {"f32": 4, "bf16": 2, "f16": 2}
@@ -62,7 +64,9 @@ def lib() -> ctypes.CDLL:
         L.ea_relation_num_blocks.argtypes = [vp, P(i64)]
         L.ea_relation_nbytes.argtypes = [vp, P(i64)]
         L.ea_relation_block.argtypes = [vp, i64, P(i64), P(i64), P(i64)]
-        L.ea_joinagg.argtypes = [ctypes.c_char_p, i32, i32, i32, P(vp), vp, P(_Params), vp]
+        L.ea_joinagg.argtypes = [ctypes.c_char_p, i32, i32, i32, P(vp), vp, P(_Params), vp, i64, vp]
+        L.ea_joinagg_workspace.argtypes = [ctypes.c_char_p, i32, i32, i32, P(vp), vp, P(_Params), P(i64), vp]
+        L.ea_repartition_plan.argtypes = [vp, vp, vp]
         L.ea_join_tuples.argtypes = [ctypes.c_char_p, i32, i32, P(vp), vp, P(_Params), vp, i64, vp, i64,
                                      P(i64), P(i64), vp]
         L.ea_repartition.argtypes = [vp, vp, vp]
@@ -197,25 +201,84 @@ def _params(eps=0.0, scale=0.0, causal=False, store=0, residual=None, gqa_group=
     return prm, ends
 
 
+def new_workspace(nbytes: int, device=None) -> torch.Tensor:
+    """A zeroed device buffer usable as a join-agg workspace of ``nbytes``
+    (the counter area must start zeroed; every call leaves it zeroed)."""
+    return torch.zeros(max(int(nbytes), 1), dtype=torch.uint8, device=device or "cuda")
+
+
+_WS = {}  # (device, stream handle) -> workspace tensor of the calls on that stream
+_WS_RETIRED = []  # outgrown workspaces: kernels queued earlier may still use them
+
+
+def _stream_workspace(nbytes: int, stream: ctypes.c_void_p) -> torch.Tensor:
+    """The binding's workspace for calls on ``stream``: calls on one stream run
+    in order, so they share one buffer, grown (zeroed) when a plan needs more."""
+    dev = torch.cuda.current_device()
+    key = (dev, stream.value or 0)
+    buf = _WS.get(key)
+    if buf is None or buf.numel() < nbytes:
+        if buf is not None:
+            _WS_RETIRED.append(buf)
+        buf = new_workspace(max(nbytes, 2 * buf.numel() if buf is not None else nbytes), device=dev)
+        torch.cuda.synchronize(dev)  # zeroed before any stream uses it
+        _WS[key] = buf
+    return buf
+
+
+def joinagg_workspace(spec: str, join_op: int, agg_op: int, inputs: Sequence[Relation], out: Relation, *,
+                      eps: float = 0.0, scale: float = 0.0, causal: bool = False, residual: Relation | None = None,
+                      store: int = 0, gqa_group: int = 0, seq_ends=None, stream=None) -> int:
+    """Plan a join-agg configuration (first call: allocate the plan, run the
+    GPU join, wait for it) and return the workspace bytes its runs need."""
+    handles = _arr(ctypes.c_void_p, [r.handle.value for r in inputs])
+    prm, _ends = _params(eps, scale, causal, store, residual, gqa_group, seq_ends)
+    n = ctypes.c_int64()
+    _check(lib().ea_joinagg_workspace(spec.encode(), join_op, agg_op, len(inputs), handles, out.handle,
+                                      ctypes.byref(prm), ctypes.byref(n), _stream(stream)))
+    return int(n.value)
+
+
 def joinagg(spec: str, join_op: int, agg_op: int, inputs: Sequence[Relation], out: Relation, *,
             eps: float = 0.0, scale: float = 0.0, causal: bool = False, residual: Relation | None = None,
-            store: int = 0, gqa_group: int = 0, seq_ends=None, stream=None) -> None:
+            store: int = 0, gqa_group: int = 0, seq_ends=None, stream=None,
+            workspace: torch.Tensor | None = None) -> None:
     """Run one GPU's share of a join-agg: join the input relations' blocks,
     run the per-tuple kernel, aggregate by output key, store into ``out``.
     ``store``: STORE_CACHED (default) or STORE_STREAM (non-temporal output
     stores, for an output nothing reads soon).  Attention: ``gqa_group``
     query heads per key-value head, ``seq_ends`` the ends of packed
-    sequences."""
+    sequences.  The configuration is planned on first use (see
+    joinagg_workspace).  ``workspace``: a device buffer from new_workspace
+    for key-split partials; by default one buffer per stream, held by the
+    binding."""
     handles = _arr(ctypes.c_void_p, [r.handle.value for r in inputs])
     prm, _ends = _params(eps, scale, causal, store, residual, gqa_group, seq_ends)
-    _check(lib().ea_joinagg(spec.encode(), join_op, agg_op, len(inputs), handles, out.handle, ctypes.byref(prm),
-                            _stream(stream)))
+    s = _stream(stream)
+    need = ctypes.c_int64()
+    spec_b = spec.encode()
+    _check(lib().ea_joinagg_workspace(spec_b, join_op, agg_op, len(inputs), handles, out.handle, ctypes.byref(prm),
+                                      ctypes.byref(need), s))
+    ws, nbytes = None, 0
+    if need.value:
+        buf = workspace if workspace is not None else _stream_workspace(need.value, s)
+        ws, nbytes = ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size()
+    _check(lib().ea_joinagg(spec_b, join_op, agg_op, len(inputs), handles, out.handle, ctypes.byref(prm), ws, nbytes,
+                            s))
+
+
+def repartition_plan(src: Relation, dst: Relation, stream=None) -> None:
+    """Plan the repartition of ``src``'s partition into ``dst``'s (first call:
+    build and upload its overlay boxes, wait)."""
+    _check(lib().ea_repartition_plan(src.handle, dst.handle, _stream(stream)))
 
 
 def repartition(src: Relation, dst: Relation, stream=None, *, store: int = 0) -> None:
     """Write ``src``'s dense tensor into ``dst`` under ``dst``'s partition
-    (``store`` as for joinagg)."""
-    _check(lib().ea_repartition_ex(src.handle, dst.handle, int(store), _stream(stream)))
+    (``store`` as for joinagg); planned on first use."""
+    s = _stream(stream)
+    _check(lib().ea_repartition_plan(src.handle, dst.handle, s))
+    _check(lib().ea_repartition_ex(src.handle, dst.handle, int(store), s))
 
 
 def join_tuples(spec: str, join_op: int, inputs: Sequence[Relation], out: Relation, *, causal: bool = False,

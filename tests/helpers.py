@@ -20,6 +20,24 @@ NP_STORAGE = {"f32": np.float32, "bf16": np.uint16, "f16": np.uint16}
 REL_FRO = 1e-3
 MAX_ABS_REL = 2e-2
 
+# End-to-end tolerance of a whole block chain (its last relation against the
+# oracle's chain, bf16 at the same boundaries).  Every stage alone is held to
+# REL_FRO on the GPU's own upstream relations; end to end, bf16 rounding flips
+# upstream are amplified by the softmax and the SwiGLU product, so even an
+# independent fp32 implementation misses REL_FRO.  tests/test_chain_tolerance_cpu.py
+# measures that implementation (torch library routines on the CPU) on the
+# full-size inputs and pins this value to between 1.25x and 2.5x its error.
+CHAIN_REL_FRO = 5e-3
+
+# End-to-end tolerance of each matrix chain (Section 6, chains A-E, every dim
+# divided by 64).  Deep chains compound rounding flips the same way: where two
+# values differ by d, their bf16 roundings differ by about sqrt(ulp * d), so a
+# small upstream difference grows at every boundary.  An independent fp32
+# chain (torch on the CPU) stays under REL_FRO / 3 on B, C and D, which are
+# held to REL_FRO; on A and E it exceeds that, and they take CHAIN_REL_FRO.
+# tests/test_chain_tolerance_cpu.py pins this split.
+CHAIN_END_TO_END = {"A": CHAIN_REL_FRO, "B": REL_FRO, "C": REL_FRO, "D": REL_FRO, "E": CHAIN_REL_FRO}
+
 
 def upload(stored: np.ndarray, dtype: str, partition) -> ea.Relation:
     """A device relation holding ``stored`` (dense, storage dtype) under ``partition``."""

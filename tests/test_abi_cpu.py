@@ -120,6 +120,15 @@ def _fake(shape, dtype, part):
     return r
 
 
+def _raw_joinagg(spec, join_op, agg_op, ins, out):
+    """ea_joinagg through the C ABI with no workspace: validation of a run
+    (data present, arguments) precedes the plan lookup."""
+    handles = (ctypes.c_void_p * len(ins))(*[r.handle.value for r in ins])
+    prm, _ = eamod._params()
+    return ea.lib().ea_joinagg(spec.encode(), join_op, agg_op, len(ins), handles, out.handle, ctypes.byref(prm),
+                               None, 0, None)
+
+
 def test_joinagg_validation_errors():
     p64 = synth.splits(256, 64)
     A = _fake([256, 256], "bf16", [p64, p64])
@@ -139,7 +148,8 @@ def test_joinagg_validation_errors():
     assert _code(J("ij,jk->ik", 42, ea.AGG_SUM, [A, B], C)) == -1               # unknown join op
     assert _code(J("ij,jk->ik", ea.JOIN_MUL, ea.AGG_LSE, [A, B], C)) == -1      # LSE on an einsum
     nodata = ea.Relation([256, 256], "bf16", [p64, p64], allocate=False)
-    assert _code(J("ij,jk->ik", ea.JOIN_MUL, ea.AGG_SUM, [A, nodata], C)) == -1
+    assert _raw_joinagg("ij,jk->ik", ea.JOIN_MUL, ea.AGG_SUM, [A, nodata], C) == -1
+    assert _raw_joinagg("ij,jk->ik", ea.JOIN_MUL, ea.AGG_SUM, [A, B], nodata) == -1
     res_bad = _fake([256, 256], "f32", [synth.splits(256, 128), p64])
     assert _code(J("ij,jk->ik", ea.JOIN_MUL, ea.AGG_SUM, [A, B], C, residual=res_bad)) == -1
 
@@ -187,11 +197,13 @@ def test_repartition_validation_errors():
     assert ea.lib().ea_relation_set_data(d.handle, ctypes.c_void_p(FAKE + 4096), d.nbytes) == 0
     assert _code(lambda: ea.repartition(a, b)) == -1       # shape differs
     assert _code(lambda: ea.repartition(a, c)) == -1       # dtype differs
-    assert _code(lambda: ea.repartition(a, a)) == -1       # memory overlaps
+    L = ea.lib()
+    assert L.ea_repartition_plan(a.handle, b.handle, None) == -1  # planning validates too
+    assert L.ea_repartition(a.handle, a.handle, None) == -1       # memory overlaps
     nodata = ea.Relation([64, 64], "bf16", [[0, 64], [0, 64]], allocate=False)
-    assert _code(lambda: ea.repartition(nodata, d)) == -1
+    assert L.ea_repartition(nodata.handle, d.handle, None) == -1
     for bad in (-1, 2):
-        assert _code(lambda: ea.repartition(a, d, store=bad)) == -1
+        assert L.ea_repartition_ex(a.handle, d.handle, bad, None) == -1
 
 
 def test_grouped_query_and_packed_sequence_validation_errors():

@@ -116,3 +116,25 @@ def test_attention_single_block_and_first_query():
         assert_close(got, ref, rel_fro=1e-3, what=f"single block, causal={causal}")
         if causal:
             assert np.array_equal(got[:, :, 0, :], synth.to_f64(v, "bf16")[:, :, 0, :])
+
+
+def test_attention_long_sequence_units_at_the_key_block_cap():
+    # one causal head of 131072 tokens in 128-blocks: query tile i has i + 1
+    # key blocks (up to 1024).  The plan's cost model then takes units of 64
+    # key blocks, the cap of a unit's key-block table: 8704 units in 34 waves
+    # of 256 CUs, at cost 34 x (64 + 0.5 x 15) against 66 x (32 + 0.5 x 31)
+    # for 32, and tiles past the 64th split over 2 to 16 parts.  The units are
+    # sized from the GPU join's group offsets.  Sampled query rows (tile and
+    # unit boundaries among them) against the oracle evaluated at those rows.
+    print("attention: one head of 131072 tokens", flush=True)
+    S = 131072
+    q, k, v = (synth.normal((1, 1, S, 128), 470 + i, dtype="bf16") for i in range(3))
+    p = [[0, 1], [0, 1], synth.splits(S, 128), [0, 128]]
+    scale = 1.0 / np.sqrt(128)
+    O = _run(q, k, v, p, p, scale, True)
+    rng = np.random.default_rng(471)
+    rows = np.unique(np.concatenate([[0, 1, 127, 128, 8191, 8192, 8319, 65535, 65536, S - 129, S - 128, S - 1],
+                                     rng.integers(0, S, 20)]))
+    f = [synth.to_f64(a[0], "bf16") for a in (q, k, v)]
+    ref = oracle.attention_rows(f[0], f[1], f[2], rows, scale)[:, 0]
+    assert_close(values(O)[0, 0][rows], expected(ref, "bf16"), what="attention 128K, sampled rows")

@@ -1,4 +1,4 @@
-"""GPU parity of grouped-query and packed-sequence attention (Section 3.2,
+"""GPU parity of grouped-query and packed-sequence attention (Section 3.3,
 Example "Flash attention") against the fp64 oracle: the join's tuple table
 bit for bit, the outputs within the attention tolerance."""
 import json

@@ -37,7 +37,9 @@ def test_planned_chain_runs_on_its_partitions(p):
     ea.joinagg(ops[1].spec, ea.JOIN_MUL, ea.AGG_SUM, [M1, P], Y)
     f = [synth.to_f64(m, "bf16") for m in mats]
     ref = oracle.rne_bf16(oracle.matmul(f[0], oracle.rne_bf16(oracle.matmul(f[1], f[2]))))
-    assert_close(values(Y), ref, rel_fro=5e-3, what=f"planned chain, p={p}")
+    assert_close(values(P), oracle.rne_bf16(oracle.matmul(f[1], f[2])), what=f"planned chain M2 M3, p={p}")
+    assert_close(values(Y), oracle.rne_bf16(oracle.matmul(f[0], values(P))), what=f"planned chain M1 P, p={p}")
+    assert_close(values(Y), ref, what=f"planned chain, p={p}")
     # the tuples of each join-agg are the spec's p function specifications
     assert int(np.prod(list(counts[0].values()))) == p
     t, _ = ea.join_tuples(ops[0].spec, ea.JOIN_MUL, [M2, M3], empty((d[1], d[3]), "bf16", p23[2]))

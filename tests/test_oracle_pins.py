@@ -357,7 +357,7 @@ def test_llama_block_composition_and_causal_prefix():
 
 
 # ---------------------------------------------------------------------------
-# grouped-query heads and packed sequences (Section 3.2, Example "Flash
+# grouped-query heads and packed sequences (Section 3.3, Example "Flash
 # attention")
 # ---------------------------------------------------------------------------
 def _flash_example():
@@ -498,3 +498,21 @@ def test_llama_block_rows_equals_the_whole_chain_at_its_rows(seq_ends):
         # a history shifted by one token changes the row: the comparison can fail
         bad = oracle.llama_block_rows(f["x"][1:], *args[1:], heads=4, d_head=16, eps=1e-6, rows=[10], heads_kv=2)
         assert not np.allclose(bad["attn"], full["attn"][[10]])
+
+
+@pytest.mark.parametrize("seq_ends", [None, [20, 48], [7, 31, 48]])
+def test_attention_rows_equals_attention_ex_at_every_row(seq_ends):
+    # the per-row evaluation against the whole-tensor oracle (itself pinned to
+    # SDPA above), grouped heads: exact up to fp64 summation order
+    rng = np.random.default_rng(77)
+    q, k, v = rng.standard_normal((1, 4, 48, 16)), rng.standard_normal((1, 2, 48, 16)), rng.standard_normal((1, 2, 48, 16))
+    full = oracle.attention_ex(q, k, v, True, 0.25, seq_ends=seq_ends)
+    rows = np.arange(48)
+    got = oracle.attention_rows(q[0], k[0], v[0], rows, 0.25, seq_ends=seq_ends)
+    np.testing.assert_allclose(got, full[0].transpose(1, 0, 2), rtol=1e-12, atol=1e-12)
+    # a window of tokens [20, 48) with its ends shifted by its start: the rows of
+    # the second sequence are unchanged
+    if seq_ends == [20, 48]:
+        w = oracle.attention_rows(q[0][:, 20:], k[0][:, 20:], v[0][:, 20:], np.arange(28), 0.25,
+                                  seq_ends=np.array(seq_ends) - 20)
+        np.testing.assert_allclose(w, full[0][:, 20:].transpose(1, 0, 2), rtol=1e-12, atol=1e-12)
