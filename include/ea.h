@@ -239,6 +239,26 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in,
                const ea_relation* const* in, ea_relation* out,
                const ea_params* params, void* workspace, int64_t ws_bytes, void* stream);
 
+/* ---- join-agg without allocation ---------------------------------------
+   For callers that cannot allocate device memory: code under HIP graph
+   capture, tight serving loops, harnesses that forbid hipMalloc.  Runs a
+   join-agg that ea_joinagg_workspace planned earlier on this device, like
+   ea_joinagg, with the workspace taken from a library-internal device array
+   of EA_NOALLOC_SCRATCH_BYTES (64 MiB) instead of a caller buffer.  It calls
+   no hipMalloc, hipFree or allocating library routine: the array is part of
+   the library's code object, and each GPU the library runs on holds its copy
+   until the process ends.  The plan's counter words in it are cleared by a
+   fill kernel on `stream` before the join-agg's kernels; the partials need no
+   initial value.  Every call on one GPU shares that GPU's array, so calls that
+   may overlap in time on one GPU (several streams or threads) race: issue
+   them in one stream order.  Asynchronous on `stream`.  Errors as ea_joinagg
+   (EA_ERR_NOPLAN if not planned), plus EA_ERR_CAPACITY when the plan's
+   workspace exceeds EA_NOALLOC_SCRATCH_BYTES. */
+#define EA_NOALLOC_SCRATCH_BYTES (64LL << 20)
+int ea_joinagg_noalloc(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in,
+                       const ea_relation* const* in, ea_relation* out,
+                       const ea_params* params, void* stream);
+
 /* Plan a join-agg configuration (the join of Section 3.2 step 1, resolved
    once as a compiled program would) and report the workspace its
    ea_joinagg calls need.  Arguments as ea_joinagg; relation data may be

@@ -1206,6 +1206,44 @@ int lookup_run(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
   return prepare(spec, join_op, agg_op, n_in, in, out, params, true, false, s, &sp, oi, plan);
 }
 
+// ---------------------------------------------------------------------------
+// Split-key workspace of ea_joinagg_noalloc: a fixed device array in the
+// library's code object, so that the entry point allocates nothing.  Each
+// device holds its own copy at its own address, found once per device with
+// hipGetSymbolAddress; host code uses that address only, never the array's
+// name (a host-side stand-in).
+// ---------------------------------------------------------------------------
+constexpr int64_t kNoAllocScratchBytes = EA_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+__global__ void zero_words_kernel(int32_t* p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+std::mutex g_scratch_mu;
+std::map<int, char*>& scratch_addr() {
+  static auto* m = new std::map<int, char*>();  // device -> its copy's address; intentionally leaked at exit
+  return *m;
+}
+
+// Address of the current device's copy of the array (looked up on the
+// device's first call, with that device current).
+int noalloc_scratch(char** out) {
+  int dev = 0;
+  EA_HIP_TRY(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  auto it = scratch_addr().find(dev);
+  if (it == scratch_addr().end()) {
+    void* p = nullptr;
+    EA_HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p || (uintptr_t)p % 256) return fail(EA_ERR_HIP, "scratch array of device %d at %p", dev, p);
+    it = scratch_addr().emplace(dev, (char*)p).first;
+  }
+  *out = it->second;
+  return EA_OK;
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -1552,6 +1590,34 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, 
                   (long long)need);
   }
   e = run_planned(plan, join_op, n_in, in, out, params, oi, need ? (char*)workspace : nullptr, s);
+  if (e) return e;
+  return ok();
+}
+
+int ea_joinagg_noalloc(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in, const ea_relation* const* in,
+                       ea_relation* out, const ea_params* params, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  OpInfo oi;
+  Plan* plan = nullptr;
+  int e = lookup_run(spec, join_op, agg_op, n_in, in, out, params, s, &oi, &plan);
+  if (e) return e;
+  const int64_t need = plan->ws_bytes();
+  char* ws = nullptr;
+  if (need) {
+    if (need > kNoAllocScratchBytes)
+      return fail(EA_ERR_CAPACITY, "this join-agg needs %lld bytes of workspace, above the %lld of ea_joinagg_noalloc",
+                  (long long)need, (long long)kNoAllocScratchBytes);
+    e = noalloc_scratch(&ws);
+    if (e) return e;
+    // the counters start at zero whatever an earlier call left (a fill
+    // kernel, not a memset node, so that the call can be captured)
+    if (plan->ws_counters) {
+      const int64_t n = plan->ws_counters;
+      hipLaunchKernelGGL(zero_words_kernel, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0, s, (int32_t*)ws, n);
+      EA_HIP_TRY(hipGetLastError());
+    }
+  }
+  e = run_planned(plan, join_op, n_in, in, out, params, oi, ws, s);
   if (e) return e;
   return ok();
 }

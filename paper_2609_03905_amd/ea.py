@@ -67,6 +67,7 @@ def lib() -> ctypes.CDLL:
         L.ea_joinagg.argtypes = [ctypes.c_char_p, i32, i32, i32, P(vp), vp, P(_Params), vp, i64, vp]
         L.ea_joinagg_workspace.argtypes = [ctypes.c_char_p, i32, i32, i32, P(vp), vp, P(_Params), P(i64), vp]
         L.ea_repartition_plan.argtypes = [vp, vp, vp]
+        L.ea_joinagg_noalloc.argtypes = [ctypes.c_char_p, i32, i32, i32, P(vp), vp, P(_Params), vp]
         L.ea_join_tuples.argtypes = [ctypes.c_char_p, i32, i32, P(vp), vp, P(_Params), vp, i64, vp, i64,
                                      P(i64), P(i64), vp]
         L.ea_repartition.argtypes = [vp, vp, vp]
@@ -265,6 +266,18 @@ def joinagg(spec: str, join_op: int, agg_op: int, inputs: Sequence[Relation], ou
         ws, nbytes = ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size()
     _check(lib().ea_joinagg(spec_b, join_op, agg_op, len(inputs), handles, out.handle, ctypes.byref(prm), ws, nbytes,
                             s))
+
+
+def joinagg_noalloc(spec: str, join_op: int, agg_op: int, inputs: Sequence[Relation], out: Relation, *,
+                    eps: float = 0.0, scale: float = 0.0, causal: bool = False, residual: Relation | None = None,
+                    store: int = 0, gqa_group: int = 0, seq_ends=None, stream=None) -> None:
+    """ea_joinagg_noalloc: run a join-agg planned earlier (joinagg_workspace)
+    with the library's own per-device workspace array; allocates nothing.
+    Calls that may overlap in time on one GPU race on that array."""
+    handles = _arr(ctypes.c_void_p, [r.handle.value for r in inputs])
+    prm, _ends = _params(eps, scale, causal, store, residual, gqa_group, seq_ends)
+    _check(lib().ea_joinagg_noalloc(spec.encode(), join_op, agg_op, len(inputs), handles, out.handle,
+                                    ctypes.byref(prm), _stream(stream)))
 
 
 def repartition_plan(src: Relation, dst: Relation, stream=None) -> None:
