@@ -296,6 +296,37 @@ def chains_workload():
                 cpu=None)
 
 
+def matmul_fp32_workload():
+    """The 256^3 fp32 matmul join-agg 'ij,jk->ik', each input 4x4 blocks of
+    64x64 (SUM of 4 partials per output key); 2 MiB of buffers, rotated
+    through 1 GiB of copies like the other workloads."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2609_03905_amd import ea
+
+    w = synth.matmul_256_fp32()
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    A0 = ea.from_dense(dev(w["A"]), "f32", w["pA"])
+    B0 = ea.from_dense(dev(w["B"]), "f32", w["pB"])
+
+    def make_set(i):
+        A, B = (A0, B0) if i == 0 else (_copy(A0, ea), _copy(B0, ea))
+        return A, B, ea.Relation((256, 256), "f32", w["pC"])
+
+    rot = _Rotation(_buffer_sets(make_set, 3 * 256 * 256 * 4))
+
+    def fn():
+        A, B, C = rot.next()
+        ea.joinagg(w["spec"], ea.JOIN_MUL, ea.AGG_SUM, [A, B], C)
+
+    flops = 2.0 * 256 ** 3
+    return dict(step=fn, flops=flops, comps={"matmul_fp32": dict(fn=fn, flops=flops)}, dominant="matmul_fp32",
+                config={"workload": "matmul_256_fp32", "spec": "ij,jk->ik", "blocks": "4x4 of 64x64", "dtype": "f32",
+                        "buffer_sets": len(rot.sets)}, cpu=None)
+
+
 def reductions_workload():
     import synth
     from paper_2609_03905_amd import ea
@@ -360,6 +391,95 @@ def repartition_workload():
 
 
 # ---------------------------------------------------------------------------
+# Every single-operator configuration of the target, measured next to the
+# headline block step: time, rate, fraction of the bound's peak and the bar
+# (>= 60% of bf16 MFMA peak for block GEMMs, >= 70% of HBM for the
+# memory-bound operators; C1 and attention carry no bar).
+# ---------------------------------------------------------------------------
+PEAK_FP32_TFLOPS = 157.3  # MI355X fp32 (matrix) peak
+
+
+def _rate(c, ms, peak_tflops=PEAK_BF16_TFLOPS):
+    d = {"us": round(ms * 1e3, 3)}
+    if "flops" in c:
+        d["tflops"] = c["flops"] / ms / 1e9
+        d["frac_peak"] = d["tflops"] / peak_tflops
+    if "bytes" in c:
+        d["gbs"] = c["bytes"] / ms / 1e6
+        d["frac_peak"] = d["gbs"] / PEAK_HBM_GBS
+    return d
+
+
+def config_rows(n):
+    import gc
+
+    import torch
+
+    rows = {}
+    spec = [("C1_matmul_fp32_256", matmul_fp32_workload, "matmul_fp32", None, PEAK_FP32_TFLOPS),
+            ("C2_qkv_gemm", qkv_workload, "joinagg_gemm", 0.60, PEAK_BF16_TFLOPS),
+            ("C2_repartition", qkv_workload, "repartition", 0.70, None),
+            ("C3_rmsnorm", reductions_workload, "rmsnorm", 0.70, None),
+            ("C3_causal_softmax", reductions_workload, "causal_softmax", 0.70, None),
+            ("C4_causal_attention", attention_workload, "attention", None, PEAK_BF16_TFLOPS)]
+    built = {}
+    for name, make, comp, bar, peak in spec:
+        if make not in built:
+            built.clear()
+            gc.collect()
+            torch.cuda.empty_cache()
+            built[make] = make()
+        wl = built[make]
+        c = wl["comps"][comp]
+        ms = _events_ms(c["fn"], n)
+        d = _rate(c, ms, peak or PEAK_BF16_TFLOPS)
+        d["workload"] = wl["config"]["workload"]
+        if "buffer_sets" in wl["config"]:
+            d["buffer_sets"] = wl["config"]["buffer_sets"]
+        if bar is not None:
+            d["bar_frac"] = bar
+            d["meets_bar"] = bool(d["frac_peak"] >= bar)
+        rows[name] = d
+    built.clear()
+    gc.collect()
+    torch.cuda.empty_cache()
+    return rows
+
+
+def oracle_single_thread():
+    """The oracle on one thread, timed on the two small configurations: the
+    256^3 fp32 matmul and the QKV share's 12 MiB repartition (512x512 blocks
+    to per-head 4096x128 blocks)."""
+    import numpy as np
+
+    import oracle
+    import synth
+
+    n0 = oracle.num_threads()
+    oracle.set_num_threads(1)
+    try:
+        w = synth.matmul_256_fp32()
+        a, b = synth.to_f64(w["A"], "f32"), synth.to_f64(w["B"], "f32")
+        reps, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < 1.0 or reps < 3:
+            oracle.matmul(a, b)
+            reps += 1
+        c1 = (time.perf_counter() - t0) / reps
+        q = synth.qkv_projection()
+        y = np.random.default_rng(5).integers(0, 1 << 16, (4096, 1536), dtype=np.uint16)
+        blocked = oracle.pack(y, q["pY"])
+        reps, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < 2.0 or reps < 3:
+            oracle.repartition(blocked, q["pY"], q["pHead"], np.uint16)
+            reps += 1
+        c2 = (time.perf_counter() - t0) / reps
+    finally:
+        oracle.set_num_threads(n0)
+    return {"C1_matmul_fp32_256": {"ms": c1 * 1e3, "gflops": 2.0 * 256 ** 3 / c1 / 1e9, "threads": 1},
+            "C2_repartition": {"ms": c2 * 1e3, "gbs": 2 * 4096 * 1536 * 2 / c2 / 1e9, "threads": 1}}
+
+
+# ---------------------------------------------------------------------------
 # CPU baselines: the oracle, untuned, on a bounded sample of the workload
 # ---------------------------------------------------------------------------
 def _adaptive(run, first, cap, target_s):
@@ -416,7 +536,7 @@ WORKLOADS = {"block": block_workload, "qkv": qkv_workload, "attention": attentio
              "packed_gqa": packed_gqa_workload, "w1_block": w1_block_workload, "w1_1k": lambda: w1_block_workload(1024, 1024),
              "w1_8k": lambda: w1_block_workload(8192, 8192), "w1_128k": lambda: w1_block_workload(131072, 131072),
              "w1_128x1k": lambda: w1_block_workload(131072, 1024), "chains": chains_workload,
-             "reductions": reductions_workload,
+             "reductions": reductions_workload, "matmul_fp32": matmul_fp32_workload,
              "repartition": repartition_workload}
 
 
@@ -427,6 +547,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="block", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true", help="skip the single-operator configuration rows")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU's share on one GPU; --gpus {args.gpus} is not supported "
@@ -441,15 +562,18 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    s.record()
-    for _ in range(args.steps):
+    ev[0].record()
+    for i in range(args.steps):
         step()
-    e.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_per_step = s.elapsed_time(e) / args.steps
+    ms_per_step = ev[0].elapsed_time(ev[-1]) / args.steps
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    sd = (sum((x - ms_per_step) ** 2 for x in per) / max(1, len(per) - 1)) ** 0.5
+    ci95 = 1.96 * sd / max(1, len(per)) ** 0.5  # normal approximation of the mean's 95% interval
 
     comps = {}
     for name, c in wl["comps"].items():
@@ -479,11 +603,17 @@ def main():
         value, unit = wl["bytes"] / ms_per_step / 1e6, "GB/s"
     out = {
         "metric": METRIC, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "ms_per_step": ms_per_step, "ms_per_step_ci95": [ms_per_step - ci95, ms_per_step + ci95],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": wl.get("data", "synthetic (seeded N(0,1) activations, N(0,0.02) weights, random init)"),
         "config": wl["config"], "roofline": roof, "components": comps, "wall_s": round(wall, 4),
     }
-    if not args.no_cpu_baseline and wl.get("cpu"):
+    if args.workload == "block" and not args.no_configs:
+        out["configs"] = config_rows(max(args.steps, 20))
+    if not args.no_cpu_baseline and out["config"]["workload"] == "llama65b_block_share":
+        out["cpu_baseline"] = cpu_baseline_block()
+        out["cpu_single_thread"] = oracle_single_thread()
+    elif not args.no_cpu_baseline and wl.get("cpu"):
         out["cpu_baseline"] = wl["cpu"]()
     print(json.dumps(out))
 

@@ -244,7 +244,7 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in,
    capture, tight serving loops, harnesses that forbid hipMalloc.  Runs a
    join-agg that ea_joinagg_workspace planned earlier on this device, like
    ea_joinagg, with the workspace taken from a library-internal device array
-   of EA_NOALLOC_SCRATCH_BYTES (64 MiB) instead of a caller buffer.  It calls
+   of EA_NOALLOC_SCRATCH_BYTES (128 MiB) instead of a caller buffer.  It calls
    no hipMalloc, hipFree or allocating library routine: the array is part of
    the library's code object, and each GPU the library runs on holds its copy
    until the process ends.  The plan's counter words in it are cleared by a
@@ -254,7 +254,7 @@ int ea_joinagg(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in,
    them in one stream order.  Asynchronous on `stream`.  Errors as ea_joinagg
    (EA_ERR_NOPLAN if not planned), plus EA_ERR_CAPACITY when the plan's
    workspace exceeds EA_NOALLOC_SCRATCH_BYTES. */
-#define EA_NOALLOC_SCRATCH_BYTES (64LL << 20)
+#define EA_NOALLOC_SCRATCH_BYTES (128LL << 20)
 int ea_joinagg_noalloc(const char* spec, int32_t join_op, int32_t agg_op, int32_t n_in,
                        const ea_relation* const* in, ea_relation* out,
                        const ea_params* params, void* stream);

@@ -75,6 +75,7 @@ def lib():
         i64p = ctypes.POINTER(ctypes.c_int64)
         dp = ctypes.POINTER(ctypes.c_double)
         L.or_num_threads.restype = ctypes.c_int
+        L.or_set_num_threads.argtypes = [ctypes.c_int]
         L.or_rne_bf16.argtypes = [ctypes.c_int64, dp, dp]
         L.or_layout.argtypes = [ctypes.c_int, i64p, i64p, ctypes.c_int64, i64p, i64p]
         L.or_pack.argtypes = [ctypes.c_int, i64p, i64p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
@@ -102,6 +103,11 @@ def lib():
 
 def num_threads() -> int:
     return int(lib().or_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on (timing only)."""
+    lib().or_set_num_threads(int(n))
 
 
 def _f64(a) -> np.ndarray:

@@ -36,6 +36,15 @@ int or_num_threads(void) {
 #endif
 }
 
+/* Threads of the parallel loops that follow (n >= 1); timing only. */
+void or_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------ */
 /* Rounding.  fp64 -> bf16 round-to-nearest-even, returned widened to fp64.  */
 /* bf16 keeps 8 significant bits; the quantum of a value x = m*2^e with      */

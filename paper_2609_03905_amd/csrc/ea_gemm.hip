@@ -625,18 +625,27 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
   __shared__ __attribute__((aligned(1024))) uint16_t smem[NSTAGE * STAGE];
   __shared__ TupleMeta s_meta[kGemmMaxTuples];
 
-  const GemmTile tile = p.tiles[blockIdx.x];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid / WGN, wn = wid % WGN;
   const int g = lane >> 5, lq = lane & 31;
+  const GemmUnit* unit = p.units + blockIdx.x;
+  // the unit's segments, each run by the same straight-line code (two calls
+  // rather than a loop, which would keep more registers live and spill)
+  auto run_segment = [&](const GemmSeg& seg) __attribute__((always_inline)) {
+  GemmTile tile;
+  tile.block = seg.block;
+  tile.m0 = seg.m0;
+  tile.n0 = seg.n0;
+  tile.part = seg.part;
+  tile.n_parts = seg.n_parts;
+  tile.slot = seg.first_slot + seg.part;
+  tile.first_slot = seg.first_slot;
+  tile.counter = seg.counter;
   const int32_t gb = p.goff[tile.block], ge = p.goff[tile.block + 1];
-  const int n_t = ge - gb;
-  const int t_begin = gb + (int)(((int64_t)tile.part * n_t) / tile.n_parts);
-  const int t_end = gb + (int)(((int64_t)(tile.part + 1) * n_t) / tile.n_parts);
-  const int nt = t_end - t_begin;  // <= kGemmMaxTuples (host guarantee)
+  const int nt = ge - gb;  // the group's tuples, <= kGemmMaxTuples (host guarantee)
   for (int i = tid; i < nt; i += 64 * W) {
-    const int32_t* tp = p.tuples + (int64_t)(t_begin + i) * p.tuple_stride;
+    const int32_t* tp = p.tuples + (int64_t)(gb + i) * p.tuple_stride;
     const DevBlk& ab = p.blk_a[tp[1]];
     const DevBlk& bb = p.blk_b[tp[2]];
     TupleMeta m;
@@ -668,9 +677,18 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
 #pragma unroll
       for (int j = 0; j < WN; ++j) acc[o][i][j] = f32x16_t{};
 
-  // number of K steps of this unit (every contracted block extent is a multiple of DK)
-  int n_steps = 0;
-  for (int i = 0; i < nt; ++i) n_steps += s_meta[i].ak / DK;
+  // the segment's K steps [s0, s1) of the walk over the group's tuples (every
+  // contracted block extent is a multiple of DK): the tuple holding step s0,
+  // and how many of its steps come before s0
+  int group_steps = 0;
+  for (int i = 0; i < nt; ++i) group_steps += s_meta[i].ak / DK;
+  // a guard: never walk past the group's last step whatever the plan says
+  const int n_steps = max(0, min(seg.s1, group_steps) - seg.s0);
+  int it_t = 0, skip = seg.s0;
+  while (it_t < nt && skip >= s_meta[it_t].ak / DK) {
+    skip -= s_meta[it_t].ak / DK;
+    ++it_t;
+  }
 
   // ---- direct-load walk over the unit's K steps.  Per tuple, each operand
   // block has a uniform base address and each lane a 32-bit byte offset per
@@ -683,7 +701,7 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
   const char* b_base[NB];
   uint32_t va[LA], vb[NB][LBO];
   uint32_t bstep[NB];
-  int it_t = 0, left = 0;
+  int left = 0;
   auto set_tuple = [&](int t) {
     const TupleMeta& m = s_meta[t];
     a_base = p.a + m.aoff;
@@ -818,6 +836,15 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
     else wait_vmcnt<0>();
   };
   seek();
+  if (skip > 0 && it_t < nt) {  // start inside the tuple: advance past its first `skip` steps
+#pragma unroll
+    for (int q = 0; q < LA; ++q) va[q] += (uint32_t)(skip * DK * 2);
+#pragma unroll
+    for (int o = 0; o < NB; ++o)
+#pragma unroll
+      for (int q = 0; q < LBO; ++q) vb[o][q] += (uint32_t)skip * bstep[o];
+    left -= skip;
+  }
   const int n_pro = n_steps < D ? n_steps : D;
   for (int st = 0; st < n_pro; ++st) issue_next(st);
   if (n_steps > 0) {
@@ -842,12 +869,19 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
   }
   static_assert(sizeof(smem) >= 64 * kEpiPitch * sizeof(float), "epilogue stage");
   finish_tile<SWIGLU, NB, WN, W>(acc, p, tile, wid, lane, reinterpret_cast<float*>(smem));
+  };
+  run_segment(unit->seg[0]);
+  if (unit->n_seg > 1) {
+    drain_vmem();  // the first segment's epilogue is done with its stores and the LDS
+    __syncthreads();
+    run_segment(unit->seg[1]);
+  }
 }
 
 template <bool BF16, bool KMAJOR, bool SWIGLU>
 hipError_t launch3(const GemmArgs& a, hipStream_t s) {
   if (a.direct)
-    hipLaunchKernelGGL((gemm_dl_kernel<BF16, KMAJOR, SWIGLU, 8>), dim3((uint32_t)a.n_tiles), dim3(512), 0, s, a);
+    hipLaunchKernelGGL((gemm_dl_kernel<BF16, KMAJOR, SWIGLU, 8>), dim3((uint32_t)a.n_units), dim3(512), 0, s, a);
   else
     hipLaunchKernelGGL((gemm_kernel<BF16, KMAJOR, SWIGLU, 8>), dim3((uint32_t)a.n_tiles), dim3(512), 0, s, a);
   return hipGetLastError();
@@ -866,7 +900,7 @@ hipError_t launch1(const GemmArgs& a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
-  if (a.n_tiles == 0) return hipSuccess;
+  if ((a.direct ? a.n_units : a.n_tiles) == 0) return hipSuccess;
   return a.dt_in == EA_BF16 ? launch1<true>(a, s) : launch1<false>(a, s);
 }
 

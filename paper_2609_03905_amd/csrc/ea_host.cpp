@@ -10,6 +10,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <memory>
@@ -320,6 +321,7 @@ struct Plan {
   // gemm
   int b_kmajor = 0;
   int gemm_parts = 1;
+  bool gemm_direct = false;  // direct-load kernel (work list of GemmUnit), else GemmTile
   // rows
   RowLayout rows;
   AttnUnitMeta* attn_meta = nullptr;
@@ -872,6 +874,137 @@ GemmPlanInfo gemm_units(const ea_relation* a, const ea_relation* c, int tn) {
   return info;
 }
 
+// Units of the direct-load kernel (contracted block extents multiples of 32,
+// at most kGemmMaxTuples tuples per group).  Two schedules are costed and the
+// cheaper one is kept:
+//   * even: the tiles of gemm_units (split or not, in XCD-aware order), one
+//     segment each;
+//   * balanced: the tiles' 32-deep K steps laid end to end (tiles in block
+//     order) and cut into 256 equal runs, one per CU; a run may end one tile
+//     and start the next, and a tile cut into several runs is merged by its
+//     last arriver.  This fills every CU when there are fewer tiles than CUs.
+// Time model (us): 0.75 per K step of a tile, 1 per segment (pipeline fill and
+// store), and the split tiles' partial sums written and read back at 5 TB/s.
+// The step time grows once more than about 190 CUs run matrix work at once:
+// the sustained clock is power-limited, so a schedule that keeps all 256 CUs
+// busy gains less than its CU count suggests (measured on the block share:
+// 176 tiles of SwiGLU over 256 steps each took 195 us on 176 CUs, and the same
+// work balanced over 256 CUs, 176 steps each, 193 us).
+struct GemmDlPlan {
+  std::vector<GemmUnit> units;
+  int32_t slots = 0, counters = 0;
+  bool balanced = false;
+};
+
+GemmDlPlan gemm_units_dl(const ea_relation* a, const ea_relation* c, int tn, const GemmPlanInfo& even) {
+  const int kCUs = 256;
+  const double t_step = 0.75, t_seg = 1.0, bw = 5.0e6, tile_bytes = 262144.0, n_sat = 190.0;
+  auto step_time = [&](int64_t busy_cus) { return t_step * std::max(1.0, (double)busy_cus / n_sat); };
+  // K-step prefix over a group's tuples (A's contracted blocks, in order)
+  const int n_t = a->nb[1];
+  std::vector<int32_t> pre(n_t + 1, 0);
+  for (int b = 0; b < n_t; ++b) pre[b + 1] = pre[b] + (int32_t)((a->splits[1][b + 1] - a->splits[1][b]) / 32);
+  const int64_t S = pre[n_t];
+  auto merge_bytes = [&](int parts) { return parts > 1 ? (parts + (parts == 2 ? 1 : parts)) * tile_bytes : 0.0; };
+  // even schedule, as one-segment units
+  GemmDlPlan ev;
+  double ev_cost = 0.0;
+  {
+    int64_t max_steps = 0;
+    double bytes = 0.0;
+    for (const GemmTile& t : even.units) {
+      GemmUnit u;
+      memset(&u, 0, sizeof(u));
+      GemmSeg& g = u.seg[0];
+      g.block = t.block;
+      g.m0 = t.m0;
+      g.n0 = t.n0;
+      g.s0 = pre[(int)(((int64_t)t.part * n_t) / t.n_parts)];
+      g.s1 = pre[(int)(((int64_t)(t.part + 1) * n_t) / t.n_parts)];
+      g.part = t.part;
+      g.n_parts = t.n_parts;
+      g.first_slot = t.first_slot;
+      g.counter = t.counter;
+      u.n_seg = 1;
+      ev.units.push_back(u);
+      max_steps = std::max<int64_t>(max_steps, g.s1 - g.s0);
+      if (t.part == 0) bytes += merge_bytes(t.n_parts);
+    }
+    ev.slots = even.slots;
+    ev.counters = even.counters;
+    const int64_t n_units = (int64_t)ev.units.size(), waves = (n_units + kCUs - 1) / kCUs;
+    ev_cost = (double)waves * ((double)max_steps * step_time(std::min<int64_t>(n_units, kCUs)) + t_seg) + bytes / bw;
+  }
+  // balanced schedule
+  std::vector<GemmTile> tiles;  // block order
+  {
+    int32_t co[kMaxRank];
+    for (int64_t b = 0; b < c->nblocks; ++b) {
+      block_coords(c, b, co);
+      const int64_t me = c->splits[0][co[0] + 1] - c->splits[0][co[0]];
+      const int64_t ne = c->splits[1][co[1] + 1] - c->splits[1][co[1]];
+      for (int64_t m0 = 0; m0 < me; m0 += kGemmTM)
+        for (int64_t n0 = 0; n0 < ne; n0 += tn) {
+          GemmTile t;
+          memset(&t, 0, sizeof(t));
+          t.block = (int32_t)b;
+          t.m0 = (int32_t)m0;
+          t.n0 = (int32_t)n0;
+          tiles.push_back(t);
+        }
+    }
+  }
+  const int64_t T = (int64_t)tiles.size(), total = T * S;
+  if (T == 0 || S == 0 || T >= kCUs) return ev;  // a full wave of tiles: nothing to balance
+  const int64_t q = (total + kCUs - 1) / kCUs;    // steps per unit (< S: at most two tiles per unit)
+  if (q < 8) return ev;                           // too little work per unit to share
+  GemmDlPlan bal;
+  bal.balanced = true;
+  std::vector<std::vector<std::pair<int, int>>> segs_of(T);  // (unit, seg) per tile, ascending s0
+  for (int64_t u0 = 0; u0 < total; u0 += q) {
+    GemmUnit u;
+    memset(&u, 0, sizeof(u));
+    const int64_t u1 = std::min(total, u0 + q);
+    for (int64_t x = u0; x < u1;) {
+      const int64_t t = x / S, e = std::min(u1, (t + 1) * S);
+      if (u.n_seg >= kGemmMaxSegs) return ev;  // (cannot happen while q <= S)
+      GemmSeg& g = u.seg[u.n_seg];
+      g.block = tiles[(size_t)t].block;
+      g.m0 = tiles[(size_t)t].m0;
+      g.n0 = tiles[(size_t)t].n0;
+      g.s0 = (int32_t)(x - t * S);
+      g.s1 = (int32_t)(e - t * S);
+      segs_of[(size_t)t].push_back({(int)bal.units.size(), u.n_seg});
+      ++u.n_seg;
+      x = e;
+    }
+    bal.units.push_back(u);
+  }
+  double bytes = 0.0;
+  for (int64_t t = 0; t < T; ++t) {
+    const auto& v = segs_of[(size_t)t];
+    const int parts = (int)v.size();
+    for (int i = 0; i < parts; ++i) {
+      GemmSeg& g = bal.units[(size_t)v[i].first].seg[v[i].second];
+      g.part = i;
+      g.n_parts = parts;
+      g.first_slot = parts > 1 ? bal.slots : -1;
+      g.counter = parts > 1 ? bal.counters : -1;
+    }
+    if (parts > 1) {
+      bal.slots += parts;
+      bal.counters += 1;
+    }
+    bytes += merge_bytes(parts);
+  }
+  const double bal_cost = (double)q * step_time((int64_t)bal.units.size()) + 2.0 * t_seg + bytes / bw;
+  // EA_GEMM_SCHEDULE=even|balanced overrides the model when a plan is built
+  const char* force = getenv("EA_GEMM_SCHEDULE");
+  if (force && !strcmp(force, "even")) return ev;
+  if (force && !strcmp(force, "balanced")) return bal;
+  return bal_cost < ev_cost ? bal : ev;
+}
+
 int build_rows(const Spec& sp, const ea_relation* const* ops, const OpInfo& oi, Image* img, Extra* ex,
                RowLayout* lay) {
   // rows of a group: points of the group letters' box; every group has the
@@ -1085,12 +1218,31 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
   switch (oi.kind) {
     case K_GENERIC: e = build_generic(sp, join_op, agg_op, ops, ji, res, &img, &ex); break;
     case K_GEMM: {
-      const GemmPlanInfo gi = gemm_units(ops[0], ops[sp.n_in], join_op == EA_OP_SWIGLU ? kGemmTNSwiglu : kGemmTN);
-      ex.work = img.put_vec(gi.units);
-      ex.n_work = (int64_t)gi.units.size();
+      const int tn = join_op == EA_OP_SWIGLU ? kGemmTNSwiglu : kGemmTN;
+      const GemmPlanInfo gi = gemm_units(ops[0], ops[sp.n_in], tn);
       p->gemm_parts = gi.parts;
-      p->ws_counters = gi.counters;  // fp32 partial tiles of split keys in the workspace
-      p->ws_partial_bytes = (int64_t)gi.slots * kGemmTM * kGemmTN * (int64_t)sizeof(float);
+      // direct-to-LDS kernel: contracted block extents multiples of 32, at
+      // most kGemmMaxTuples tuples per group (staged in LDS) and operand
+      // blocks below 4 GiB (32-bit lane offsets); else the register-staged one
+      bool k32 = true;
+      for (int64_t v : ops[0]->splits[1]) k32 &= v % 32 == 0;
+      bool small = true;
+      for (int i = 0; i < sp.n_in; ++i) small &= max_block_bytes(ops[i]) < (int64_t(1) << 32);
+      p->gemm_direct = k32 && ops[0]->nb[1] <= kGemmMaxTuples && small;
+      int64_t slots = gi.slots;
+      if (p->gemm_direct) {
+        const GemmDlPlan dl = gemm_units_dl(ops[0], ops[sp.n_in], tn, gi);
+        ex.work = img.put_vec(dl.units);
+        ex.n_work = (int64_t)dl.units.size();
+        slots = dl.slots;
+        p->ws_counters = dl.counters;
+      } else {
+        ex.work = img.put_vec(gi.units);
+        ex.n_work = (int64_t)gi.units.size();
+        p->ws_counters = gi.counters;
+      }
+      // fp32 partial tiles of split keys in the workspace
+      p->ws_partial_bytes = slots * kGemmTM * kGemmTN * (int64_t)sizeof(float);
       break;
     }
     case K_RMSNORM:
@@ -1463,23 +1615,18 @@ int run_planned(const Plan* plan, int32_t join_op, int32_t n_in, const ea_relati
       a.c = (char*)out->data;
       a.res = res ? (const char*)res->data : nullptr;
       a.dt_res = res ? res->dtype : 0;
-      a.tiles = (const GemmTile*)plan->d_work;
-      a.n_tiles = (int32_t)plan->n_work;
+      a.direct = plan->gemm_direct;
+      if (a.direct) {
+        a.units = (const GemmUnit*)plan->d_work;
+        a.n_units = (int32_t)plan->n_work;
+      } else {
+        a.tiles = (const GemmTile*)plan->d_work;
+        a.n_tiles = (int32_t)plan->n_work;
+      }
       a.tuple_stride = n_in + 1;
       a.b_kmajor = plan->b_kmajor;
       a.dt_in = in[0]->dtype;
       a.dt_out = out->dtype;
-      {
-        // direct-to-LDS kernel: contracted block extents multiples of 32, at
-        // most kGemmMaxTuples tuples per unit and operand blocks below 4 GiB
-        // (32-bit lane offsets); else the register-staged one
-        bool k32 = true;
-        for (int64_t v : in[0]->splits[1]) k32 &= v % 32 == 0;
-        const int64_t per_unit = (in[0]->nb[1] + plan->gemm_parts - 1) / plan->gemm_parts;
-        bool small = true;
-        for (int i = 0; i < n_in; ++i) small &= max_block_bytes(in[i]) < (int64_t(1) << 32);
-        a.direct = k32 && per_unit <= kGemmMaxTuples && small;
-      }
       a.partials = (float*)(ws + kWsCounterBytes);
       a.counters = (int32_t*)ws;
       EA_HIP_TRY(launch_gemm(a, s));

@@ -153,6 +153,24 @@ struct GemmTile {      // one workgroup: a tile of one output block and a run of
   int32_t counter;     // arrival counter of the tile (split tiles only)
 };
 
+// Direct-load kernel: a workgroup's unit is up to kGemmMaxSegs segments, each a
+// run of 32-deep K steps of one output tile.  Balanced units take equal runs of
+// the tiles' K steps laid end to end, so a unit may finish one tile and start
+// the next; a tile cut into several segments is merged by its last arriver.
+struct GemmSeg {
+  int32_t block, m0, n0;  // output tile
+  int32_t s0, s1;         // K steps [s0, s1) of the tile's walk over its group's tuples
+  int32_t part, n_parts;  // place among the tile's segments (ascending s0); n_parts 1: not split
+  int32_t first_slot;     // split tile: part i's partial sums go to workspace slot first_slot + i
+  int32_t counter;        // split tile: its arrival counter
+  int32_t pad[3];
+};
+constexpr int kGemmMaxSegs = 2;
+struct GemmUnit {
+  GemmSeg seg[kGemmMaxSegs];
+  int32_t n_seg, pad[3];
+};
+
 struct GemmArgs {
   const int32_t* tuples;
   const int32_t* goff;
@@ -165,8 +183,10 @@ struct GemmArgs {
   const char* b2;
   char* c;
   const char* res;       // residual relation data (same layout as c) or null
-  const GemmTile* tiles;
+  const GemmTile* tiles;  // register-staged kernel: one tile and run of tuples per workgroup
   int32_t n_tiles;
+  const GemmUnit* units;  // direct-load kernel: one unit per workgroup
+  int32_t n_units;
   int32_t tuple_stride;  // 1 + n_in
   int32_t b_kmajor;      // 1: B blocks are [n][k] ("ab,cb->ac"); 0: [k][n]
   int32_t dt_in;         // EA_BF16 or EA_F16

@@ -38,15 +38,16 @@ def _gemm_case(T, J, K, block, seed):
 
 def test_noalloc_gemm_matches_joinagg_on_two_calls():
     # call 1: the block share's QKV projection, 2048 x 8192 x 3072 in 512-blocks
-    # (keys split over two workgroups: 48 MiB of partials); call 2: a smaller
-    # split-key GEMM, 512 x 4096 x 512 in 256-blocks
+    # (96 tiles whose K steps are shared out over 256 workgroups: tens of MiB
+    # of partials); call 2: a smaller split-key GEMM, 512 x 4096 x 512 in
+    # 256-blocks
     spec = "tj,jk->tk"
     for (T, J, K, block, seed) in ((2048, 8192, 3072, 512, 961), (512, 4096, 512, 256, 963)):
         print(f"noalloc gemm {T}x{J}x{K}", flush=True)
         x, w, X, W, py = _gemm_case(T, J, K, block, seed)
         Yref = ea.Relation((T, K), "bf16", py)
         need = ea.joinagg_workspace(spec, ea.JOIN_MUL, ea.AGG_SUM, [X, W], Yref)
-        assert ea.WS_COUNTER_BYTES < need <= (64 << 20)
+        assert ea.WS_COUNTER_BYTES < need <= (128 << 20)
         ea.joinagg(spec, ea.JOIN_MUL, ea.AGG_SUM, [X, W], Yref)
         Y = ea.Relation((T, K), "bf16", py)
         Y.data.fill_(0xFF)
@@ -88,13 +89,14 @@ def test_noalloc_refuses_unplanned_and_oversized():
     n_plans = ea.plan_cache_size()
     assert _raw_noalloc("tj,jk->tk", ea.JOIN_MUL, ea.AGG_SUM, [X, W], Y) == -9
     assert ea.plan_cache_size() == n_plans
-    # a plan whose workspace exceeds the 64 MiB array: EA_ERR_CAPACITY.
-    # 2048 x 32768 x 4096 in 512-blocks has 128 output tiles of 256 x 256 and
-    # 512 K steps; the plan splits each tile over 2 parts (one wave of 256
-    # units): 256 partial tiles of 256 KiB = 64 MiB, plus the counter area
-    X = ea.Relation((2048, 32768), "bf16", [synth.splits(2048, 512), synth.splits(32768, 512)])
-    W = ea.Relation((32768, 4096), "bf16", [synth.splits(32768, 512), synth.splits(4096, 512)])
-    Y = ea.Relation((2048, 4096), "bf16", [synth.splits(2048, 512), synth.splits(4096, 512)])
-    need = ea.joinagg_workspace("tj,jk->tk", ea.JOIN_MUL, ea.AGG_SUM, [X, W], Y)
-    assert need == ea.WS_COUNTER_BYTES + 256 * 256 * 256 * 4
-    assert _raw_noalloc("tj,jk->tk", ea.JOIN_MUL, ea.AGG_SUM, [X, W], Y) == -4
+    # a plan whose workspace exceeds the 128 MiB array: EA_ERR_CAPACITY.  One
+    # causal head of 131072 tokens in 128-blocks splits its long key runs over
+    # up to 16 parts: thousands of 65 KiB partials
+    S = 131072
+    part = [[0, 1], [0, 1], synth.splits(S, 128), [0, 128]]
+    Q, K, V, O = (ea.Relation((1, 1, S, 128), "bf16", part) for _ in range(4))
+    need = ea.joinagg_workspace("bhqd,bhkd,bhkd->bhqd", ea.OP_ATTENTION, ea.AGG_LSE, [Q, K, V], O,
+                                scale=1.0 / np.sqrt(128), causal=True)
+    assert need > (128 << 20)
+    assert _raw_noalloc("bhqd,bhkd,bhkd->bhqd", ea.OP_ATTENTION, ea.AGG_LSE, [Q, K, V], O,
+                        scale=1.0 / np.sqrt(128), causal=True) == -4
