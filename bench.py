@@ -410,6 +410,26 @@ def _rate(c, ms, peak_tflops=PEAK_BF16_TFLOPS):
     return d
 
 
+def copy_ceiling_us(nbytes: int, n: int):
+    """Practical ceiling of a memory-bound operator moving nbytes each way:
+    the faster of a device-to-device copy (torch copy_, the runtime's copy
+    kernel) and the library's own repartition between two one-block relations
+    (a contiguous copy), with buffers rotated through >= 1 GiB like the
+    operators' own workloads.  Returns (us, which)."""
+    import torch
+
+    from paper_2609_03905_amd import ea
+
+    m = nbytes // 2
+    sets = [(torch.empty(nbytes, dtype=torch.uint8, device="cuda"), torch.empty(nbytes, dtype=torch.uint8, device="cuda"))
+            for _ in range(max(1, -(-ROTATE_BYTES // (2 * nbytes))))]
+    rels = [(ea.Relation((m,), "bf16", [[0, m]], data=a), ea.Relation((m,), "bf16", [[0, m]], data=b)) for a, b in sets]
+    rot_t, rot_r = _Rotation(sets), _Rotation(rels)
+    t_copy = _events_ms(lambda: (lambda ab: ab[1].copy_(ab[0]))(rot_t.next()), n) * 1e3
+    t_own = _events_ms(lambda: (lambda ab: ea.repartition(ab[0], ab[1], store=ea.STORE_STREAM))(rot_r.next()), n) * 1e3
+    return (t_copy, "device copy") if t_copy <= t_own else (t_own, "library repartition")
+
+
 def config_rows(n):
     import gc
 
@@ -439,6 +459,11 @@ def config_rows(n):
         if bar is not None:
             d["bar_frac"] = bar
             d["meets_bar"] = bool(d["frac_peak"] >= bar)
+        if "bytes" in c:  # memory-bound: against a copy moving the same bytes
+            cu, how = copy_ceiling_us(int(c["bytes"]) // 2, n)
+            d["copy_ceiling_us"] = round(cu, 3)
+            d["copy_ceiling"] = how
+            d["within_10pct_of_copy"] = bool(d["us"] <= 1.1 * cu)
         rows[name] = d
     built.clear()
     gc.collect()

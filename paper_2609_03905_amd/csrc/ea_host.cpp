@@ -293,7 +293,7 @@ struct Image {
   size_t put_vec(const std::vector<T>& v) { return put(v.data(), v.size() * sizeof(T)); }
 };
 
-enum Kind { K_GENERIC = 1, K_GEMM, K_RMSNORM, K_SOFTMAX, K_ATTENTION, K_REPART };
+enum Kind { K_GENERIC = 1, K_GEMM, K_GEMM32, K_RMSNORM, K_SOFTMAX, K_ATTENTION, K_REPART };
 
 // row-reduction plan constants (see RowArgs)
 struct RowLayout {
@@ -507,6 +507,23 @@ int classify(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation*
         for (int d = 0; d < o->rank; ++d)
           if (r->splits[d] != o->splits[d]) return fail(EA_ERR_ARG, "residual partition differs from the output's");
         if (!r->data) return fail(EA_ERR_ARG, "residual relation has no data");
+      }
+      // fp32 block products "ab,bc->ac" / "ab,cb->ac" without a residual:
+      // the vector-ALU tile kernel
+      if (join_op == EA_JOIN_MUL && agg_op == EA_AGG_SUM && n_in == 2 && sp.rank[0] == 2 && sp.rank[1] == 2 &&
+          sp.rank[2] == 2 && ops[0]->dtype == EA_F32 && ops[1]->dtype == EA_F32 && !(prm && prm->residual)) {
+        const char a = sp.let[0][0], b = sp.let[0][1];
+        const char* L1 = sp.let[1];
+        const char* L2 = sp.let[2];
+        int kmaj = -1;
+        char c = 0;
+        if (L1[0] == b && L1[1] != a && L1[1] != b) { kmaj = 0; c = L1[1]; }
+        else if (L1[1] == b && L1[0] != a && L1[0] != b) { kmaj = 1; c = L1[0]; }
+        if (kmaj >= 0 && L2[0] == a && L2[1] == c) {
+          oi->kind = K_GEMM32;
+          oi->b_kmajor = kmaj;
+          return EA_OK;
+        }
       }
       // matrix-core path: "ab,bc->ac" or "ab,cb->ac", 16-bit inputs, SUM of products
       if (join_op == EA_JOIN_MUL && agg_op == EA_AGG_SUM && n_in == 2 && sp.rank[0] == 2 &&
@@ -1245,6 +1262,22 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
       p->ws_partial_bytes = slots * kGemmTM * kGemmTN * (int64_t)sizeof(float);
       break;
     }
+    case K_GEMM32: {  // square tiles of every output block
+      std::vector<Gemm32Work> work;
+      const ea_relation* c = ops[sp.n_in];
+      int32_t co[kMaxRank];
+      for (int64_t b = 0; b < c->nblocks; ++b) {
+        block_coords(c, b, co);
+        const int64_t me = c->splits[0][co[0] + 1] - c->splits[0][co[0]];
+        const int64_t ne = c->splits[1][co[1] + 1] - c->splits[1][co[1]];
+        for (int64_t m0 = 0; m0 < me; m0 += kGemm32Tile)
+          for (int64_t n0 = 0; n0 < ne; n0 += kGemm32Tile)
+            work.push_back(Gemm32Work{(int32_t)b, (int32_t)m0, (int32_t)n0, 0});
+      }
+      ex.work = img.put_vec(work);
+      ex.n_work = (int64_t)work.size();
+      break;
+    }
     case K_RMSNORM:
     case K_SOFTMAX: e = build_rows(sp, ops, oi, &img, &ex, &p->rows); break;
     case K_ATTENTION: break;  // work units follow the GPU join (below)
@@ -1632,6 +1665,25 @@ int run_planned(const Plan* plan, int32_t join_op, int32_t n_in, const ea_relati
       EA_HIP_TRY(launch_gemm(a, s));
       break;
     }
+    case K_GEMM32: {
+      Gemm32Args a;
+      memset(&a, 0, sizeof(a));
+      a.tuples = plan->d_tuples;
+      a.goff = plan->d_goff;
+      a.blk_a = plan->d_blk[0];
+      a.blk_b = plan->d_blk[1];
+      a.blk_c = plan->d_blk[2];
+      a.a = (const char*)in[0]->data;
+      a.b = (const char*)in[1]->data;
+      a.c = (char*)out->data;
+      a.work = (const Gemm32Work*)plan->d_work;
+      a.n_work = plan->n_work;
+      a.tuple_stride = 3;
+      a.b_kmajor = plan->b_kmajor;
+      a.dt_out = out->dtype;
+      EA_HIP_TRY(launch_gemm32(a, s));
+      break;
+    }
     case K_RMSNORM:
     case K_SOFTMAX: {
       RowArgs a;
@@ -1879,6 +1931,9 @@ int get_repartition_plan(const ea_relation* src, const ea_relation* dst, bool bu
           if (rb > INT32_MAX || rows > INT32_MAX) return fail(EA_ERR_UNSUPPORTED, "repartition box too large");
           if (rows * rb > INT32_MAX) return fail(EA_ERR_UNSUPPORTED, "repartition box too large");
           t.row_bytes = (int32_t)rb;
+          t.row_shift = -1;
+          for (int b = 0; b < 31; ++b)
+            if (((int64_t)1 << b) == rb) t.row_shift = b;
           int vec = 16;
           auto fits = [&](int64_t v) { return v % vec == 0; };
           while (vec > 1) {

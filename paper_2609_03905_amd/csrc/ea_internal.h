@@ -129,6 +129,8 @@ struct RepTask {
   int32_t row_bytes;
   int32_t vec;                      // bytes per vector access: 16, 8, 4, 2 or 1
   int32_t begin, end;               // byte range of the box (rows x row_bytes) copied
+  int32_t row_shift;                // log2(row_bytes) when a power of two, else -1
+  int32_t pad;
 };
 
 hipError_t launch_repartition(const RepTask* d_tasks, int64_t n_tasks, const char* src, char* dst, bool stream_out,
@@ -199,6 +201,33 @@ struct GemmArgs {
 };
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// fp32 block product "ab,bc->ac" / "ab,cb->ac" on the vector ALUs: a workgroup
+// owns a kGemm32Tile-square tile of one output block and sums its key's tuples.
+// ---------------------------------------------------------------------------
+constexpr int kGemm32Tile = 32;
+struct Gemm32Work {
+  int32_t block, m0, n0, pad;
+};
+
+struct Gemm32Args {
+  const int32_t* tuples;
+  const int32_t* goff;
+  const DevBlk* blk_a;
+  const DevBlk* blk_b;
+  const DevBlk* blk_c;
+  const char* a;
+  const char* b;
+  char* c;
+  const Gemm32Work* work;
+  int64_t n_work;
+  int32_t tuple_stride;
+  int32_t b_kmajor;  // 1: B blocks are [n][k] ("ab,cb->ac")
+  int32_t dt_out;    // EA_F32, EA_BF16 or EA_F16
+};
+
+hipError_t launch_gemm32(const Gemm32Args& a, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Row reductions.  A row is the concatenation of its segments, one per tuple

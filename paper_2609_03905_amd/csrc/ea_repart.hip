@@ -29,12 +29,20 @@ constexpr int kThreads = 256;
 
 constexpr int kUnroll = 4;  // vectors per thread loaded before any is stored
 
-// Byte offsets (source, destination) of byte L of the task's box.
+// Byte offsets (source, destination) of byte L of the task's box.  Rows of a
+// power-of-two width take a shift instead of a division, and a box with one
+// outer dim (the usual 2-d block) needs no further division.
 __device__ __forceinline__ void box_offsets(const RepTask& t, int32_t L, int64_t& so, int64_t& dof) {
-  int32_t row = L / t.row_bytes;
+  const int sh = t.row_shift;
+  int32_t row = sh >= 0 ? L >> sh : L / t.row_bytes;
   const int32_t col = L - row * t.row_bytes;
   so = col;
   dof = col;
+  if (t.n_outer == 1) {  // row < outer_ext[0] for every byte of the range
+    so += (int64_t)row * t.src_stride[0];
+    dof += (int64_t)row * t.dst_stride[0];
+    return;
+  }
   for (int d = t.n_outer - 1; d >= 0; --d) {
     const int32_t c = row % t.outer_ext[d];
     row /= t.outer_ext[d];

@@ -191,6 +191,30 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
       if (vis[k]) v[k] = *reinterpret_cast<const uint4*>(x_at(sg, e0));
     }
   }
+  // Causal softmax: chunks wholly after the row's query position are zeros
+  // of the output whatever the row's max and sum, so they are stored now,
+  // while the row's loads are in flight, rather than after the reduction
+  if constexpr (SOFTMAX) {
+    if (a.causal && active) {
+      auto store_zeros = [&](auto stream_tag) {
+        constexpr bool STREAM = decltype(stream_tag)::value;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int c = k * 64 + lane;
+          if (c >= total || vis[k]) continue;
+          char* yp = y_at(seg[k], e0s[k]);  // the chunk's EPC outputs, stored as write_row stores them
+          if ((a.dt_y == EA_BF16 && ES == 2) || (a.dt_y == EA_F32 && ES == 4)) {
+            store_out<STREAM>(yp, make_uint4(0, 0, 0, 0));
+          } else {
+#pragma unroll
+            for (int i = 0; i < EPC; ++i) st_elem(yp, i, a.dt_y, 0.0f);
+          }
+        }
+      };
+      if (a.stream_out) store_zeros(std::true_type{});
+      else store_zeros(std::false_type{});
+    }
+  }
   // RMSNorm: while the row's loads are in flight, every wave of the
   // workgroup helps stage the weights
   if constexpr (!SOFTMAX) {
@@ -236,6 +260,14 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     }
   }
   float scale = 0.0f, m = 0.0f;
+  // softmax rows of at most 4 chunks per lane keep their exponentials from
+  // the sum for the output, instead of computing them a second time
+  constexpr bool KEEP = SOFTMAX && K <= 4;
+  float ex[KEEP ? K : 1][KEEP ? 8 : 1];
+#pragma unroll
+  for (int k = 0; k < (KEEP ? K : 1); ++k)
+#pragma unroll
+    for (int i = 0; i < (KEEP ? 8 : 1); ++i) ex[k][i] = 0.0f;
   if constexpr (SOFTMAX) {
     m = wave_max(part);
     float l = 0.0f;
@@ -248,7 +280,9 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
 #pragma unroll
       for (int i = 0; i < EPC; ++i) {
         const bool ok = !a.causal || k0 + i <= qpos;
-        l += ok ? __expf(f[i] - m) : 0.0f;
+        const float e = ok ? __expf(f[i] - m) : 0.0f;
+        if constexpr (KEEP) ex[k][i] = e;
+        l += e;
       }
     }
     l = wave_sum(l);
@@ -265,12 +299,16 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     for (int k = 0; k < K; ++k) {
       const int c = k * 64 + lane;
       if (c >= total) continue;
+      if (SOFTMAX && a.causal && !vis[k]) continue;  // stored as zeros above
       const int sg = seg[k];
       const int e0 = e0s[k];
       float f[8];
-      unpack<XT>(v[k], f);
+      if constexpr (!KEEP) unpack<XT>(v[k], f);
       float o[8];
-      if constexpr (SOFTMAX) {
+      if constexpr (KEEP) {  // masked and invisible entries hold exact zeros
+#pragma unroll
+        for (int i = 0; i < EPC; ++i) o[i] = vis[k] ? ex[k][i] * scale : 0.0f;
+      } else if constexpr (SOFTMAX) {
         const int k0 = klo(sg) + e0;
 #pragma unroll
         for (int i = 0; i < EPC; ++i) {

@@ -18,7 +18,7 @@ pytestmark = pytest.mark.gpu
 
 
 # ---------------------------------------------------------------------------
-# generic einsum path
+# fp32 block products and the generic einsum path
 # ---------------------------------------------------------------------------
 def test_matmul_fp32_256_in_64_blocks():
     w = synth.matmul_256_fp32()
@@ -27,6 +27,26 @@ def test_matmul_fp32_256_in_64_blocks():
     ea.joinagg(w["spec"], ea.JOIN_MUL, ea.AGG_SUM, [A, B], C)
     ref = oracle.matmul(synth.to_f64(w["A"], "f32"), synth.to_f64(w["B"], "f32"))
     assert_close(values(C), ref, what="C1")
+
+
+@pytest.mark.parametrize("kmajor", [False, True])
+@pytest.mark.parametrize("out_dtype", ["f32", "bf16"])
+def test_fp32_block_product_ragged_blocks(kmajor, out_dtype):
+    # f32 'ij,jk->ik' / 'ij,kj->ik': 64 x 64 tiles of every output block, the
+    # key's tuples summed in order; ragged blocks on every letter
+    rng = np.random.default_rng(11)
+    M, J, N = 200, 333, 150
+    pm, pj, pn = (synth.random_splits(n, 3, rng) for n in (M, J, N))
+    a = synth.normal((M, J), 12, dtype="f32")
+    b = synth.normal((N, J) if kmajor else (J, N), 13, dtype="f32")
+    A = upload(a, "f32", [pm, pj])
+    B = upload(b, "f32", [pn, pj] if kmajor else [pj, pn])
+    C = empty((M, N), out_dtype, [pm, pn])
+    ea.joinagg("ij,kj->ik" if kmajor else "ij,jk->ik", ea.JOIN_MUL, ea.AGG_SUM, [A, B], C)
+    fb = synth.to_f64(b, "f32")
+    ref = oracle.matmul(synth.to_f64(a, "f32"), np.ascontiguousarray(fb.T) if kmajor else fb)
+    assert_close(values(C), expected(ref, out_dtype), rel_fro=1e-5 if out_dtype == "f32" else 1e-3,
+                 what=f"fp32 block product kmajor={kmajor} {out_dtype}")
 
 
 @pytest.mark.parametrize("seed", range(4))
