@@ -10,8 +10,10 @@
 // in ascending key-block order.
 //
 // Work unit = (group, 128-row query tile, a run of the group's tuples).  A
-// workgroup holds two groups of 4 waves x 32 query rows; one group's loads
-// overlap the other's MFMAs.  Per 64-key chunk:
+// workgroup holds two groups of 4 waves x 32 query rows; in each phase group
+// 0 computes one 64-key chunk and group 1 the next, while every wave issues
+// its share of the loads of the next phase's two chunks (four 32 KiB
+// buffers: two computed, two loading).  Per 64-key chunk:
 //   * K and V chunks [key][d] (bf16, 256-byte rows) go straight from global
 //     memory into LDS (global_load_lds_dwordx4), their 16-byte chunks
 //     XOR-swizzled per key row so that the fragment reads below spread over
@@ -42,8 +44,11 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 constexpr int kThreads = 512;       // two groups of 4 waves x 32 query rows
 constexpr int D = 128;              // head dim
 constexpr int KC = 64;              // keys per staged chunk
+constexpr int KT = KC / 32;         // 32-key MFMA tiles per chunk
+constexpr int LPW = KC / 32;        // direct loads per wave per chunk, for K and for V each
 constexpr int BUF = 2 * KC * D;     // LDS elements per chunk buffer: K chunk, then V chunk
 constexpr int NBUF = 4;             // two chunks computed while the next two load
+constexpr int LOOKAHEAD = NBUF / 2 - 1;  // phases between a chunk's loads and its compute
 
 // Per-tuple K/V metadata of a unit, staged in LDS once so that the chunk walk
 // never waits on a chain of global table loads.
@@ -189,7 +194,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   for (int b = 0; b < NBUF; ++b) key0_buf[b] = 0;
 
   // Load the next chunk of the walk into buffer b (a compile-time constant):
-  // all 8 waves take part, 2 K and 2 V loads of 4 key rows each per wave.
+  // all 8 waves take part, LPW K and LPW V loads of 4 key rows each per wave.
   auto load_chunk = [&](int b) {
     const KvMeta& mt = s_tm[it_t];
     const char* kbase = p.k + mt.koff + (int64_t)it_c * D * 2;
@@ -197,8 +202,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
     key0_buf[b] = mt.klo + it_c;
     const uint32_t ldsK = lds0 + b * BUF * 2, ldsV = ldsK + KC * D * 2;
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int inst = wid * 2 + q;
+    for (int q = 0; q < LPW; ++q) {
+      const int inst = wid * LPW + q;
       const int r = inst * 4 + (lane >> 4);  // key row of this lane's piece
       const int ck = (lane & 15) ^ swz_krow(r), cv = (lane & 15) ^ swz_vrow(r);
       dl_load16(kbase, (uint32_t)((r * D + 8 * ck) * 2), ldsK + inst * 1024);
@@ -214,8 +219,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   auto convert_v = [&](int b) {
     uint16_t* sVb = sKV + b * BUF + KC * D;
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      uint4* piece = reinterpret_cast<uint4*>(sVb + (wid * 2 + q) * 512 + lane * 8);
+    for (int q = 0; q < LPW; ++q) {
+      uint4* piece = reinterpret_cast<uint4*>(sVb + (wid * LPW + q) * 512 + lane * 8);
       const uint4 w = *piece;
       *piece = make_uint4(bf16x2_to_f16x2(w.x), bf16x2_to_f16x2(w.y), bf16x2_to_f16x2(w.z), bf16x2_to_f16x2(w.w));
     }
@@ -228,25 +233,25 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
     const uint16_t* sV = sK + KC * D;
     const int key0 = key0_buf[b];
     if (causal && key0 > qpos_wave_max) return;  // the whole wave is masked in this chunk
-    f32x16_t acc_s[2];
-    acc_s[0] = f32x16_t{};
-    acc_s[1] = f32x16_t{};
+    f32x16_t acc_s[KT];
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) acc_s[kt] = f32x16_t{};
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
-      uint4 a[2];
+      uint4 a[KT];
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
+      for (int kt = 0; kt < KT; ++kt) {
         const int r = 32 * kt + lq;
         a[kt] = *reinterpret_cast<const uint4*>(sK + r * D + 8 * ((2 * s + g) ^ swz_krow(r)));
       }
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) acc_s[kt] = mfma_bf16(a[kt], qreg[s], acc_s[kt]);
+      for (int kt = 0; kt < KT; ++kt) acc_s[kt] = mfma_bf16(a[kt], qreg[s], acc_s[kt]);
     }
     // online softmax in the log2 domain; the scale is one FMA ahead of exp2
     const bool diag = causal && key0 + KC - 1 > qpos_wave_min;  // some key is past some query
     float mx = -INFINITY;
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float sv = acc_s[kt][r];
@@ -267,7 +272,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
     const float m_use = m_new == -INFINITY ? 0.0f : m_new;
     float rs = 0.0f;
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float pv = fast_exp2(fmaf(acc_s[kt][r], sc, -m_use));
@@ -289,7 +294,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
     // 32 kt + 16 h + 8 + 4 g + (e - 4); P in fp16 (RNE), V in fp16
     const int gq = lane >> 4, li = lane & 15;
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const uint4 ph = make_uint4(pack_f16(acc_s[kt][8 * h], acc_s[kt][8 * h + 1]),
@@ -307,29 +312,60 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
       }
   };
 
-  // Phases: in phase ph every wave issues its loads of chunks 2ph and 2ph+1
-  // (buffers 2ph % 4, 2ph % 4 + 1), group 0 computes chunk 2ph - 2 and group
-  // 1 chunk 2ph - 1 (the other two buffers) while those loads are in
-  // flight; then each wave waits for its own loads, converts its V pieces,
-  // and the workgroup meets at the barrier.  The loop runs two phases per
-  // iteration so that every buffer index is a compile-time constant.
-  const int n_phase = (nc + 1) / 2 + 1;
-  for (int ph0 = 0; ph0 < n_phase; ph0 += 2) {
+  // Phases: in phase ph group 0 computes chunk 2ph and group 1 chunk 2ph+1
+  // (buffers 2ph % NBUF and 2ph % NBUF + 1), while every wave issues its
+  // loads of the chunks LOOKAHEAD phases ahead into the buffers of phase ph -
+  // 1 (both groups finished them before that phase's barrier).  At the end of
+  // the phase each wave waits for its own loads of the next phase's two
+  // chunks, converts its V pieces of them, and the workgroup meets at the
+  // barrier.  The loop runs NBUF / 2 phases per iteration so that every
+  // buffer index is a compile-time constant.  (Eight 16 KiB buffers of
+  // 32-key chunks, three phases of lookahead, were measured slower: 34.8 ->
+  // 38.8 us on 2 x 4 heads of 2048 tokens; the per-phase costs doubled, and
+  // more bytes in flight did not shorten the phase.)
+  // s_waitcnt vmcnt(n) in the gfx9 encoding (vmcnt in bits 3:0 and 15:14,
+  // expcnt and lgkmcnt left at their maxima)
+  constexpr auto vmcnt = [](int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); };
+  static_assert(2 * LOOKAHEAD * 2 * LPW < 64, "vmcnt range");
+  auto wait_loads = [&](int later_chunks) {  // this wave's loads landed but those of `later_chunks` chunks
+    asm volatile("" ::: "memory");
+    if (LOOKAHEAD == 1 || later_chunks <= 0) {
+      __builtin_amdgcn_s_waitcnt(vmcnt(0));
+    } else {
+      switch (later_chunks) {
+        case 1: __builtin_amdgcn_s_waitcnt(vmcnt(2 * LPW)); break;
+        case 2: __builtin_amdgcn_s_waitcnt(vmcnt(4 * LPW)); break;
+        case 3: __builtin_amdgcn_s_waitcnt(vmcnt(6 * LPW)); break;
+        default: __builtin_amdgcn_s_waitcnt(vmcnt(8 * LPW)); break;
+      }
+    }
+    asm volatile("" ::: "memory");
+  };
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
+  for (int j = 0; j < 2 * LOOKAHEAD; ++j)
+    if (j < nc) load_chunk(j);
+  if (nc > 0) {
+    const int last = nc < 2 ? 0 : 1;  // the last chunk of phase 0
+    wait_loads(min(nc, 2 * LOOKAHEAD) - (last + 1));
+    convert_v(0);
+    if (nc > 1) convert_v(1);
+  }
+  __syncthreads();
+  const int n_phase = (nc + 1) / 2;
+  for (int ph0 = 0; ph0 < n_phase; ph0 += NBUF / 2) {
+#pragma unroll
+    for (int e = 0; e < NBUF / 2; ++e) {
       const int ph = ph0 + e;
       if (ph < n_phase) {
-        const int lb = 2 * e, cb = 2 * (1 - e);  // buffers loaded / computed in this phase
-        if (2 * ph < nc) load_chunk(lb);
-        if (2 * ph + 1 < nc) load_chunk(lb + 1);
-        const int cj = 2 * ph - 2 + grp;  // this group's chunk to compute
-        if (ph >= 1 && cj < nc) compute_chunk(cb + grp);
-        if (2 * ph < nc) {
-          asm volatile("" ::: "memory");
-          __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0): this wave's pieces landed
-          asm volatile("" ::: "memory");
-          convert_v(lb);
-          if (2 * ph + 1 < nc) convert_v(lb + 1);
+        const int cb = 2 * e, lb = (2 * e + 2 * LOOKAHEAD) % NBUF;  // buffers computed / loaded
+        if (2 * ph + 2 * LOOKAHEAD < nc) load_chunk(lb);
+        if (2 * ph + 2 * LOOKAHEAD + 1 < nc) load_chunk(lb + 1);
+        if (2 * ph + grp < nc) compute_chunk(cb + grp);
+        if (2 * ph + 2 < nc) {  // the next phase's chunks
+          const int last = min(2 * ph + 3, nc - 1);
+          wait_loads(min(nc, 2 * ph + 2 + 2 * LOOKAHEAD) - (last + 1));
+          convert_v((cb + 2) % NBUF);
+          if (2 * ph + 3 < nc) convert_v((cb + 3) % NBUF);
         }
         __syncthreads();
       }
