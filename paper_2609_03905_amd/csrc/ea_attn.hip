@@ -10,10 +10,11 @@
 // in ascending key-block order.
 //
 // Work unit = (group, 128-row query tile, a run of the group's tuples).  A
-// workgroup holds two groups of 4 waves x 32 query rows; in each phase group
-// 0 computes one 64-key chunk and group 1 the next, while every wave issues
-// its share of the loads of the next phase's two chunks (four 32 KiB
-// buffers: two computed, two loading).  Per 64-key chunk:
+// workgroup is 4 waves x 32 query rows, and two workgroups share a CU: they
+// meet at no common barrier, so one's softmax VALU work runs beside the
+// other's MFMAs.  Every wave computes each 64-key chunk of the walk while
+// the workgroup's loads of the next chunk land in the other of two 32 KiB
+// buffers.  Per 64-key chunk:
 //   * K and V chunks [key][d] (bf16, 256-byte rows) go straight from global
 //     memory into LDS (global_load_lds_dwordx4), their 16-byte chunks
 //     XOR-swizzled per key row so that the fragment reads below spread over
@@ -41,14 +42,13 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kThreads = 512;       // two groups of 4 waves x 32 query rows
+constexpr int kThreads = 256;       // 4 waves x 32 query rows
 constexpr int D = 128;              // head dim
-constexpr int KC = 64;              // keys per staged chunk
+constexpr int KC = kAttnChunkKeys;  // keys per staged chunk (64)
 constexpr int KT = KC / 32;         // 32-key MFMA tiles per chunk
-constexpr int LPW = KC / 32;        // direct loads per wave per chunk, for K and for V each
+constexpr int LPW = KC / 16;        // direct loads (4 key rows each) per wave per chunk, for K and for V each
 constexpr int BUF = 2 * KC * D;     // LDS elements per chunk buffer: K chunk, then V chunk
-constexpr int NBUF = 4;             // two chunks computed while the next two load
-constexpr int LOOKAHEAD = NBUF / 2 - 1;  // phases between a chunk's loads and its compute
+constexpr int NBUF = 2;             // one chunk computed while the next loads
 
 // Per-tuple K/V metadata of a unit, staged in LDS once so that the chunk walk
 // never waits on a chain of global table loads.
@@ -57,10 +57,9 @@ struct KvMeta {
   int32_t klo, kext;   // key interval of the block
 };
 constexpr float kLog2e = 1.4426950408889634f;
+template <bool B>
+struct Bool { static constexpr bool value = B; };
 constexpr float kLazyMax = 8.0f;  // log2 of the largest P the lazy running max allows
-// LDS byte offset of the epilogue's per-wave row staging: past the area the
-// two groups' (m, l, O) merge uses (16384 + 512 floats)
-constexpr int kEpiStageOffset = 68 * 1024;
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
@@ -126,32 +125,79 @@ __device__ __forceinline__ uint2 tr_read(const uint16_t* p) {
 // of the row's largest term.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-__global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
+__global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
   __shared__ __attribute__((aligned(1024))) uint16_t sKV[NBUF * BUF];  // chunk buffers: K, then V
   __shared__ KvMeta s_tm[kAttnMaxUnitTuples];
   __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int grp = wid >> 2, wq = wid & 3;  // group, and wave inside it (32 query rows)
+  const int wq = wid;  // wave: query rows 32 wq .. 32 wq + 31 of the tile
   const int g = lane >> 5, lq = lane & 31;
   const AttnUnit u = p.units[blockIdx.x];
   // the unit's blocks, resolved at plan time from the tuple table
   const AttnUnitMeta& um = p.meta[blockIdx.x];
   const int nt = ld_uniform(&um.nt);
+  const int nc = ld_uniform(&um.nc);  // chunks of the walk, up to the first past the tile's last query
   const int q_lo = ld_uniform(&um.q_lo);
   const int64_t qoff = ld_uniform(&um.qoff), ooff = ld_uniform(&um.ooff);
   const int row = u.q0 + wq * 32 + lq;  // this lane's query row inside the block
   const int qpos = q_lo + row;          // its position
   const int qpos_wave_min = q_lo + u.q0 + wq * 32;
   const int qpos_wave_max = qpos_wave_min + 31;
-  const int qpos_tile_max = q_lo + u.q0 + 127;
   const float sc = p.scale * kLog2e;
   const bool causal = p.causal != 0;
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t*)sKV;
 
-  // the unit's tuples' K/V metadata (nt <= kAttnMaxUnitTuples: host
-  // guarantee), loaded first so that its wait does not cover the Q loads
+  // walk of the chunks in load order; chunk j goes to buffer j % NBUF
+  int it_t = 0, it_c = 0;  // tuple (index into s_tm) and offset of the next chunk to load
+  int key0_buf[NBUF];  // first key of the chunk held in each buffer (constant indices only)
+#pragma unroll
+  for (int b = 0; b < NBUF; ++b) key0_buf[b] = 0;
+
+  // Issue the K or the V loads of one chunk into buffer b (a compile-time
+  // constant): all 4 waves take part, LPW loads of 4 key rows each per wave.
+  auto issue_k = [&](int b, const char* kbase) {
+    const uint32_t ldsK = lds0 + b * BUF * 2;
+#pragma unroll
+    for (int q = 0; q < LPW; ++q) {
+      const int inst = wid * LPW + q;
+      const int r = inst * 4 + (lane >> 4);  // key row of this lane's piece
+      dl_load16(kbase, (uint32_t)((r * D + 8 * ((lane & 15) ^ swz_krow(r))) * 2), ldsK + inst * 1024);
+    }
+  };
+  auto issue_v = [&](int b, const char* vbase) {
+    const uint32_t ldsV = lds0 + b * BUF * 2 + KC * D * 2;
+#pragma unroll
+    for (int q = 0; q < LPW; ++q) {
+      const int inst = wid * LPW + q;
+      const int r = inst * 4 + (lane >> 4);
+      dl_load16(vbase, (uint32_t)((r * D + 8 * ((lane & 15) ^ swz_vrow(r))) * 2), ldsV + inst * 1024);
+    }
+  };
+  auto advance = [&](int kext) {
+    it_c += KC;
+    if (it_c >= kext) {
+      ++it_t;
+      it_c = 0;
+    }
+  };
+
+  // The first chunk goes out first, its addresses taken from the record by
+  // scalar loads (before the metadata table reaches LDS, and before Q).
+#pragma unroll
+  for (int j = 0; j < 1; ++j)
+    if (j < nc) {
+      const AttnKv* kvp = &um.kv[it_t];  // it_t < nt whenever j < nc
+      const int64_t ko = ld_uniform(&kvp->koff), vo = ld_uniform(&kvp->voff);
+      const int klo = ld_uniform(&kvp->klo), kext = ld_uniform(&kvp->kext);
+      key0_buf[j] = klo + it_c;
+      issue_k(j, p.k + ko + (int64_t)it_c * D * 2);
+      issue_v(j, p.v + vo + (int64_t)it_c * D * 2);
+      advance(kext);
+    }
+
+  // the unit's tuples' K/V metadata (nt <= kAttnMaxUnitTuples: host guarantee)
   AttnKv kv{};
   if (tid < nt) kv = um.kv[tid];
 
@@ -168,8 +214,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   for (int i = 0; i < 4; ++i) acc_o[i] = f32x16_t{};
   float m = -INFINITY, l = 0.0f;  // running max (log2 domain, scaled) and sum
 
-  // metadata into LDS; the barrier waits for LDS only (not for the Q loads,
-  // which stay in flight under the first chunk loads)
+  // metadata into LDS; it is read after the prologue barrier below
   if (tid < nt) {
     KvMeta mt;
     mt.koff = kv.koff;
@@ -178,42 +223,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
     mt.kext = kv.kext;
     s_tm[tid] = mt;
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-  // The unit's 64-key chunks, ascending: (tuple, offset) pairs up to the
-  // first chunk past the tile's last query (later ones are masked for every row).
-  int nc = 0;
-  for (int t = 0; t < nt; ++t)
-    for (int c0 = 0; c0 < s_tm[t].kext && !(causal && s_tm[t].klo + c0 > qpos_tile_max); c0 += KC) ++nc;
-  // walk of the chunks in load order; chunk j goes to buffer j % 4
-  int it_t = 0, it_c = 0;  // tuple (index into s_tm) and offset of the next chunk to load
-  int key0_buf[NBUF];  // first key of the chunk held in each buffer (constant indices only)
-#pragma unroll
-  for (int b = 0; b < NBUF; ++b) key0_buf[b] = 0;
 
-  // Load the next chunk of the walk into buffer b (a compile-time constant):
-  // all 8 waves take part, LPW K and LPW V loads of 4 key rows each per wave.
-  auto load_chunk = [&](int b) {
+  // The next chunk of the walk (metadata from LDS) for buffer b: its first
+  // key, and its K and V block addresses.
+  auto next_chunk = [&](int b, const char*& kbase, const char*& vbase) {
     const KvMeta& mt = s_tm[it_t];
-    const char* kbase = p.k + mt.koff + (int64_t)it_c * D * 2;
-    const char* vbase = p.v + mt.voff + (int64_t)it_c * D * 2;
     key0_buf[b] = mt.klo + it_c;
-    const uint32_t ldsK = lds0 + b * BUF * 2, ldsV = ldsK + KC * D * 2;
-#pragma unroll
-    for (int q = 0; q < LPW; ++q) {
-      const int inst = wid * LPW + q;
-      const int r = inst * 4 + (lane >> 4);  // key row of this lane's piece
-      const int ck = (lane & 15) ^ swz_krow(r), cv = (lane & 15) ^ swz_vrow(r);
-      dl_load16(kbase, (uint32_t)((r * D + 8 * ck) * 2), ldsK + inst * 1024);
-      dl_load16(vbase, (uint32_t)((r * D + 8 * cv) * 2), ldsV + inst * 1024);
-    }
-    it_c += KC;
-    if (it_c >= mt.kext) {
-      ++it_t;
-      it_c = 0;
-    }
+    kbase = p.k + mt.koff + (int64_t)it_c * D * 2;
+    vbase = p.v + mt.voff + (int64_t)it_c * D * 2;
+    advance(mt.kext);
   };
   // after this wave's loads have landed: its V pieces of buffer b to fp16
   auto convert_v = [&](int b) {
@@ -227,12 +245,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
   };
 
   // compute the 64-key chunk held in buffer b: S^T = K Q^T, an online
-  // softmax step, O^T += V^T P^T
-  auto compute_chunk = [&](int b) {
+  // softmax step, O^T += V^T P^T.  DIAG: some key of the chunk is past some
+  // query of the wave, so the causal mask is applied (a separate
+  // instantiation: the other chunks carry no mask arithmetic at all).
+  auto compute_chunk_impl = [&](int b, auto diag_tag, auto&& mid) {
+    constexpr bool DIAG = decltype(diag_tag)::value;
     const uint16_t* sK = sKV + b * BUF;
     const uint16_t* sV = sK + KC * D;
     const int key0 = key0_buf[b];
-    if (causal && key0 > qpos_wave_max) return;  // the whole wave is masked in this chunk
     f32x16_t acc_s[KT];
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt) acc_s[kt] = f32x16_t{};
@@ -247,15 +267,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) acc_s[kt] = mfma_bf16(a[kt], qreg[s], acc_s[kt]);
     }
+    mid();  // issued while the score MFMAs run
     // online softmax in the log2 domain; the scale is one FMA ahead of exp2
-    const bool diag = causal && key0 + KC - 1 > qpos_wave_min;  // some key is past some query
     float mx = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float sv = acc_s[kt][r];
-        if (diag) {
+        if (DIAG) {
           const int kpos = key0 + 32 * kt + 8 * (r >> 2) + 4 * g + (r & 3);
           sv = kpos > qpos ? -INFINITY : sv;
           acc_s[kt][r] = sv;
@@ -311,92 +331,56 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
         }
       }
   };
+  auto compute_chunk = [&](int b, auto&& mid) {
+    const int key0 = key0_buf[b];
+    if (causal && key0 > qpos_wave_max) mid();  // the whole wave is masked in this chunk
+    else if (causal && key0 + KC - 1 > qpos_wave_min) compute_chunk_impl(b, Bool<true>{}, mid);
+    else compute_chunk_impl(b, Bool<false>{}, mid);
+  };
 
-  // Phases: in phase ph group 0 computes chunk 2ph and group 1 chunk 2ph+1
-  // (buffers 2ph % NBUF and 2ph % NBUF + 1), while every wave issues its
-  // loads of the chunks LOOKAHEAD phases ahead into the buffers of phase ph -
-  // 1 (both groups finished them before that phase's barrier).  At the end of
-  // the phase each wave waits for its own loads of the next phase's two
-  // chunks, converts its V pieces of them, and the workgroup meets at the
-  // barrier.  The loop runs NBUF / 2 phases per iteration so that every
-  // buffer index is a compile-time constant.  (Eight 16 KiB buffers of
-  // 32-key chunks, three phases of lookahead, were measured slower: 34.8 ->
-  // 38.8 us on 2 x 4 heads of 2048 tokens; the per-phase costs doubled, and
-  // more bytes in flight did not shorten the phase.)
-  // s_waitcnt vmcnt(n) in the gfx9 encoding (vmcnt in bits 3:0 and 15:14,
-  // expcnt and lgkmcnt left at their maxima)
-  constexpr auto vmcnt = [](int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); };
-  static_assert(2 * LOOKAHEAD * 2 * LPW < 64, "vmcnt range");
-  auto wait_loads = [&](int later_chunks) {  // this wave's loads landed but those of `later_chunks` chunks
+  // The walk: chunk j is computed from buffer j % 2 while every wave issues
+  // its loads of chunk j + 1 into the other buffer (which all waves finished
+  // with before the previous barrier); then each wave waits for its own
+  // loads and the workgroup meets at the barrier.  A chunk's V pieces are
+  // turned to fp16 by the waves that loaded them once the chunk's score
+  // MFMAs are issued, and the workgroup meets again before its PV product.
+  // The loop runs two chunks per iteration so that every buffer index is a
+  // compile-time constant.  (Earlier designs measured: eight
+  // waves in two groups computing alternate chunks of one tile, with four
+  // buffers, spent most of each phase with both waves of a SIMD in the same
+  // stage -- MFMA, then VALU -- and were slower; so were 32-key chunks with
+  // three phases of lookahead, and V transposed to [d][key] once per chunk.)
+  // s_waitcnt vmcnt(0) (gfx9 encoding; expcnt and lgkmcnt at their maxima)
+  auto wait_loads = [&]() {
     asm volatile("" ::: "memory");
-    if (LOOKAHEAD == 1 || later_chunks <= 0) {
-      __builtin_amdgcn_s_waitcnt(vmcnt(0));
-    } else {
-      switch (later_chunks) {
-        case 1: __builtin_amdgcn_s_waitcnt(vmcnt(2 * LPW)); break;
-        case 2: __builtin_amdgcn_s_waitcnt(vmcnt(4 * LPW)); break;
-        case 3: __builtin_amdgcn_s_waitcnt(vmcnt(6 * LPW)); break;
-        default: __builtin_amdgcn_s_waitcnt(vmcnt(8 * LPW)); break;
-      }
-    }
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
     asm volatile("" ::: "memory");
   };
-#pragma unroll
-  for (int j = 0; j < 2 * LOOKAHEAD; ++j)
-    if (j < nc) load_chunk(j);
-  if (nc > 0) {
-    const int last = nc < 2 ? 0 : 1;  // the last chunk of phase 0
-    wait_loads(min(nc, 2 * LOOKAHEAD) - (last + 1));
-    convert_v(0);
-    if (nc > 1) convert_v(1);
-  }
+  wait_loads();
   __syncthreads();
-  const int n_phase = (nc + 1) / 2;
-  for (int ph0 = 0; ph0 < n_phase; ph0 += NBUF / 2) {
+  for (int j0 = 0; j0 < nc; j0 += NBUF) {
 #pragma unroll
-    for (int e = 0; e < NBUF / 2; ++e) {
-      const int ph = ph0 + e;
-      if (ph < n_phase) {
-        const int cb = 2 * e, lb = (2 * e + 2 * LOOKAHEAD) % NBUF;  // buffers computed / loaded
-        if (2 * ph + 2 * LOOKAHEAD < nc) load_chunk(lb);
-        if (2 * ph + 2 * LOOKAHEAD + 1 < nc) load_chunk(lb + 1);
-        if (2 * ph + grp < nc) compute_chunk(cb + grp);
-        if (2 * ph + 2 < nc) {  // the next phase's chunks
-          const int last = min(2 * ph + 3, nc - 1);
-          wait_loads(min(nc, 2 * ph + 2 + 2 * LOOKAHEAD) - (last + 1));
-          convert_v((cb + 2) % NBUF);
-          if (2 * ph + 3 < nc) convert_v((cb + 3) % NBUF);
+    for (int e = 0; e < NBUF; ++e) {
+      const int j = j0 + e;
+      if (j < nc) {
+        // the next chunk's K loads go out first
+        const char *kb = nullptr, *vb = nullptr;
+        if (j + 1 < nc) {
+          next_chunk(1 - e, kb, vb);
+          issue_k(1 - e, kb);
         }
+        // once this chunk's score MFMAs are issued: the next chunk's V loads
+        // go out, this wave's V pieces of this chunk are turned to fp16 (the
+        // MFMAs hide the conversion's latency), and the workgroup meets
+        // before the PV product reads them
+        compute_chunk(e, [&]() {
+          if (j + 1 < nc) issue_v(1 - e, vb);
+          convert_v(e);
+          __syncthreads();
+        });
+        if (j + 1 < nc) wait_loads();
         __syncthreads();
       }
-    }
-  }
-
-  // ---- merge the two groups' (m, l, O) through LDS: group 1 writes its
-  // registers lane by lane, group 0 combines them with its own.
-  {
-    float* mb = reinterpret_cast<float*>(sKV);
-    if (grp == 1) {
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mb[((wq * 64) + dt * 16 + r) * 64 + lane] = acc_o[dt][r];
-      mb[16384 + (wq * 64 + lane) * 2] = m;
-      mb[16384 + (wq * 64 + lane) * 2 + 1] = l;
-    }
-    __syncthreads();
-    if (grp == 0) {
-      const float m1 = mb[16384 + (wq * 64 + lane) * 2], l1 = mb[16384 + (wq * 64 + lane) * 2 + 1];
-      const float M = fmaxf(m, m1);
-      const float Mu = M == -INFINITY ? 0.0f : M;
-      const float a0 = fast_exp2(m - Mu), a1 = fast_exp2(m1 - Mu);
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          acc_o[dt][r] = acc_o[dt][r] * a0 + mb[((wq * 64) + dt * 16 + r) * 64 + lane] * a1;
-      l = l * a0 + l1 * a1;
-      m = M;
     }
   }
 
@@ -415,7 +399,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
     };
     auto o_piece = [&](int q) { return (uint32_t)(((wq * 16 + q) * 64 + lane) * 16); };
     const uint32_t ml_off = (uint32_t)((wq * 32 + lq) * 8);
-    if (grp == 0) {
+    {
       const auto ro = o_rsrc(u.slot);
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
@@ -434,79 +418,89 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(const AttnArgs p) {
     __syncthreads();
     if (tid == 0) s_last = arrive_agent(p.counters + u.counter) == u.n_parts - 1;
     __syncthreads();
-    if (!s_last || grp != 0) return;
+    if (!s_last) return;
     if (tid == 0) reset_agent(p.counters + u.counter);  // ready for the next call (stream-ordered)
     auto load_ml = [&](int slot) {
       const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(ml_rsrc(slot), ml_off, 0, kCoherent);
       return make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
     };
-    // acc_o = a_own * acc_o + w * O_slot, loads in batches of 8 pieces
-    auto add_slot = [&](int slot, float a_own, float w) {
+    // one part's partial, its 16 O pieces and its (m, l), in one batch of
+    // loads
+    auto load_part = [&](int slot, u32x4_t (&o)[16], float2& ml) {
+      ml = load_ml(slot);
       const auto ro = o_rsrc(slot);
 #pragma unroll
-      for (int q0 = 0; q0 < 16; q0 += 8) {
-        u32x4_t v[8];
+      for (int t = 0; t < 16; ++t) o[t] = __builtin_amdgcn_raw_buffer_load_b128(ro, o_piece(t), 0, kCoherent);
+    };
+    // acc_o = a_own * acc_o + w * O_part; both products rounded before the
+    // add (no fused multiply-add)
+    auto add_part = [&](const u32x4_t (&o)[16], float a_own, float w) {
 #pragma unroll
-        for (int t = 0; t < 8; ++t) v[t] = __builtin_amdgcn_raw_buffer_load_b128(ro, o_piece(q0 + t), 0, kCoherent);
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-          // both products rounded before the add (no fused multiply-add):
-          // the sum must not depend on which operand is own and which loaded
+      for (int t = 0; t < 16; ++t) {
 #pragma clang fp contract(off)
-          f32x16_t& c = acc_o[(q0 + t) / 4];
-          const int r0 = 4 * ((q0 + t) % 4);
-          c[r0] = c[r0] * a_own + __uint_as_float(v[t].x) * w;
-          c[r0 + 1] = c[r0 + 1] * a_own + __uint_as_float(v[t].y) * w;
-          c[r0 + 2] = c[r0 + 2] * a_own + __uint_as_float(v[t].z) * w;
-          c[r0 + 3] = c[r0 + 3] * a_own + __uint_as_float(v[t].w) * w;
-        }
-        __builtin_amdgcn_sched_barrier(0);
+        f32x16_t& c = acc_o[t / 4];
+        const int r0 = 4 * (t % 4);
+        c[r0] = c[r0] * a_own + __uint_as_float(o[t].x) * w;
+        c[r0 + 1] = c[r0 + 1] * a_own + __uint_as_float(o[t].y) * w;
+        c[r0 + 2] = c[r0 + 2] * a_own + __uint_as_float(o[t].z) * w;
+        c[r0 + 3] = c[r0 + 3] * a_own + __uint_as_float(o[t].w) * w;
       }
     };
-    if (u.n_parts == 2) {
+    const int np = u.n_parts;
+    if (np == 2) {
       // own + other: every term is formed the same way whichever part holds
       // it, and a + b == b + a exactly, so the bits do not depend on which
       // part arrived last
-      const float2 ml1 = load_ml(u.first_slot + (u.slot == u.first_slot ? 1 : 0));
+      u32x4_t o[16];
+      float2 ml1;
+      load_part(u.first_slot + (u.slot == u.first_slot ? 1 : 0), o, ml1);
       const float M = fmaxf(m, ml1.x);
       const float Mu = M == -INFINITY ? 0.0f : M;
       const float a0 = exp2f(m - Mu), a1 = exp2f(ml1.x - Mu);
-      add_slot(u.first_slot + (u.slot == u.first_slot ? 1 : 0), a0, a1);
+      add_part(o, a0, a1);
       {
 #pragma clang fp contract(off)
         l = l * a0 + ml1.y * a1;
       }
     } else {
       // more parts: from zero, in part order (own partial re-read), a fixed
-      // order whoever arrives last
+      // order whoever arrives last.  The common max first, from (m, l) loads
+      // eight parts at a time (a short batch repeats the last part).
       float M = -INFINITY;
-      for (int q = 0; q < u.n_parts; ++q) M = fmaxf(M, load_ml(u.first_slot + q).x);
+      for (int q0 = 0; q0 < np; q0 += 8) {
+        float2 mb[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) mb[i] = load_ml(u.first_slot + min(q0 + i, np - 1));
+#pragma unroll
+        for (int i = 0; i < 8; ++i) M = fmaxf(M, mb[i].x);
+      }
       const float Mu = M == -INFINITY ? 0.0f : M;
       l = 0.0f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) acc_o[i] = f32x16_t{};
-      for (int q = 0; q < u.n_parts; ++q) {
-        const float2 mlq = load_ml(u.first_slot + q);
+      // then the parts in order, each part's loads in one batch
+      for (int q = 0; q < np; ++q) {
+        u32x4_t o[16];
+        float2 mlq;
+        load_part(u.first_slot + q, o, mlq);
         const float w = exp2f(mlq.x - Mu);
-        add_slot(u.first_slot + q, 1.0f, w);
+        add_part(o, 1.0f, w);
         l += mlq.y * w;
       }
     }
   }
 
-  // ---- epilogue (group 0).  acc_o[dt] register r of lane (lq, g) holds O^T
-  // row d = 32 dt + 8 (r/4) + 4 g + r%4, column = this lane's query.
-  if (grp != 0) return;
+  // ---- epilogue.  acc_o[dt] register r of lane (lq, g) holds O^T row
+  // d = 32 dt + 8 (r/4) + 4 g + r%4, column = this lane's query.
   const float inv = l > 0.0f ? 1.0f / l : 0.0f;
   char* orow = p.o + ooff;
   if (p.dt_o == EA_BF16) {
-    // Each wave stages its 32 rows in its own LDS region (past the group
-    // merge area, so no barrier with the other waves) and writes them as
+    // Each wave stages its 32 rows in its own LDS region (the chunk
+    // buffers are free after the walk's last barrier) and writes them as
     // 16-byte pieces of contiguous rows: the tile's rows are contiguous in
     // the O block, so every store instruction writes whole lines.
     constexpr int kPitch = 128 * 2 + 16;  // bytes per staged row
-    char* stage = reinterpret_cast<char*>(sKV) + kEpiStageOffset + wq * 32 * kPitch;
+    char* stage = reinterpret_cast<char*>(sKV) + wq * 32 * kPitch;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -554,8 +548,20 @@ __global__ __launch_bounds__(64) void attn_prep_kernel(const AttnArgs p) {
     um.qoff = qb.off;
     um.ooff = p.blk_o[p.tuples[(int64_t)gb * 4 + 0]].off;
     um.q_lo = qb.lo[p.q_dim];
-    um.nt = min(te - tb, kAttnMaxUnitTuples);
+    const int nt = min(te - tb, kAttnMaxUnitTuples);
+    um.nt = nt;
     if (te - tb > kAttnMaxUnitTuples) *p.overflow = 1;  // the host refuses the plan
+    // the walk's chunks: every kAttnChunkKeys keys of the unit's blocks, in
+    // tuple order, up to the first chunk past the tile's last query (later
+    // ones are masked for every row under the causal predicate)
+    const int qpos_tile_max = qb.lo[p.q_dim] + u.q0 + kAttnTileRows - 1;
+    int nc = 0;
+    for (int t = 0; t < nt; ++t) {
+      const DevBlk& kb = p.blk_k[p.tuples[(int64_t)(tb + t) * 4 + 2]];
+      const int klo = kb.lo[p.k_dim], kext = kb.ext[p.k_dim];
+      for (int c0 = 0; c0 < kext && !(p.causal && klo + c0 > qpos_tile_max); c0 += kAttnChunkKeys) ++nc;
+    }
+    um.nc = nc;
   }
   for (int t = lane; t < te - tb && t < kAttnMaxUnitTuples; t += 64) {
     const int32_t* tp = p.tuples + (int64_t)(tb + t) * 4;

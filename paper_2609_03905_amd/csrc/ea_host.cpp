@@ -1134,9 +1134,10 @@ int attention_units(const ea_relation* Q, const std::vector<int32_t>& goff, Attn
     for (int64_t q0 = 0; q0 < q_ext; q0 += 128) tiles.push_back(TileWork{g, q0, n_t});
   }
   // key blocks per unit (the online-softmax partial): the run that minimises
-  // waves of units over the 256 CUs x (longest unit + half a key block per
-  // extra part of a split tile, the merge); ties go to the longer run
-  const int kCUs = 256;
+  // waves of units over the 512 workgroup slots (two per CU) x (longest
+  // unit + half a key block per extra part of a split tile, the merge); ties
+  // go to the longer run
+  const int kCUs = 512;
   int max_nt = 1;
   for (const TileWork& t : tiles) max_nt = std::max(max_nt, t.n_t);
   int chunk = kAttnMaxUnitTuples;

@@ -308,10 +308,13 @@ struct AttnKv {
   int64_t koff, voff;  // byte offsets of the K and V blocks
   int32_t klo, kext;   // key interval of the block
 };
+constexpr int kAttnChunkKeys = 64;  // keys the attention kernel stages per chunk
+constexpr int kAttnTileRows = 128;  // query rows of an attention work unit
 struct AttnUnitMeta {
   int64_t qoff, ooff;  // byte offsets of the unit's Q and O blocks
   int32_t q_lo, nt;    // query position of the Q block's first row; the unit's tuples
-  int32_t pad[2];
+  int32_t nc;          // kAttnChunkKeys-key chunks of the unit's walk (causal cut applied)
+  int32_t pad;
   AttnKv kv[kAttnMaxUnitTuples];
 };
 
