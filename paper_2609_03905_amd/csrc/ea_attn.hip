@@ -115,9 +115,16 @@ __device__ __forceinline__ void dl_load16(const char* base, uint32_t voff, uint3
 #pragma clang diagnostic pop
 }
 
-__device__ __forceinline__ uint2 tr_read(const uint16_t* p) {
-  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
-  return __builtin_bit_cast(uint2, v);
+__device__ __forceinline__ s16x4 tr_read(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
+}
+// the PV MFMA's A operand from two transposing reads, concatenated as one
+// vector (so that the reads can land in the operand's registers directly)
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ f32x16_t mfma_f16_tr(const s16x4& lo, const s16x4& hi, const uint4& b, const f32x16_t& c) {
+  const s16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), c, 0,
+                                                 0, 0);
 }
 
 // 2^x on the transcendental unit; arguments here are at most kLazyMax, and
@@ -325,9 +332,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
           const int d = 32 * dt + 16 * (gq & 1) + 4 * (li & 3);
-          const uint2 v0 = tr_read(sV + k0 * D + 8 * ((d >> 3) ^ swz_vrow(k0)) + (d & 4));
-          const uint2 v1 = tr_read(sV + (k0 + 8) * D + 8 * ((d >> 3) ^ swz_vrow(k0 + 8)) + (d & 4));
-          acc_o[dt] = mfma_f16(make_uint4(v0.x, v0.y, v1.x, v1.y), ph, acc_o[dt]);
+          const s16x4 v0 = tr_read(sV + k0 * D + 8 * ((d >> 3) ^ swz_vrow(k0)) + (d & 4));
+          const s16x4 v1 = tr_read(sV + (k0 + 8) * D + 8 * ((d >> 3) ^ swz_vrow(k0 + 8)) + (d & 4));
+          acc_o[dt] = mfma_f16_tr(v0, v1, ph, acc_o[dt]);
         }
       }
   };
@@ -372,7 +379,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
         // once this chunk's score MFMAs are issued: the next chunk's V loads
         // go out, this wave's V pieces of this chunk are turned to fp16 (the
         // MFMAs hide the conversion's latency), and the workgroup meets
-        // before the PV product reads them
+        // before the PV product reads them.  (Issuing the K loads there too
+        // was measured 1-3% slower.)
         compute_chunk(e, [&]() {
           if (j + 1 < nc) issue_v(1 - e, vb);
           convert_v(e);
