@@ -71,10 +71,6 @@ __device__ __forceinline__ f32x16_t mfma_bf16(const uint4& a, const uint4& b, co
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ f32x16_t mfma_f16(const uint4& a, const uint4& b, const f32x16_t& c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), c,
-                                                 0, 0, 0);
-}
 
 // two floats -> packed fp16 pair, round to nearest even (v_cvt_pk_f16_f32)
 __device__ __forceinline__ uint32_t pack_f16(float x0, float x1) {

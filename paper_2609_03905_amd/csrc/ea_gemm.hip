@@ -13,8 +13,10 @@
 // Inputs bf16 or f16, fp32 accumulation (v_mfma_f32_32x32x16_{bf16,f16}).
 // 512 threads = 8 waves in a 2 (rows) x 4 (columns) grid, two waves per SIMD
 // so that one wave's LDS reads overlap the other's MFMAs.  Tile 256 x 256
-// (each wave 128 x 64: 4 x 2 MFMA tiles, 128 accumulators), or for SwiGLU
-// 256 x 128 with two right operands (each wave 128 x 32 per operand).
+// (each wave 128 x 64: 4 x 2 MFMA tiles, 128 accumulators), or 256 x 128
+// (each wave 128 x 32), which a plan takes when 256-wide tiles would leave
+// CUs idle or need split sums; for SwiGLU 256 x 128 with two right operands
+// (each wave 128 x 32 per operand).
 //
 // Two K pipelines share the tile layout and the epilogue:
 //   * gemm_dl_kernel (every contracted block extent a multiple of 32): operands
@@ -605,11 +607,11 @@ __device__ __forceinline__ void stage_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <bool BF16, bool KMAJOR, bool SWIGLU, int W>
+template <bool BF16, bool KMAJOR, bool SWIGLU, bool NARROW, int W>
 __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
-  constexpr int WGN = W / 2;                   // waves along n (2 along m)
-  constexpr int NB = SWIGLU ? 2 : 1;           // right operands
-  constexpr int BN = SWIGLU ? 128 : 256;       // columns per right operand
+  constexpr int WGN = W / 2;                         // waves along n (2 along m)
+  constexpr int NB = SWIGLU ? 2 : 1;                 // right operands
+  constexpr int BN = SWIGLU || NARROW ? 128 : 256;  // columns per right operand
   constexpr int WCOLS = BN / WGN;              // columns per wave, per operand
   constexpr int WN = WCOLS / 32;               // MFMA tiles per wave along n, per operand
   constexpr int A_ELEMS = TM * DK;             // per stage
@@ -880,8 +882,11 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
 
 template <bool BF16, bool KMAJOR, bool SWIGLU>
 hipError_t launch3(const GemmArgs& a, hipStream_t s) {
-  if (a.direct)
-    hipLaunchKernelGGL((gemm_dl_kernel<BF16, KMAJOR, SWIGLU, 8>), dim3((uint32_t)a.n_units), dim3(512), 0, s, a);
+  if (a.direct && !SWIGLU && a.tile_n == 128)
+    hipLaunchKernelGGL((gemm_dl_kernel<BF16, KMAJOR, false, true, 8>), dim3((uint32_t)a.n_units), dim3(512), 0, s, a);
+  else if (a.direct)
+    hipLaunchKernelGGL((gemm_dl_kernel<BF16, KMAJOR, SWIGLU, false, 8>), dim3((uint32_t)a.n_units), dim3(512), 0, s,
+                       a);
   else
     hipLaunchKernelGGL((gemm_kernel<BF16, KMAJOR, SWIGLU, 8>), dim3((uint32_t)a.n_tiles), dim3(512), 0, s, a);
   return hipGetLastError();

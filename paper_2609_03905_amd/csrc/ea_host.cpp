@@ -322,6 +322,7 @@ struct Plan {
   int b_kmajor = 0;
   int gemm_parts = 1;
   bool gemm_direct = false;  // direct-load kernel (work list of GemmUnit), else GemmTile
+  int gemm_tn = kGemmTN;     // output tile columns per right operand (256, or 128)
   // rows
   RowLayout rows;
   AttnUnitMeta* attn_meta = nullptr;
@@ -770,14 +771,22 @@ int build_generic(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_rela
 // Units are then ordered so that the workgroups one XCD receives (ids
 // congruent mod 8) form a compact rectangle of the tile grid and share
 // operand panels in that XCD's L2.
+// K-step time of a 256 x 128 tile over that of a 256 x 256 one.  Measured on
+// the block share's QKV projection (2048 x 8192 x 3072), 192 workgroups
+// either way: 256 x 128 tiles, 256 K steps each, 142.6 us; 256 x 256 tiles
+// split in two, 128 K steps each plus the merge, 107.8 us (about 15 us of it
+// the merge): 0.557 against 0.725 us per step.
+constexpr double kNarrowStep = 0.77;
+
 struct GemmPlanInfo {
   std::vector<GemmTile> units;
   int32_t slots = 0, counters = 0;
   int parts = 1;
 };
 
-GemmPlanInfo gemm_units(const ea_relation* a, const ea_relation* c, int tn) {
+GemmPlanInfo gemm_units(const ea_relation* a, const ea_relation* c, int tn, double step_scale = 1.0) {
   const int kCUs = 256;
+  const double tile_bytes = (double)kGemmTM * tn * 4;
   // K steps of a group: every group has the same contracted blocks (a's column blocks)
   int64_t steps = 0;
   const int n_t = a->nb[1];
@@ -806,7 +815,7 @@ GemmPlanInfo gemm_units(const ea_relation* a, const ea_relation* c, int tn) {
   for (int P = 1; P <= std::min(n_t, 16); ++P) {
     const int64_t units = tiles * P;
     const double waves = (double)((units + kCUs - 1) / kCUs);
-    const double t = waves * (double)((steps + P - 1) / P) * 1.0 + (P > 1 ? units * 2.0 * 262144.0 / 4.0e6 : 0.0);
+    const double t = waves * (double)((steps + P - 1) / P) * step_scale + (P > 1 ? units * 2.0 * tile_bytes / 4.0e6 : 0.0);
     if (t < best_t - 1e-9) {
       best_t = t;
       best_p = P;
@@ -911,11 +920,14 @@ struct GemmDlPlan {
   std::vector<GemmUnit> units;
   int32_t slots = 0, counters = 0;
   bool balanced = false;
+  double cost = 0.0;  // the model's time of the kept schedule (us)
 };
 
-GemmDlPlan gemm_units_dl(const ea_relation* a, const ea_relation* c, int tn, const GemmPlanInfo& even) {
+GemmDlPlan gemm_units_dl(const ea_relation* a, const ea_relation* c, int tn, const GemmPlanInfo& even,
+                         double step_scale = 1.0) {
   const int kCUs = 256;
-  const double t_step = 0.75, t_seg = 1.0, bw = 5.0e6, tile_bytes = 262144.0, n_sat = 190.0;
+  const double t_step = 0.75 * step_scale, t_seg = 1.0, bw = 5.0e6, tile_bytes = (double)kGemmTM * tn * 4,
+               n_sat = 190.0;
   auto step_time = [&](int64_t busy_cus) { return t_step * std::max(1.0, (double)busy_cus / n_sat); };
   // K-step prefix over a group's tuples (A's contracted blocks, in order)
   const int n_t = a->nb[1];
@@ -971,6 +983,7 @@ GemmDlPlan gemm_units_dl(const ea_relation* a, const ea_relation* c, int tn, con
         }
     }
   }
+  ev.cost = ev_cost;
   const int64_t T = (int64_t)tiles.size(), total = T * S;
   if (T == 0 || S == 0 || T >= kCUs) return ev;  // a full wave of tiles: nothing to balance
   const int64_t q = (total + kCUs - 1) / kCUs;    // steps per unit (< S: at most two tiles per unit)
@@ -1015,6 +1028,7 @@ GemmDlPlan gemm_units_dl(const ea_relation* a, const ea_relation* c, int tn, con
     bytes += merge_bytes(parts);
   }
   const double bal_cost = (double)q * step_time((int64_t)bal.units.size()) + 2.0 * t_seg + bytes / bw;
+  bal.cost = bal_cost;
   // EA_GEMM_SCHEDULE=even|balanced overrides the model when a plan is built
   const char* force = getenv("EA_GEMM_SCHEDULE");
   if (force && !strcmp(force, "even")) return ev;
@@ -1236,9 +1250,8 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
   switch (oi.kind) {
     case K_GENERIC: e = build_generic(sp, join_op, agg_op, ops, ji, res, &img, &ex); break;
     case K_GEMM: {
-      const int tn = join_op == EA_OP_SWIGLU ? kGemmTNSwiglu : kGemmTN;
-      const GemmPlanInfo gi = gemm_units(ops[0], ops[sp.n_in], tn);
-      p->gemm_parts = gi.parts;
+      const bool swiglu = join_op == EA_OP_SWIGLU;
+      int tn = swiglu ? kGemmTNSwiglu : kGemmTN;
       // direct-to-LDS kernel: contracted block extents multiples of 32, at
       // most kGemmMaxTuples tuples per group (staged in LDS) and operand
       // blocks below 4 GiB (32-bit lane offsets); else the register-staged one
@@ -1247,9 +1260,28 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
       bool small = true;
       for (int i = 0; i < sp.n_in; ++i) small &= max_block_bytes(ops[i]) < (int64_t(1) << 32);
       p->gemm_direct = k32 && ops[0]->nb[1] <= kGemmMaxTuples && small;
+      GemmPlanInfo gi = gemm_units(ops[0], ops[sp.n_in], tn);
+      GemmDlPlan dl;
+      if (p->gemm_direct) dl = gemm_units_dl(ops[0], ops[sp.n_in], tn, gi);
+      if (p->gemm_direct && !swiglu) {
+        // 256 x 128 tiles: twice the workgroups for the same work, so fewer
+        // split sums (or none) where 256-wide tiles leave CUs idle; a K step
+        // of one costs kNarrowStep of a 256-wide one (the operand bytes per
+        // MFMA rise by half)
+        const GemmPlanInfo gn = gemm_units(ops[0], ops[sp.n_in], kGemmTNSwiglu, kNarrowStep);
+        const GemmDlPlan dn = gemm_units_dl(ops[0], ops[sp.n_in], kGemmTNSwiglu, gn, kNarrowStep);
+        const char* force = getenv("EA_GEMM_TILE_N");  // 128 or 256 overrides the model when a plan is built
+        const bool narrow = force ? atoi(force) == 128 : dn.cost < dl.cost;
+        if (narrow) {
+          tn = kGemmTNSwiglu;
+          gi = gn;
+          dl = dn;
+        }
+      }
+      p->gemm_tn = tn;
+      p->gemm_parts = gi.parts;
       int64_t slots = gi.slots;
       if (p->gemm_direct) {
-        const GemmDlPlan dl = gemm_units_dl(ops[0], ops[sp.n_in], tn, gi);
         ex.work = img.put_vec(dl.units);
         ex.n_work = (int64_t)dl.units.size();
         slots = dl.slots;
@@ -1650,6 +1682,7 @@ int run_planned(const Plan* plan, int32_t join_op, int32_t n_in, const ea_relati
       a.res = res ? (const char*)res->data : nullptr;
       a.dt_res = res ? res->dtype : 0;
       a.direct = plan->gemm_direct;
+      a.tile_n = plan->gemm_tn;
       if (a.direct) {
         a.units = (const GemmUnit*)plan->d_work;
         a.n_units = (int32_t)plan->n_work;

@@ -196,6 +196,7 @@ struct GemmArgs {
   int32_t dt_res;
   int32_t swiglu;        // 1: out = silu(A B) * (A B2)
   int32_t direct;        // 1: direct-to-LDS kernel (contracted block extents multiples of 32)
+  int32_t tile_n;        // output tile columns per right operand: 256, or 128 (SwiGLU, or a narrow plan)
   float* partials;       // [slots][256 x 256] fp32 partial sums of split tiles
   int32_t* counters;     // one per split tile; zero between calls
 };

@@ -1,12 +1,13 @@
-"""Work schedules of the direct-load block GEMM (one GPU's share of
-'tj,jk->tk' and SwiGLU, Section 3.2, Example "Matrix multiply, decomposed").
-With fewer output tiles than CUs a plan either splits each tile's K steps
-evenly over a few workgroups, or shares all tiles' K steps out in 256 equal
-runs, a run possibly finishing one tile and starting the next (a tile cut
-into several runs is merged by the last to arrive).  The plan's cost model
-chooses; EA_GEMM_SCHEDULE forces one when a plan is built.  Integer-valued
-data make every summation order exact, so both schedules must give the same
-bits; N(0,1) data are compared with the oracle."""
+"""Work schedules and tile shapes of the direct-load block GEMM (one GPU's
+share of 'tj,jk->tk' and SwiGLU, Section 3.2, Example "Matrix multiply,
+decomposed").  With fewer output tiles than CUs a plan either splits each
+tile's K steps evenly over a few workgroups, or shares all tiles' K steps out
+in 256 equal runs, a run possibly finishing one tile and starting the next (a
+tile cut into several runs is merged by the last to arrive); and a plain
+product may take 256 x 128 tiles instead of 256 x 256 ones.  The plan's cost
+model chooses; EA_GEMM_SCHEDULE and EA_GEMM_TILE_N force a choice when a plan
+is built.  Integer-valued data make every summation order exact, so every
+choice must give the same bits; N(0,1) data are compared with the oracle."""
 import os
 
 import numpy as np
@@ -21,16 +22,20 @@ from paper_2609_03905_amd import ea
 pytestmark = pytest.mark.gpu
 
 
-def _run(schedule, spec, op, ins, out_shape, part, dtype="bf16"):
+def _run(schedule, spec, op, ins, out_shape, part, dtype="bf16", tile_n=None, residual=None):
     ea.plan_cache_clear()
-    os.environ["EA_GEMM_SCHEDULE"] = schedule
+    env = {"EA_GEMM_SCHEDULE": schedule}
+    if tile_n is not None:
+        env["EA_GEMM_TILE_N"] = str(tile_n)
+    os.environ.update(env)
     try:
         Y = ea.Relation(out_shape, dtype, part)
         Y.data.fill_(0xFF)
-        ea.joinagg(spec, op, ea.AGG_SUM, ins, Y)
+        ea.joinagg(spec, op, ea.AGG_SUM, ins, Y, residual=residual)
         torch.cuda.synchronize()
     finally:
-        del os.environ["EA_GEMM_SCHEDULE"]
+        for k in env:
+            del os.environ[k]
         ea.plan_cache_clear()
     return Y
 
@@ -76,3 +81,42 @@ def test_balanced_schedule_swiglu_and_ragged_blocks_match_the_oracle():
     ref = oracle.silu_mul(oracle.matmul(fh, synth.to_f64(wg, "bf16")), oracle.matmul(fh, synth.to_f64(wu, "bf16")))
     for Y, name in ((Yb, "balanced"), (Ye, "even")):
         assert_close(synth.to_f64(download(Y), "bf16"), expected(ref, "bf16"), what=f"swiglu {name}")
+
+
+@pytest.mark.parametrize("kmajor", [False, True])
+def test_narrow_and_wide_tiles_agree_on_integer_data(kmajor):
+    # 768 x 2048 x 1472 in 512-blocks (the last output block 448 wide, so
+    # 256 x 128 tiles end half masked): wide and narrow tiles, each with the
+    # even and the balanced schedule, give the same exact sums
+    T, J, K = 768, 2048, 1472
+    print(f"tile-width test, kmajor={kmajor}", flush=True)
+    x = synth.integers((T, J), 996, -2, 3, dtype="bf16")
+    w = synth.integers((K, J) if kmajor else (J, K), 997, -2, 3, dtype="bf16")
+    pk = synth.splits(K, 512)
+    X = upload(x, "bf16", [synth.splits(T, 512), synth.splits(J, 512)])
+    W = upload(w, "bf16", [pk, synth.splits(J, 512)] if kmajor else [synth.splits(J, 512), pk])
+    spec = "tj,kj->tk" if kmajor else "tj,jk->tk"
+    py = [synth.splits(T, 512), pk]
+    outs = [_run(sch, spec, ea.JOIN_MUL, [X, W], (T, K), py, "f32", tile_n=tn)
+            for tn in (256, 128) for sch in ("even", "balanced")]
+    for Y in outs[1:]:
+        assert torch.equal(outs[0].bytes(), Y.bytes())
+    fx, fw = synth.to_f64(x, "bf16"), synth.to_f64(w, "bf16")
+    ref = oracle.matmul(fx, fw.T.copy() if kmajor else fw)
+    assert np.array_equal(download(outs[1]).astype(np.float64), ref)
+
+
+def test_narrow_tiles_with_residual_match_the_oracle():
+    # the O projection's shape cut to 512 tokens, bf16 out with a residual:
+    # 2 x 64 tiles of 256 x 128
+    T, J, K = 512, 1024, 8192
+    a = synth.normal((T, J), 998, dtype="bf16")
+    w = synth.normal((J, K), 999, 0.02, dtype="bf16")
+    r = synth.normal((T, K), 1000, dtype="bf16")
+    py = [synth.splits(T, 512), synth.splits(K, 512)]
+    A = upload(a, "bf16", [synth.splits(T, 512), synth.splits(J, 512)])
+    W = upload(w, "bf16", [synth.splits(J, 512), synth.splits(K, 512)])
+    R = upload(r, "bf16", py)
+    Y = _run("even", "tj,jk->tk", ea.JOIN_MUL, [A, W], (T, K), py, "bf16", tile_n=128, residual=R)
+    ref = oracle.matmul(synth.to_f64(a, "bf16"), synth.to_f64(w, "bf16")) + synth.to_f64(r, "bf16")
+    assert_close(synth.to_f64(download(Y), "bf16"), expected(ref, "bf16"), what="narrow tiles + residual")
