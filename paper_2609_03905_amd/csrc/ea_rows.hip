@@ -174,7 +174,6 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
   uint4 v[K];
   int seg[K], e0s[K];
   bool vis[K];
-  float part = SOFTMAX ? -INFINITY : 0.0f;
 #pragma unroll
   for (int k = 0; k < K; ++k) {
     const int c = k * 64 + lane;
@@ -242,7 +241,56 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     __syncthreads();
   }
   if (!active) return;
+  float scale = 0.0f, m = 0.0f;
+  // softmax rows of at most 4 chunks per lane keep their exponentials from
+  // the sum for the output, instead of computing them a second time
+  constexpr bool KEEP = SOFTMAX && K <= 4;
+  float ex[KEEP ? K : 1][KEEP ? 8 : 1];
+#pragma unroll
+  for (int k = 0; k < (KEEP ? K : 1); ++k)
+#pragma unroll
+    for (int i = 0; i < (KEEP ? 8 : 1); ++i) ex[k][i] = 0.0f;
+  if constexpr (KEEP) {
+    // Scores to the log2 domain once, kept in registers; the causal mask
+    // (-inf, whose exponential is an exact 0) only where a lane's chunk
+    // reaches past the row's query position, at most one chunk per row; the
+    // max; then 2^(s - m) with one FMA and one exp per element.
+    constexpr float kLog2e = 1.4426950408889634f;
+    float part = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (!vis[k]) continue;
+      float f[8];
+      unpack<XT>(v[k], f);
+#pragma unroll
+      for (int i = 0; i < EPC; ++i) ex[k][i] = f[i];
+      if (a.causal) {
+        const int k0 = klo(seg[k]) + e0s[k];
+        if (__any(k0 + EPC - 1 > qpos)) {
+#pragma unroll
+          for (int i = 0; i < EPC; ++i) ex[k][i] = k0 + i <= qpos ? ex[k][i] : -INFINITY;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < EPC; ++i) part = fmaxf(part, ex[k][i]);
+    }
+    m = wave_max(part);
+    const float mb = m == -INFINITY ? 0.0f : m * kLog2e;  // all entries -inf: every term 0
+    float l = 0.0f;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (!vis[k]) continue;
+#pragma unroll
+      for (int i = 0; i < EPC; ++i) {
+        ex[k][i] = __builtin_amdgcn_exp2f(fmaf(ex[k][i], kLog2e, -mb));
+        l += ex[k][i];
+      }
+    }
+    l = wave_sum(l);
+    scale = m == -INFINITY ? 0.0f : 1.0f / l;
+  } else {
   // local partials, then the aggregation across lanes
+  float part = SOFTMAX ? -INFINITY : 0.0f;
 #pragma unroll
   for (int k = 0; k < K; ++k) {
     if (!vis[k]) continue;
@@ -259,15 +307,6 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
       }
     }
   }
-  float scale = 0.0f, m = 0.0f;
-  // softmax rows of at most 4 chunks per lane keep their exponentials from
-  // the sum for the output, instead of computing them a second time
-  constexpr bool KEEP = SOFTMAX && K <= 4;
-  float ex[KEEP ? K : 1][KEEP ? 8 : 1];
-#pragma unroll
-  for (int k = 0; k < (KEEP ? K : 1); ++k)
-#pragma unroll
-    for (int i = 0; i < (KEEP ? 8 : 1); ++i) ex[k][i] = 0.0f;
   if constexpr (SOFTMAX) {
     m = wave_max(part);
     float l = 0.0f;
@@ -280,9 +319,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
 #pragma unroll
       for (int i = 0; i < EPC; ++i) {
         const bool ok = !a.causal || k0 + i <= qpos;
-        const float e = ok ? __expf(f[i] - m) : 0.0f;
-        if constexpr (KEEP) ex[k][i] = e;
-        l += e;
+        l += ok ? __expf(f[i] - m) : 0.0f;
       }
     }
     l = wave_sum(l);
@@ -290,6 +327,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
   } else {
     const float ss = wave_sum(part);
     scale = 1.0f / sqrtf(ss / (float)a.row_len + a.eps);
+  }
   }
   // write the row, under the output store policy (one branch around the
   // whole loop, see store_out)
