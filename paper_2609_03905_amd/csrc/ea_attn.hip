@@ -259,6 +259,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
     f32x16_t acc_s[KT];
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt) acc_s[kt] = f32x16_t{};
+    // wave priority up while this wave's MFMAs issue: the SIMD's other wave
+    // (the other workgroup's) fills the gaps with its VALU work
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       uint4 a[KT];
@@ -270,6 +273,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) acc_s[kt] = mfma_bf16(a[kt], qreg[s], acc_s[kt]);
     }
+    __builtin_amdgcn_s_setprio(0);
     mid();  // issued while the score MFMAs run
     // online softmax in the log2 domain; the scale is one FMA ahead of exp2
     float mx = -INFINITY;
@@ -316,6 +320,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
     // MFMA k index 8 g + e maps to key 32 kt + 16 h + 4 g + e (e < 4) or
     // 32 kt + 16 h + 8 + 4 g + (e - 4); P in fp16 (RNE), V in fp16
     const int gq = lane >> 4, li = lane & 15;
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
@@ -333,6 +338,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
           acc_o[dt] = mfma_f16_tr(v0, v1, ph, acc_o[dt]);
         }
       }
+    __builtin_amdgcn_s_setprio(0);
   };
   auto compute_chunk = [&](int b, auto&& mid) {
     const int key0 = key0_buf[b];
