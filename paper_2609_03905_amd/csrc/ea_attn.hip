@@ -18,21 +18,23 @@
 //   * K and V chunks [key][d] (bf16, 256-byte rows) go straight from global
 //     memory into LDS (global_load_lds_dwordx4), their 16-byte chunks
 //     XOR-swizzled per key row so that the fragment reads below spread over
-//     all banks; each wave then converts the V pieces it loaded to fp16 in
-//     place (exact for values in fp16's normal range);
+//     all banks;
 //   * S^T = K Q^T on bf16 MFMA 32x32x16 (Q^T from registers), so each lane
 //     holds the scores of one query: the row max and sum need one exchange
 //     between lanes l and l^32;
+//   * while those MFMAs run, each wave converts the V pieces it loaded to
+//     fp16 in place (exact for values in fp16's normal range), and the
+//     workgroup meets;
 //   * the scale (log2 domain) is one FMA ahead of exp2; the causal mask is
 //     applied only on chunks that reach past a query of the wave;
-//   * P = 2^(S - m), in [0, 2^8] (m lags the true max by at most 8), is rounded to fp16 and O^T += V^T P^T runs
-//     on fp16 MFMA 32x32x16; the V^T operand (8 keys of one d per lane)
-//     comes from two transposing LDS reads (ds_read_b64_tr_b16) of the
-//     [key][d] chunk, with the MFMA's k order matched to the accumulator
-//     layout of S^T.
+//   * P = 2^(S - m), in [0, 2^8] (m lags the true max by at most 8), is
+//     rounded to fp16 and O^T += V^T P^T runs on fp16 MFMA 32x32x16; the V^T
+//     operand (8 keys of one d per lane) comes from two transposing LDS reads
+//     (ds_read_b64_tr_b16) of the [key][d] chunk, with the MFMA's k order
+//     matched to the accumulator layout of S^T.
 // A group whose tuples are split across units writes partial (m, l, O) to the
-// plan's scratch; the last unit to arrive (device-scope counter, no waiting)
-// merges the partials in tuple order and stores the output block rows.
+// workspace; the last unit to arrive (device-scope counter, no waiting)
+// merges the partials in a fixed order and stores the output block rows.
 #include "ea_device.h"
 
 namespace ea {
