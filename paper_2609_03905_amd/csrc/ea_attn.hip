@@ -14,7 +14,9 @@
 // meet at no common barrier, so one's softmax VALU work runs beside the
 // other's MFMAs.  Every wave computes each 64-key chunk of the walk while
 // the workgroup's loads of the next chunk land in the other of two 32 KiB
-// buffers.  Per 64-key chunk:
+// buffers; each wave issues its share of them one per score step, so that a
+// wave held by the load path waits under its own running MFMAs.  Per
+// 64-key chunk:
 //   * K and V chunks [key][d] (bf16, 256-byte rows) go straight from global
 //     memory into LDS (global_load_lds_dwordx4), their 16-byte chunks
 //     XOR-swizzled per key row so that the fragment reads below spread over
@@ -180,6 +182,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
       dl_load16(vbase, (uint32_t)((r * D + 8 * ((lane & 15) ^ swz_vrow(r))) * 2), ldsV + inst * 1024);
     }
   };
+  // one of a chunk's 2 LPW loads of this wave: q < LPW a K piece, else a V piece
+  auto issue_piece = [&](int b, int q, const char* kbase, const char* vbase) {
+    const int qq = q % LPW, inst = wid * LPW + qq;
+    const int r = inst * 4 + (lane >> 4);
+    if (q < LPW)
+      dl_load16(kbase, (uint32_t)((r * D + 8 * ((lane & 15) ^ swz_krow(r))) * 2), lds0 + b * BUF * 2 + inst * 1024);
+    else
+      dl_load16(vbase, (uint32_t)((r * D + 8 * ((lane & 15) ^ swz_vrow(r))) * 2),
+                lds0 + b * BUF * 2 + KC * D * 2 + inst * 1024);
+  };
   auto advance = [&](int kext) {
     it_c += KC;
     if (it_c >= kext) {
@@ -253,7 +265,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
   // softmax step, O^T += V^T P^T.  DIAG: some key of the chunk is past some
   // query of the wave, so the causal mask is applied (a separate
   // instantiation: the other chunks carry no mask arithmetic at all).
-  auto compute_chunk_impl = [&](int b, auto diag_tag, auto&& mid) {
+  auto compute_chunk_impl = [&](int b, auto diag_tag, auto&& mid, auto&& load) {
     constexpr bool DIAG = decltype(diag_tag)::value;
     const uint16_t* sK = sKV + b * BUF;
     const uint16_t* sV = sK + KC * D;
@@ -272,6 +284,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
         const int r = 32 * kt + lq;
         a[kt] = *reinterpret_cast<const uint4*>(sK + r * D + 8 * ((2 * s + g) ^ swz_krow(r)));
       }
+      load(s);  // one of the next chunk's loads per step, behind running MFMAs
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) acc_s[kt] = mfma_bf16(a[kt], qreg[s], acc_s[kt]);
     }
@@ -342,11 +355,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
       }
     __builtin_amdgcn_s_setprio(0);
   };
-  auto compute_chunk = [&](int b, auto&& mid) {
+  auto compute_chunk = [&](int b, auto&& mid, auto&& load) {
     const int key0 = key0_buf[b];
-    if (causal && key0 > qpos_wave_max) mid();  // the whole wave is masked in this chunk
-    else if (causal && key0 + KC - 1 > qpos_wave_min) compute_chunk_impl(b, Bool<true>{}, mid);
-    else compute_chunk_impl(b, Bool<false>{}, mid);
+    if (causal && key0 > qpos_wave_max) {  // the whole wave is masked in this chunk
+#pragma unroll
+      for (int q = 0; q < 2 * LPW; ++q) load(q);
+      mid();
+    } else if (causal && key0 + KC - 1 > qpos_wave_min) {
+      compute_chunk_impl(b, Bool<true>{}, mid, load);
+    } else {
+      compute_chunk_impl(b, Bool<false>{}, mid, load);
+    }
   };
 
   // The walk: chunk j is computed from buffer j % 2 while every wave issues
@@ -374,22 +393,23 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
     for (int e = 0; e < NBUF; ++e) {
       const int j = j0 + e;
       if (j < nc) {
-        // the next chunk's K loads go out first
+        // the next chunk's loads go out one per score step, so that a wave
+        // held by the load path waits under its own running MFMAs; once
+        // the scores are issued, this wave's V pieces of this chunk are
+        // turned to fp16 and the workgroup meets before the PV product
+        // reads them
         const char *kb = nullptr, *vb = nullptr;
-        if (j + 1 < nc) {
-          next_chunk(1 - e, kb, vb);
-          issue_k(1 - e, kb);
-        }
-        // once this chunk's score MFMAs are issued: the next chunk's V loads
-        // go out, this wave's V pieces of this chunk are turned to fp16 (the
-        // MFMAs hide the conversion's latency), and the workgroup meets
-        // before the PV product reads them.  (Issuing the K loads there too
-        // was measured 1-3% slower.)
-        compute_chunk(e, [&]() {
-          if (j + 1 < nc) issue_v(1 - e, vb);
-          convert_v(e);
-          __syncthreads();
-        });
+        const bool more = j + 1 < nc;
+        if (more) next_chunk(1 - e, kb, vb);
+        compute_chunk(
+            e,
+            [&]() {
+              convert_v(e);
+              __syncthreads();
+            },
+            [&](int q) {
+              if (more) issue_piece(1 - e, q, kb, vb);
+            });
         if (j + 1 < nc) wait_loads();
         __syncthreads();
       }
