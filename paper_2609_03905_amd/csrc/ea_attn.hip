@@ -127,14 +127,6 @@ __device__ __forceinline__ f32x16_t mfma_f16_tr(const s16x4& lo, const s16x4& hi
                                                  0, 0);
 }
 
-// The value of lane l ^ 32: v_permlane32_swap of x with itself leaves lanes
-// 32..63's values in the second result's lanes 0..31 and lanes 0..31's in
-// the first result's lanes 32..63 (no LDS round trip, unlike a bpermute).
-__device__ __forceinline__ float xor32(float x, int lane) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(lane < 32 ? r[1] : r[0]);
-}
-
 // 2^x on the transcendental unit; arguments here are at most kLazyMax, and
 // results below the normal range contribute nothing next to the at least 1
 // of the row's largest term.
@@ -312,7 +304,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
         }
         mx = fmaxf(mx, sv);
       }
-    mx = fmaxf(mx, xor32(mx, lane));
+    mx = fmaxf(mx, other32(mx));  // the lane-pair exchange, no LDS round trip
     // The running max moves only when a score passes it by more than
     // kLazyMax (log2 domain).  O / l is the same for any m the two share, P
     // stays at most 2^kLazyMax (exact range and precision in fp16), and the
@@ -329,7 +321,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
         acc_s[kt][r] = pv;
         rs += pv;
       }
-    rs += xor32(rs, lane);
+    rs += other32(rs);
     if (__any(m_new != m)) {  // a running max moved: rescale (else alpha is 1 on every lane)
       const float alpha = fast_exp2(m - m_use);
       l *= alpha;

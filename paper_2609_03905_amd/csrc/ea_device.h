@@ -135,17 +135,40 @@ __device__ __forceinline__ void st_elem(char* base, int64_t idx, int dt, float v
   }
 }
 
-// Wavefront (64 lanes) reductions.
+// Wavefront (64 lanes) reductions without LDS round trips: DPP swaps of
+// lane pairs (quad_perm 1,0,3,2) and of pair pairs (quad_perm 2,3,0,1), the
+// 8- and 16-lane mirrors, then v_permlane16_swap and v_permlane32_swap for
+// the other 16-lane row and the other 32-lane half.  At every stage a lane
+// combines its value with one that holds the same kind of partial, so every
+// lane ends with the same bits (x + y == y + x).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, true));
+}
+__device__ __forceinline__ float other16(float v) {  // the value of lane l ^ 16
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float((threadIdx.x & 16) ? r[0] : r[1]);
+}
+__device__ __forceinline__ float other32(float v) {  // the value of lane l ^ 32
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
+}
+template <class Op>
+__device__ __forceinline__ float wave_reduce(float v, Op op) {
+  v = op(v, dpp_f<0xB1>(v));   // quad_perm [1, 0, 3, 2]
+  v = op(v, dpp_f<0x4E>(v));   // quad_perm [2, 3, 0, 1]
+  v = op(v, dpp_f<0x141>(v));  // row_half_mirror
+  v = op(v, dpp_f<0x140>(v));  // row_mirror
+  v = op(v, other16(v));
+  return op(v, other32(v));
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  return wave_reduce(v, [](float a, float b) { return a + b; });
 }
 
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  return wave_reduce(v, [](float a, float b) { return fmaxf(a, b); });
 }
 
 }  // namespace ea
