@@ -214,9 +214,23 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
       else store_zeros(std::false_type{});
     }
   }
-  // RMSNorm: while the row's loads are in flight, every wave of the
-  // workgroup helps stage the weights
-  if constexpr (!SOFTMAX) {
+  // RMSNorm weights.  On the affine layout with bf16 weights each lane loads
+  // the weights of its own chunks into registers next to the row's loads
+  // (L2 hits after the first rows); otherwise every wave of the workgroup
+  // helps stage them in LDS while the row's loads are in flight.
+  constexpr bool WREG = !SOFTMAX && AFF && ES == 2;
+  uint4 wv[WREG ? K : 1];
+  if constexpr (WREG) {
+    if (a.dt_w == EA_BF16) {
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const int c = k * 64 + lane;
+        wv[k] = make_uint4(0, 0, 0, 0);
+        if (c < total && active) wv[k] = *reinterpret_cast<const uint4*>(w_at(seg[k]) + (int64_t)e0s[k] * 2);
+      }
+    }
+  }
+  if (!SOFTMAX && !(WREG && a.dt_w == EA_BF16)) {
     for (int c = threadIdx.x; c < total; c += kThreads) {
       int sg, e0;
       if constexpr (AFF) {
@@ -353,6 +367,11 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
           const bool ok = vis[k] && (!a.causal || k0 + i <= qpos);
           o[i] = ok ? __expf(f[i] - m) * scale : 0.0f;
         }
+      } else if (WREG && a.dt_w == EA_BF16) {
+        float wf[8];
+        unpack<uint16_t>(wv[WREG ? k : 0], wf);
+#pragma unroll
+        for (int i = 0; i < EPC; ++i) o[i] = wf[i] * (f[i] * scale);
       } else {
 #pragma unroll
         for (int i = 0; i < EPC; ++i) o[i] = sw[c * EPC + i] * (f[i] * scale);
