@@ -583,14 +583,10 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// Per-tuple operand metadata of one unit, staged in LDS before the pipeline
-// starts, so that the K loop reads it (once per tuple) with LDS reads and
-// never with vector-memory loads, which share a counter with the in-flight
-// operand loads.
-struct TupleMeta {
-  int64_t aoff, boff, b2off;
-  int32_t am, ak, b0, b1, b20, b21, pad0, pad1;
-};
+// The group's per-tuple operand metadata (GemmTupleMeta, resolved at plan
+// time) is staged in LDS before the pipeline starts, so that the K loop reads
+// it (once per tuple) with LDS reads and never with vector-memory loads,
+// which share a counter with the in-flight operand loads.
 
 // Workgroup barrier for the direct-load pipeline.  __syncthreads() carries a
 // workgroup-scope fence that waits for every outstanding LDS-DMA load, which
@@ -625,7 +621,7 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
   constexpr int CPR = ROWB / 16;               // 16-byte chunks per [k][n] row
   static_assert(LA >= 1 && LBO >= 1 && 4 * LS < 64, "stage shape");
   __shared__ __attribute__((aligned(1024))) uint16_t smem[NSTAGE * STAGE];
-  __shared__ TupleMeta s_meta[kGemmMaxTuples];
+  __shared__ GemmTupleMeta s_meta[kGemmMaxTuples];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -644,31 +640,11 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
   tile.slot = seg.first_slot + seg.part;
   tile.first_slot = seg.first_slot;
   tile.counter = seg.counter;
-  const int32_t gb = p.goff[tile.block], ge = p.goff[tile.block + 1];
-  const int nt = ge - gb;  // the group's tuples, <= kGemmMaxTuples (host guarantee)
-  for (int i = tid; i < nt; i += 64 * W) {
-    const int32_t* tp = p.tuples + (int64_t)(gb + i) * p.tuple_stride;
-    const DevBlk& ab = p.blk_a[tp[1]];
-    const DevBlk& bb = p.blk_b[tp[2]];
-    TupleMeta m;
-    m.aoff = ab.off;
-    m.am = ab.ext[0];
-    m.ak = ab.ext[1];
-    m.boff = bb.off;
-    m.b0 = bb.ext[0];
-    m.b1 = bb.ext[1];
-    if constexpr (SWIGLU) {
-      const DevBlk& b2 = p.blk_b2[tp[3]];
-      m.b2off = b2.off;
-      m.b20 = b2.ext[0];
-      m.b21 = b2.ext[1];
-    } else {
-      m.b2off = 0;
-      m.b20 = m.b21 = 0;
-    }
-    m.pad0 = m.pad1 = 0;
-    s_meta[i] = m;
-  }
+  // the group's tuples [gb, gb + nt), nt <= kGemmMaxTuples (host guarantee),
+  // resolved from the join at plan time: one load per tuple, no chain of
+  // dependent table lookups at the start of the kernel
+  const int gb = seg.gb, nt = seg.nt;
+  for (int i = tid; i < nt; i += 64 * W) s_meta[i] = p.meta[gb + i];
   __syncthreads();
 
   f32x16_t acc[NB][4][WN];
@@ -680,17 +656,11 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
       for (int j = 0; j < WN; ++j) acc[o][i][j] = f32x16_t{};
 
   // the segment's K steps [s0, s1) of the walk over the group's tuples (every
-  // contracted block extent is a multiple of DK): the tuple holding step s0,
-  // and how many of its steps come before s0
-  int group_steps = 0;
-  for (int i = 0; i < nt; ++i) group_steps += s_meta[i].ak / DK;
-  // a guard: never walk past the group's last step whatever the plan says
-  const int n_steps = max(0, min(seg.s1, group_steps) - seg.s0);
-  int it_t = 0, skip = seg.s0;
-  while (it_t < nt && skip >= s_meta[it_t].ak / DK) {
-    skip -= s_meta[it_t].ak / DK;
-    ++it_t;
-  }
+  // contracted block extent is a multiple of DK), from the plan: the step
+  // count (never past the group's last step), the tuple holding step s0 and
+  // how many of its steps come before s0
+  const int n_steps = seg.n_steps;
+  int it_t = seg.t0, skip = seg.skip;
 
   // ---- direct-load walk over the unit's K steps.  Per tuple, each operand
   // block has a uniform base address and each lane a 32-bit byte offset per
@@ -705,7 +675,7 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_dl_kernel(const GemmArgs p) {
   uint32_t bstep[NB];
   int left = 0;
   auto set_tuple = [&](int t) {
-    const TupleMeta& m = s_meta[t];
+    const GemmTupleMeta& m = s_meta[t];
     a_base = p.a + m.aoff;
 #pragma unroll
     for (int q = 0; q < LA; ++q) {
@@ -902,7 +872,68 @@ hipError_t launch1(const GemmArgs& a, hipStream_t s) {
   return a.b_kmajor ? launch2<BF16, true>(a, s) : launch2<BF16, false>(a, s);
 }
 
+// Plan time, after the join.  One thread per tuple of the join: its operand
+// blocks' offsets and extents, in tuple-table order.
+__global__ __launch_bounds__(256) void gemm_meta_kernel(const GemmArgs p, int64_t tuple_cap) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= tuple_cap || q >= *p.count) return;
+  const int32_t* tp = p.tuples + q * p.tuple_stride;
+  const DevBlk& ab = p.blk_a[tp[1]];
+  const DevBlk& bb = p.blk_b[tp[2]];
+  GemmTupleMeta m;
+  m.aoff = ab.off;
+  m.am = ab.ext[0];
+  m.ak = ab.ext[1];
+  m.boff = bb.off;
+  m.b0 = bb.ext[0];
+  m.b1 = bb.ext[1];
+  if (p.swiglu) {
+    const DevBlk& b2 = p.blk_b2[tp[3]];
+    m.b2off = b2.off;
+    m.b20 = b2.ext[0];
+    m.b21 = b2.ext[1];
+  } else {
+    m.b2off = 0;
+    m.b20 = m.b21 = 0;
+  }
+  m.pad[0] = m.pad[1] = m.pad[2] = m.pad[3] = 0;
+  p.meta[q] = m;
+}
+
+// Plan time, after the join.  One thread per unit: each segment's group
+// (first tuple, count) and where its K steps start in the group's walk.
+__global__ __launch_bounds__(256) void gemm_seg_kernel(const GemmArgs p, GemmUnit* units) {
+  const int u = blockIdx.x * 256 + threadIdx.x;
+  if (u >= p.n_units) return;
+  GemmUnit& un = units[u];
+  for (int k = 0; k < un.n_seg && k < kGemmMaxSegs; ++k) {
+    GemmSeg& sg = un.seg[k];
+    const int32_t gb = p.goff[sg.block], nt = p.goff[sg.block + 1] - gb;
+    auto steps = [&](int i) { return p.blk_a[p.tuples[(int64_t)(gb + i) * p.tuple_stride + 1]].ext[1] / DK; };
+    int group_steps = 0;
+    for (int i = 0; i < nt; ++i) group_steps += steps(i);
+    int t = 0, skip = sg.s0;
+    while (t < nt && skip >= steps(t)) {
+      skip -= steps(t);
+      ++t;
+    }
+    sg.gb = gb;
+    sg.nt = nt;
+    sg.t0 = t;
+    sg.skip = skip;
+    sg.n_steps = max(0, min(sg.s1, group_steps) - sg.s0);  // never past the group's last step
+  }
+}
+
 }  // namespace
+
+hipError_t launch_gemm_prep(const GemmArgs& a, GemmUnit* units, int64_t tuple_cap, hipStream_t s) {
+  if (tuple_cap > 0)
+    hipLaunchKernelGGL(gemm_meta_kernel, dim3((uint32_t)((tuple_cap + 255) / 256)), dim3(256), 0, s, a, tuple_cap);
+  if (a.n_units > 0)
+    hipLaunchKernelGGL(gemm_seg_kernel, dim3((uint32_t)((a.n_units + 255) / 256)), dim3(256), 0, s, a, units);
+  return hipGetLastError();
+}
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
   if ((a.direct ? a.n_units : a.n_tiles) == 0) return hipSuccess;

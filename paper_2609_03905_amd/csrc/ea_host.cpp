@@ -323,6 +323,7 @@ struct Plan {
   int gemm_parts = 1;
   bool gemm_direct = false;  // direct-load kernel (work list of GemmUnit), else GemmTile
   int gemm_tn = kGemmTN;     // output tile columns per right operand (256, or 128)
+  GemmTupleMeta* d_gemm_meta = nullptr;  // direct-load plans: per-tuple operand blocks
   // rows
   RowLayout rows;
   AttnUnitMeta* attn_meta = nullptr;
@@ -710,7 +711,7 @@ int classify(const Spec& sp, int32_t join_op, int32_t agg_op, const ea_relation*
 // kind-specific plan sections
 // ---------------------------------------------------------------------------
 struct Extra {
-  size_t desc = 0, work = 0;
+  size_t desc = 0, work = 0, meta = 0;
   int64_t n_work = 0;
 };
 
@@ -1284,6 +1285,7 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
       if (p->gemm_direct) {
         ex.work = img.put_vec(dl.units);
         ex.n_work = (int64_t)dl.units.size();
+        ex.meta = img.put_zero((size_t)p->tuple_cap * sizeof(GemmTupleMeta));
         slots = dl.slots;
         p->ws_counters = dl.counters;
       } else {
@@ -1324,6 +1326,25 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
   p->n_work = ex.n_work;
   e = finish_join(p.get(), js, sp.n_in + 1, s);
   if (e) return e;
+  if (oi.kind == K_GEMM && p->gemm_direct) {
+    // resolve the join into the work list: per-tuple operand blocks and
+    // each segment's place in its group's walk (the join has completed)
+    p->d_gemm_meta = (GemmTupleMeta*)(p->dmem + ex.meta);
+    GemmArgs a;
+    memset(&a, 0, sizeof(a));
+    a.tuples = p->d_tuples;
+    a.goff = p->d_goff;
+    a.count = p->d_count;
+    a.blk_a = p->d_blk[0];
+    a.blk_b = p->d_blk[1];
+    a.swiglu = join_op == EA_OP_SWIGLU;
+    if (a.swiglu) a.blk_b2 = p->d_blk[2];
+    a.tuple_stride = sp.n_in + 1;
+    a.n_units = (int32_t)p->n_work;
+    a.meta = p->d_gemm_meta;
+    EA_HIP_TRY(launch_gemm_prep(a, (GemmUnit*)(p->dmem + ex.work), p->tuple_cap, s));
+    EA_HIP_TRY(hipStreamSynchronize(s));
+  }
   if (oi.kind == K_ATTENTION) {
     // units from the GPU-built group offsets (the join has completed)
     std::vector<int32_t> goff((size_t)p->n_groups + 1);
@@ -1683,6 +1704,7 @@ int run_planned(const Plan* plan, int32_t join_op, int32_t n_in, const ea_relati
       a.dt_res = res ? res->dtype : 0;
       a.direct = plan->gemm_direct;
       a.tile_n = plan->gemm_tn;
+      a.meta = plan->d_gemm_meta;
       if (a.direct) {
         a.units = (const GemmUnit*)plan->d_work;
         a.n_units = (int32_t)plan->n_work;

@@ -165,8 +165,23 @@ struct GemmSeg {
   int32_t part, n_parts;  // place among the tile's segments (ascending s0); n_parts 1: not split
   int32_t first_slot;     // split tile: part i's partial sums go to workspace slot first_slot + i
   int32_t counter;        // split tile: its arrival counter
-  int32_t pad[3];
+  // resolved from the GPU join at plan time (gemm_prep_kernel): the group's
+  // first tuple and tuple count, the tuple holding step s0 and the steps of
+  // it before s0, and the segment's step count (s1 clamped to the group's)
+  int32_t gb, nt, t0, skip, n_steps;
+  int32_t pad[2];
 };
+static_assert(sizeof(GemmSeg) == 64, "GemmSeg layout");
+
+// Operand blocks of one tuple of the direct-load kernel, in tuple-table
+// order (written at plan time from the tuple table and the block records).
+struct GemmTupleMeta {
+  int64_t aoff, boff, b2off;  // block byte offsets in A, B and (SwiGLU) B2
+  int32_t am, ak;             // A block extents
+  int32_t b0, b1, b20, b21;   // B and B2 block extents
+  int32_t pad[4];
+};
+static_assert(sizeof(GemmTupleMeta) == 64, "GemmTupleMeta layout");
 constexpr int kGemmMaxSegs = 2;
 struct GemmUnit {
   GemmSeg seg[kGemmMaxSegs];
@@ -197,11 +212,16 @@ struct GemmArgs {
   int32_t swiglu;        // 1: out = silu(A B) * (A B2)
   int32_t direct;        // 1: direct-to-LDS kernel (contracted block extents multiples of 32)
   int32_t tile_n;        // output tile columns per right operand: 256, or 128 (SwiGLU, or a narrow plan)
+  GemmTupleMeta* meta;   // direct-load kernel: per-tuple operand blocks (plan time)
+  const int32_t* count;  // number of tuples of the join (plan time)
   float* partials;       // [slots][256 x 256] fp32 partial sums of split tiles
   int32_t* counters;     // one per split tile; zero between calls
 };
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
+// Plan time, after the join: fills a.meta (tuple_cap entries) and the
+// join-derived fields of every segment of a.units (direct-load plans).
+hipError_t launch_gemm_prep(const GemmArgs& a, GemmUnit* units, int64_t tuple_cap, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // fp32 block product "ab,bc->ac" / "ab,cb->ac" on the vector ALUs: a workgroup
