@@ -324,6 +324,8 @@ struct Plan {
   bool gemm_direct = false;  // direct-load kernel (work list of GemmUnit), else GemmTile
   int gemm_tn = kGemmTN;     // output tile columns per right operand (256, or 128)
   GemmTupleMeta* d_gemm_meta = nullptr;  // direct-load plans: per-tuple operand blocks
+  // repartition: tasks of kRepTaskBytesSmall (relations below kRepLargeBytes)
+  bool rep_small = false;
   // rows
   RowLayout rows;
   AttnUnitMeta* attn_meta = nullptr;
@@ -1924,6 +1926,9 @@ int get_repartition_plan(const ea_relation* src, const ea_relation* dst, bool bu
       const int R = src->rank;
       const int es = dtype_size(src->dtype);
       std::vector<RepTask> tasks;
+      int64_t rel_bytes = es;
+      for (int d = 0; d < R; ++d) rel_bytes *= src->shape[d];
+      const bool small_tasks = rel_bytes < kRepLargeBytes;
       int32_t cd[kMaxRank];
       std::vector<DevBlk> sb = dev_blocks(src);
       for (int64_t b = 0; b < dst->nblocks; ++b) {
@@ -1999,8 +2004,8 @@ int get_repartition_plan(const ea_relation* src, const ea_relation* dst, bool bu
             vec /= 2;
           }
           t.vec = vec;
-          // 16 KiB of the box per workgroup task (one pass of 256 lanes x 4 x 16 B)
-          const int64_t total = rows * rb, per = 16384;
+          // a range of the box per workgroup task (one pass of its 256 lanes)
+          const int64_t total = rows * rb, per = small_tasks ? kRepTaskBytesSmall : kRepTaskBytes;
           for (int64_t b0 = 0; b0 < total; b0 += per) {
             RepTask u = t;
             u.begin = (int32_t)b0;
@@ -2020,6 +2025,7 @@ int get_repartition_plan(const ea_relation* src, const ea_relation* dst, bool bu
       const size_t toff = img.put_vec(tasks);
       auto p = std::make_unique<Plan>();
       p->kind = K_REPART;
+      p->rep_small = small_tasks;
       int e = plan_upload(p.get(), img, s);
       if (e) return e;
       EA_HIP_TRY(hipStreamSynchronize(s));
@@ -2055,7 +2061,7 @@ int ea_repartition_ex(const ea_relation* src, ea_relation* dst, int32_t store, v
   e = get_repartition_plan(src, dst, false, s, &plan);
   if (e) return e;
   EA_HIP_TRY(launch_repartition((const RepTask*)plan->d_work, plan->n_work, (const char*)src->data,
-                                (char*)dst->data, store == EA_STORE_STREAM, s));
+                                (char*)dst->data, store == EA_STORE_STREAM, plan->rep_small, s));
   return ok();
 }
 

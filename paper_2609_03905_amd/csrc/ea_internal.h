@@ -133,8 +133,15 @@ struct RepTask {
   int32_t pad;
 };
 
+// A task copies kRepTaskBytes of one box (one pass of 256 lanes x 4 x 16
+// bytes) in relations of at least kRepLargeBytes, else kRepTaskBytesSmall (256
+// lanes x 2 x 16 bytes): where the whole copy takes a few microseconds,
+// smaller tasks put more workgroups to work at once.
+constexpr int kRepTaskBytes = 16384;
+constexpr int kRepTaskBytesSmall = 8192;
+constexpr int64_t kRepLargeBytes = int64_t(64) << 20;
 hipError_t launch_repartition(const RepTask* d_tasks, int64_t n_tasks, const char* src, char* dst, bool stream_out,
-                              hipStream_t s);
+                              bool small_tasks, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Block GEMM on the matrix cores: out = sum over the group's tuples of
