@@ -113,6 +113,16 @@ def test_repartition_qkv_output_to_heads_full_size():
     _check_repart(y, "bf16", w["pHead"], w["pY"])
 
 
+def test_repartition_large_relation_bitexact():
+    """A 64 MiB relation: the library cuts relations of at least 64 MiB into
+    16 KiB tasks (smaller ones into 8 KiB tasks).  Ragged blocks both ways."""
+    x = synth.normal((8192, 4096), 11, dtype="bf16")
+    p1 = [synth.splits(8192, 1000), synth.splits(4096, 512)]
+    p2 = [synth.splits(8192, 128), synth.splits(4096, 1536)]
+    _check_repart(x, "bf16", p1, p2)
+    _check_repart(x, "bf16", p2, p1)
+
+
 def test_repartition_round_trip_and_single_block():
     x = synth.normal((300, 200), 9, dtype="f32")
     p1 = [synth.splits(300, 64), synth.splits(200, 48)]
