@@ -1205,6 +1205,33 @@ int attention_units(const ea_relation* Q, const std::vector<int32_t>& goff, Attn
   // heaviest units first so that the long runs start early
   std::stable_sort(info->units.begin(), info->units.end(),
                    [](const AttnUnit& a, const AttnUnit& b) { return a.weight > b.weight; });
+  // Between one and two units per CU: the first 256 workgroups take a CU
+  // each, and workgroup 256 + j shares the CU of workgroup j (same XCD, the
+  // dispatch's next round).  A unit that shares its CU runs its key blocks
+  // slower (kPairCost, against 1 alone) until its partner ends.  The lightest
+  // units are already last; moving the lightest of the first round to the
+  // front gives them, rather than the heaviest, a partner.  The order with the
+  // shorter estimated longest CU is kept.
+  const int64_t n_units = (int64_t)info->units.size(), first = kCUs / 2;
+  if (n_units > first && n_units <= kCUs) {
+    constexpr double kPairCost = 1.5;
+    const int64_t m = n_units - first;
+    auto longest = [&](const std::vector<AttnUnit>& u) {
+      double t = 0;
+      for (int64_t j = 0; j < first; ++j) {
+        double c = u[(size_t)j].weight;
+        if (j < m) {
+          const double a = u[(size_t)j].weight, b = u[(size_t)(first + j)].weight;
+          c = kPairCost * std::min(a, b) + (std::max(a, b) - std::min(a, b));
+        }
+        t = std::max(t, c);
+      }
+      return t;
+    };
+    std::vector<AttnUnit> rot = info->units;
+    std::rotate(rot.begin(), rot.begin() + (first - m), rot.begin() + first);
+    if (longest(rot) < longest(info->units)) info->units.swap(rot);
+  }
   info->slots = slot;
   info->counters = counter;
   return EA_OK;
