@@ -1207,9 +1207,9 @@ int attention_units(const ea_relation* Q, const std::vector<int32_t>& goff, Attn
                    [](const AttnUnit& a, const AttnUnit& b) { return a.weight > b.weight; });
   // Between one and two units per CU: the first 256 workgroups take a CU
   // each, and workgroup 256 + j shares the CU of workgroup j (same XCD, the
-  // dispatch's next round).  A unit that shares its CU runs its key blocks
+  // dispatch's second pass).  A unit that shares its CU runs its key blocks
   // slower (kPairCost, against 1 alone) until its partner ends.  The lightest
-  // units are already last; moving the lightest of the first round to the
+  // units are already last; moving the lightest of the first pass to the
   // front gives them, rather than the heaviest, a partner.  The order with the
   // shorter estimated longest CU is kept.
   const int64_t n_units = (int64_t)info->units.size(), first = kCUs / 2;
