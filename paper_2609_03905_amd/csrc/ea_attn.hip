@@ -265,7 +265,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
   // softmax step, O^T += V^T P^T.  DIAG: some key of the chunk is past some
   // query of the wave, so the causal mask is applied (a separate
   // instantiation: the other chunks carry no mask arithmetic at all).
-  auto compute_chunk_impl = [&](int b, auto diag_tag, auto&& mid, auto&& load) {
+  auto compute_chunk_impl = [&](int b, auto diag_tag, auto&& load) {
     constexpr bool DIAG = decltype(diag_tag)::value;
     const uint16_t* sK = sKV + b * BUF;
     const uint16_t* sV = sK + KC * D;
@@ -289,7 +289,6 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
       for (int kt = 0; kt < KT; ++kt) acc_s[kt] = mfma_bf16(a[kt], qreg[s], acc_s[kt]);
     }
     __builtin_amdgcn_s_setprio(0);
-    mid();  // issued while the score MFMAs run
     // online softmax in the log2 domain; the scale is one FMA ahead of exp2
     float mx = -INFINITY;
 #pragma unroll
@@ -355,25 +354,23 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
       }
     __builtin_amdgcn_s_setprio(0);
   };
-  auto compute_chunk = [&](int b, auto&& mid, auto&& load) {
+  auto compute_chunk = [&](int b, auto&& load) {
     const int key0 = key0_buf[b];
     if (causal && key0 > qpos_wave_max) {  // the whole wave is masked in this chunk
 #pragma unroll
       for (int q = 0; q < 2 * LPW; ++q) load(q);
-      mid();
     } else if (causal && key0 + KC - 1 > qpos_wave_min) {
-      compute_chunk_impl(b, Bool<true>{}, mid, load);
+      compute_chunk_impl(b, Bool<true>{}, load);
     } else {
-      compute_chunk_impl(b, Bool<false>{}, mid, load);
+      compute_chunk_impl(b, Bool<false>{}, load);
     }
   };
 
   // The walk: chunk j is computed from buffer j % 2 while every wave issues
   // its loads of chunk j + 1 into the other buffer (which all waves finished
   // with before the previous barrier); then each wave waits for its own
-  // loads and the workgroup meets at the barrier.  A chunk's V pieces are
-  // turned to fp16 by the waves that loaded them once the chunk's score
-  // MFMAs are issued, and the workgroup meets again before its PV product.
+  // loads, turns the V pieces it loaded to fp16 in place, and the workgroup
+  // meets at the barrier (one per chunk).
   // The loop runs two chunks per iteration so that every buffer index is a
   // compile-time constant.  (Earlier designs measured: eight
   // waves in two groups computing alternate chunks of one tile, with four
@@ -387,6 +384,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
     asm volatile("" ::: "memory");
   };
   wait_loads();
+  if (nc > 0) convert_v(0);
   __syncthreads();
   for (int j0 = 0; j0 < nc; j0 += NBUF) {
 #pragma unroll
@@ -394,23 +392,20 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
       const int j = j0 + e;
       if (j < nc) {
         // the next chunk's loads go out one per score step, so that a wave
-        // held by the load path waits under its own running MFMAs; once
-        // the scores are issued, this wave's V pieces of this chunk are
-        // turned to fp16 and the workgroup meets before the PV product
-        // reads them
+        // held by the load path waits under its own running MFMAs; after
+        // its PV MFMAs are issued, each wave waits for its own loads and
+        // turns its V pieces of the next chunk to fp16 while they run, and
+        // the workgroup meets once per chunk
         const char *kb = nullptr, *vb = nullptr;
         const bool more = j + 1 < nc;
         if (more) next_chunk(1 - e, kb, vb);
-        compute_chunk(
-            e,
-            [&]() {
-              convert_v(e);
-              __syncthreads();
-            },
-            [&](int q) {
-              if (more) issue_piece(1 - e, q, kb, vb);
-            });
-        if (j + 1 < nc) wait_loads();
+        compute_chunk(e, [&](int q) {
+          if (more) issue_piece(1 - e, q, kb, vb);
+        });
+        if (more) {
+          wait_loads();
+          convert_v(1 - e);
+        }
         __syncthreads();
       }
     }
