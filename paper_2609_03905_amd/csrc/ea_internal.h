@@ -172,7 +172,7 @@ struct GemmSeg {
   int32_t part, n_parts;  // place among the tile's segments (ascending s0); n_parts 1: not split
   int32_t first_slot;     // split tile: part i's partial sums go to workspace slot first_slot + i
   int32_t counter;        // split tile: its arrival counter
-  // resolved from the GPU join at plan time (gemm_prep_kernel): the group's
+  // resolved from the GPU join at plan time (launch_gemm_prep): the group's
   // first tuple and tuple count, the tuple holding step s0 and the steps of
   // it before s0, and the segment's step count (s1 clamped to the group's)
   int32_t gb, nt, t0, skip, n_steps;
