@@ -120,3 +120,30 @@ def test_narrow_tiles_with_residual_match_the_oracle():
     Y = _run("even", "tj,jk->tk", ea.JOIN_MUL, [A, W], (T, K), py, "bf16", tile_n=128, residual=R)
     ref = oracle.matmul(synth.to_f64(a, "bf16"), synth.to_f64(w, "bf16")) + synth.to_f64(r, "bf16")
     assert_close(synth.to_f64(download(Y), "bf16"), expected(ref, "bf16"), what="narrow tiles + residual")
+
+
+def _uneven_splits(n_blocks):
+    # contracted block widths cycling 32, 64, 96, 32 (multiples of the
+    # direct-load kernel's 32-deep K step)
+    widths = [(32, 64, 96, 32)[i % 4] for i in range(n_blocks)]
+    return [0] + list(np.cumsum(widths))
+
+
+@pytest.mark.parametrize("schedule", ["even", "balanced"])
+@pytest.mark.parametrize("n_blocks", [128, 129])
+def test_most_tuples_per_key_and_uneven_k_blocks(schedule, n_blocks):
+    # 128 contracted blocks per output key is the most the direct-load
+    # kernel's tuple table holds (129 take the register-staged kernel); the
+    # uneven widths make runs start inside a tuple.  Integer data: exact in
+    # any summation order, so the bits equal the oracle's
+    print(f"most tuples per key, {n_blocks} blocks, {schedule}", flush=True)
+    pj = _uneven_splits(n_blocks)
+    T, J, K = 512, int(pj[-1]), 256
+    x = synth.integers((T, J), 995, -2, 3, dtype="bf16")
+    w = synth.integers((J, K), 996, -2, 3, dtype="bf16")
+    X = upload(x, "bf16", [synth.splits(T, 256), pj])
+    W = upload(w, "bf16", [pj, [0, K]])
+    py = [synth.splits(T, 256), [0, K]]
+    Y = _run(schedule, "tj,jk->tk", ea.JOIN_MUL, [X, W], (T, K), py, "f32")
+    exact = synth.to_f64(x, "bf16") @ synth.to_f64(w, "bf16")
+    np.testing.assert_array_equal(download(Y), exact)
