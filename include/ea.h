@@ -31,7 +31,9 @@
  * device tables (block tables, the GPU-built tuple table, the kernel's work
  * list).  Plans are built only by the planning calls ea_joinagg_workspace,
  * ea_repartition_plan and ea_join_tuples: they allocate the plan's device
- * memory, run the GPU join enumerator on the given stream and wait for it.
+ * memory, run the GPU join enumerator on the given stream (for block GEMMs and
+ * attention, then a kernel that resolves the join into the work list) and
+ * wait for it.
  * ea_joinagg and ea_repartition never allocate and never synchronize: they
  * find the plan (EA_ERR_NOPLAN if none was built on the current device) and
  * enqueue kernels.  A plan is immutable once built, so calls that share one
