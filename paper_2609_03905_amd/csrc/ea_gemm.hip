@@ -230,7 +230,9 @@ __device__ __forceinline__ void epilogue(const f32x16_t (&acc)[NB][4][WN], const
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float v = acc[0][i][j][r];
-        if constexpr (SWIGLU) v = v / (1.0f + __expf(-v)) * acc[NB - 1][i][j][r];
+        // silu(g) * u: the reciprocal (about 1 ulp) in place of a correctly
+        // rounded division, far below the output's bf16 rounding
+        if constexpr (SWIGLU) v = v * __builtin_amdgcn_rcpf(1.0f + __expf(-v)) * acc[NB - 1][i][j][r];
         const int row = wm * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
         stage[row * kEpiPitch + wn * WCOLS + 32 * j + lq] = v;
       }
