@@ -1795,6 +1795,7 @@ int run_planned(const Plan* plan, int32_t join_op, int32_t n_in, const ea_relati
       a.row_len = plan->rows.row_len;
       a.vec = plan->rows.vec;
       a.seg_chunks = plan->rows.cps;
+      a.seg_inv = a.seg_chunks > 0 ? 1.0f / (float)a.seg_chunks : 0.0f;
       a.affine = plan->rows.affine;
       a.stream_out = params ? params->store : 0;
       a.seg_len = plan->rows.seg_len;

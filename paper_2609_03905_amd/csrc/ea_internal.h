@@ -291,6 +291,7 @@ struct RowArgs {
   int32_t vec;           // 1: register path (see rows_vec_ok)
   int32_t seg_chunks;    // register path: 16-byte chunks of every segment but the
                          // last (which has at most as many), or 0 if uneven
+  float seg_inv;         // 1 / seg_chunks (fp32), or 0
   float eps;
   // Affine layout (set on the host when it holds): every segment has seg_len
   // elements, x, y and w have the same partition of the normalised letter,
