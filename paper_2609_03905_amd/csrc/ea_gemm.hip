@@ -283,12 +283,21 @@ struct KStep {
   int t, k0;
 };
 
-// Split output keys: every unit writes its partial sums, the last unit of
-// the key (device-scope arrival counter, no waiting) adds the partials in a
-// fixed order -- part order, or for two parts its own plus the other's,
-// which is the same sum -- so results are deterministic, and stores.
+// Split output keys of three or more parts: every unit writes its partial
+// sums, and the last unit of the key to arrive (device-scope arrival counter)
+// adds the partials in part order from zero and stores.
+// Two parts: the first to arrive writes its partial and marks it written;
+// the second keeps its own in registers, waits for that mark and merges, so
+// one partial per tile is written instead of two.  The second arriver waits
+// only for a workgroup that has already arrived, i.e. is running and only
+// storing, so the wait ends within that store's time (a few us); the 100 ms
+// guard could only be reached by a writer descheduled for that long.  Its
+// sum, own + other, equals other + own exactly, so the result does not depend
+// on which part arrived first.
 // Partials are laid out in accumulator order (lane-contiguous float4s).
 // Then the epilogue, with dtype and residual decided outside its unrolled loops.
+constexpr int32_t kWritten = 1 << 16;         // added by the first of two parts once its partial is stored
+constexpr uint64_t kWrittenWaitTicks = 10000000;  // guard on the second's wait: 100 ms of the 100 MHz clock
 template <bool SWIGLU, int NB, int WN, int W>
 __device__ __forceinline__ void finish_tile(f32x16_t (&acc)[NB][4][WN], const GemmArgs& p, const GemmTile& tile,
                                             int wid, int lane, float* stage) {
@@ -310,7 +319,17 @@ __device__ __forceinline__ void finish_tile(f32x16_t (&acc)[NB][4][WN], const Ge
       const int q = ((o * 4 + i) * WN + j) * 4 + r4;
       return (uint32_t)(wid * WAVE_BYTES + (q * 64 + lane) * 16);
     };
-    {
+    int32_t* const counter = p.counters + tile.counter;
+    // two parts: arrivals in the low bits; the second sees 1, or
+    // 1 + kWritten when the first has already stored its partial
+    const bool two_parts = tile.n_parts == 2;
+    bool write = true;
+    if (two_parts) {
+      if (tid == 0) s_last = (arrive_agent(counter) & (kWritten - 1)) == 1;
+      __syncthreads();
+      write = !s_last;
+    }
+    if (write) {
       const auto rs = slot_rsrc(tile.slot);
 #pragma unroll
       for (int o = 0; o < NB; ++o)
@@ -325,10 +344,21 @@ __device__ __forceinline__ void finish_tile(f32x16_t (&acc)[NB][4][WN], const Ge
                                  __float_as_uint(c[4 * r4 + 2]), __float_as_uint(c[4 * r4 + 3])};
               __builtin_amdgcn_raw_buffer_store_b128(v, rs, piece(o, i, j, r4), 0, kCoherent);
             }
+      drain_vmem();
     }
-    drain_vmem();
     __syncthreads();
-    if (tid == 0) s_last = arrive_agent(p.counters + tile.counter) == tile.n_parts - 1;
+    if (tid == 0) {
+      if (!two_parts) {
+        s_last = arrive_agent(counter) == tile.n_parts - 1;
+      } else if (write) {
+        __hip_atomic_fetch_add(counter, kWritten, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      } else {  // the first arriver is storing: wait for its mark
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        while (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < kWritten &&
+               __builtin_amdgcn_s_memrealtime() - t0 < kWrittenWaitTicks)
+          __builtin_amdgcn_s_sleep(2);
+      }
+    }
     __syncthreads();
     if (!s_last) return;
     // add one slot's partials: 16 loads in flight per batch (latency hidden,
@@ -376,7 +406,7 @@ __device__ __forceinline__ void finish_tile(f32x16_t (&acc)[NB][4][WN], const Ge
     }
     const int n_add = two ? 1 : tile.n_parts;
     for (int k = 0; k < n_add; ++k) add_slot(two ? other : tile.first_slot + k);
-    if (tid == 0) reset_agent(p.counters + tile.counter);  // ready for the next call (stream-ordered)
+    if (tid == 0) reset_agent(counter);  // ready for the next call (stream-ordered)
   }
   const DevBlk& cb = p.blk_c[tile.block];
   const EpiArgs e{p.c + cb.off, p.res ? p.res + cb.off : nullptr, cb.ext[0], cb.ext[1], tile.m0, tile.n0};
