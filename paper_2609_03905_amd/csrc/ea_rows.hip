@@ -25,6 +25,8 @@ constexpr int kThreads = 64 * kRowsPerTask;  // one row per wavefront
 constexpr int kMaxSeg = 64;    // segments per row on the register path
 constexpr int kMaxK = 16;      // 16-byte chunks per lane on the register path
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
 struct SegTable {
   int32_t start[kMaxSeg];  // first chunk of the segment within the row
   int64_t xoff[kMaxSeg];   // byte offset of the row's segment in x
@@ -312,6 +314,23 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
   } else {
   // local partials, then the aggregation across lanes
   float part = SOFTMAX ? -INFINITY : 0.0f;
+  if constexpr (!SOFTMAX && ES == 2) {
+    // bf16 sum of squares straight from the packed pairs: one v_dot2c_f32_bf16
+    // per two elements (the bf16 products are exact in fp32), in four
+    // running sums, one per 4-byte word of the chunk
+    float p4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (!vis[k]) continue;
+      const uint32_t w[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bf16x2_t h = __builtin_bit_cast(bf16x2_t, w[i]);
+        p4[i] = __builtin_amdgcn_fdot2_f32_bf16(h, h, p4[i], false);
+      }
+    }
+    part = (p4[0] + p4[1]) + (p4[2] + p4[3]);
+  } else {
 #pragma unroll
   for (int k = 0; k < K; ++k) {
     if (!vis[k]) continue;
@@ -327,6 +346,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
         part += f[i] * f[i];
       }
     }
+  }
   }
   if constexpr (SOFTMAX) {
     m = wave_max(part);
