@@ -225,7 +225,8 @@ int ea_relation_block(const ea_relation* rel, int64_t b, int64_t* lo, int64_t* h
      same extent; bf16 data.  Scores and softmax in f32; for the P.V product
      P (in [0, 2^8]: the running max may lag the true one by up to 8 in
      the log2 domain) is rounded to fp16 and V is converted to fp16, so V
-     values must lie within the fp16 range; fp32 accumulation.
+     values must lie within the fp16 range; fp32 accumulation.  The
+     softmax denominator sums the same fp16 P values.
    EA_OP_SWIGLU, agg SUM: in = (X "tj", W1 "jk", W2 "jk"), out "tk" =
      silu(X W1) * (X W2), silu(g) = g / (1 + e^-g); bf16 data.
    Errors: EA_ERR_ARG, EA_ERR_SPEC, EA_ERR_DTYPE, EA_ERR_JOIN,

@@ -30,7 +30,8 @@
 //   * the scale (log2 domain) is one FMA ahead of exp2; the causal mask is
 //     applied only on chunks that reach past a query of the wave;
 //   * P = 2^(S - m), in [0, 2^8] (m lags the true max by at most 8), is
-//     rounded to fp16 and O^T += V^T P^T runs on fp16 MFMA 32x32x16; the V^T
+//     rounded to fp16; the row sum adds those fp16 values (v_dot2_f32_f16)
+//     and O^T += V^T P^T runs on fp16 MFMA 32x32x16; the V^T
 //     operand (8 keys of one d per lane) comes from two transposing LDS reads
 //     (ds_read_b64_tr_b16) of the [key][d] chunk, with the MFMA's k order
 //     matched to the accumulator layout of S^T.
@@ -75,6 +76,12 @@ __device__ __forceinline__ f32x16_t mfma_bf16(const uint4& a, const uint4& b, co
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 
+
+// acc + x.lo + x.hi for a packed fp16 pair x (v_dot2_f32_f16 against 1, 1)
+__device__ __forceinline__ float sum_f16x2(uint32_t x, float acc) {
+  const f16x2_t one = {(_Float16)1.0f, (_Float16)1.0f};
+  return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2_t, x), one, acc, false);
+}
 
 // two floats -> packed fp16 pair, round to nearest even (v_cvt_pk_f16_f32)
 __device__ __forceinline__ uint32_t pack_f16(float x0, float x1) {
@@ -311,16 +318,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
     const float cand = mx * sc;
     const float m_new = cand > m + kLazyMax ? cand : m;
     const float m_use = m_new == -INFINITY ? 0.0f : m_new;
-    float rs = 0.0f;
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float pv = fast_exp2(fmaf(acc_s[kt][r], sc, -m_use));
-        acc_s[kt][r] = pv;
-        rs += pv;
-      }
-    rs += other32(rs);
+      for (int r = 0; r < 16; ++r) acc_s[kt][r] = fast_exp2(fmaf(acc_s[kt][r], sc, -m_use));
     if (__any(m_new != m)) {  // a running max moved: rescale (else alpha is 1 on every lane)
       const float alpha = fast_exp2(m - m_use);
       l *= alpha;
@@ -329,7 +330,6 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc_o[dt][r] *= alpha;
     }
-    l += rs;
     m = m_new;
     // MFMA k index 8 g + e maps to key 32 kt + 16 h + 4 g + e (e < 4) or
     // 32 kt + 16 h + 8 + 4 g + (e - 4); P in fp16 (RNE), V in fp16
@@ -343,6 +343,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
                                     pack_f16(acc_s[kt][8 * h + 2], acc_s[kt][8 * h + 3]),
                                     pack_f16(acc_s[kt][8 * h + 4], acc_s[kt][8 * h + 5]),
                                     pack_f16(acc_s[kt][8 * h + 6], acc_s[kt][8 * h + 7]));
+        // the row sum takes the same fp16 P as the PV product, two terms per
+        // v_dot2_f32_f16 (this lane's half of the row: the pair's halves
+        // are added once after the walk, as both share every running max)
+        l = sum_f16x2(ph.x, l);
+        l = sum_f16x2(ph.y, l);
+        l = sum_f16x2(ph.z, l);
+        l = sum_f16x2(ph.w, l);
         const int k0 = 32 * kt + 16 * h + 4 * (gq >> 1) + (li >> 2);  // key row of this lane's first read
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
@@ -410,6 +417,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
       }
     }
   }
+
+  l += other32(l);  // the row's two halves (lanes l and l^32)
 
   // ---- split group: write this unit's partial (m, l, O), the last unit of
   // the (group, tile) merges in registers.  Partials go through the plan's
