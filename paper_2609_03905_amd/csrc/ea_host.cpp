@@ -913,12 +913,17 @@ GemmPlanInfo gemm_units(const ea_relation* a, const ea_relation* c, int tn, doub
 //     and start the next, and a tile cut into several runs is merged by its
 //     last arriver.  This fills every CU when there are fewer tiles than CUs.
 // Time model (us): 0.75 per K step of a tile, 1 per segment (pipeline fill and
-// store), and the split tiles' partial sums written and read back at 5 TB/s.
+// store), and the split tiles' partial sums written and read back at an
+// effective 8 TB/s: two-part tiles move two partials (the first arriver's
+// write, the second's read), more parts every part's write and a read of
+// each.  The rate is above HBM's because those exchanges partly overlap
+// other workgroups' K steps; it is fitted to the block share, where balanced
+// SwiGLU (176 tiles, 176 steps per run, almost every tile in two or three
+// runs) measured 188 us against 191-194 us even, and balanced QKV 125 us
+// against 109-112 us even.
 // The step time grows once more than about 190 CUs run matrix work at once:
 // the sustained clock is power-limited, so a schedule that keeps all 256 CUs
-// busy gains less than its CU count suggests (measured on the block share:
-// 176 tiles of SwiGLU over 256 steps each took 195 us on 176 CUs, and the same
-// work balanced over 256 CUs, 176 steps each, 193 us).
+// busy gains less than its CU count suggests.
 struct GemmDlPlan {
   std::vector<GemmUnit> units;
   int32_t slots = 0, counters = 0;
@@ -929,7 +934,7 @@ struct GemmDlPlan {
 GemmDlPlan gemm_units_dl(const ea_relation* a, const ea_relation* c, int tn, const GemmPlanInfo& even,
                          double step_scale = 1.0) {
   const int kCUs = 256;
-  const double t_step = 0.75 * step_scale, t_seg = 1.0, bw = 5.0e6, tile_bytes = (double)kGemmTM * tn * 4,
+  const double t_step = 0.75 * step_scale, t_seg = 1.0, bw = 8.0e6, tile_bytes = (double)kGemmTM * tn * 4,
                n_sat = 190.0;
   auto step_time = [&](int64_t busy_cus) { return t_step * std::max(1.0, (double)busy_cus / n_sat); };
   // K-step prefix over a group's tuples (A's contracted blocks, in order)
@@ -937,7 +942,7 @@ GemmDlPlan gemm_units_dl(const ea_relation* a, const ea_relation* c, int tn, con
   std::vector<int32_t> pre(n_t + 1, 0);
   for (int b = 0; b < n_t; ++b) pre[b + 1] = pre[b] + (int32_t)((a->splits[1][b + 1] - a->splits[1][b]) / 32);
   const int64_t S = pre[n_t];
-  auto merge_bytes = [&](int parts) { return parts > 1 ? (parts + (parts == 2 ? 1 : parts)) * tile_bytes : 0.0; };
+  auto merge_bytes = [&](int parts) { return parts > 1 ? (parts == 2 ? 2 : 2 * parts) * tile_bytes : 0.0; };
   // even schedule, as one-segment units
   GemmDlPlan ev;
   double ev_cost = 0.0;
