@@ -155,6 +155,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
   const int nc = ld_uniform(&um.nc);  // chunks of the walk, up to the first past the tile's last query
   const int q_lo = ld_uniform(&um.q_lo);
   const int64_t qoff = ld_uniform(&um.qoff), ooff = ld_uniform(&um.ooff);
+  // the first tuple's K/V record, read with the fields above (one round trip
+  // of scalar loads, not two): kv[0] is part of every unit's record, and is
+  // used only when the walk has a chunk
+  const int64_t ko0 = ld_uniform(&um.kv[0].koff), vo0 = ld_uniform(&um.kv[0].voff);
+  const int klo0 = ld_uniform(&um.kv[0].klo), kext0 = ld_uniform(&um.kv[0].kext);
+  // an empty statement that takes the four values keeps the compiler from
+  // sinking their loads into the branch below, behind a wait of their own
+  asm volatile("" ::"s"(ko0), "s"(vo0), "s"(klo0), "s"(kext0));
   const int row = u.q0 + wq * 32 + lq;  // this lane's query row inside the block
   const int qpos = q_lo + row;          // its position
   const int qpos_wave_min = q_lo + u.q0 + wq * 32;
@@ -209,17 +217,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
 
   // The first chunk goes out first, its addresses taken from the record by
   // scalar loads (before the metadata table reaches LDS, and before Q).
-#pragma unroll
-  for (int j = 0; j < 1; ++j)
-    if (j < nc) {
-      const AttnKv* kvp = &um.kv[it_t];  // it_t < nt whenever j < nc
-      const int64_t ko = ld_uniform(&kvp->koff), vo = ld_uniform(&kvp->voff);
-      const int klo = ld_uniform(&kvp->klo), kext = ld_uniform(&kvp->kext);
-      key0_buf[j] = klo + it_c;
-      issue_k(j, p.k + ko + (int64_t)it_c * D * 2);
-      issue_v(j, p.v + vo + (int64_t)it_c * D * 2);
-      advance(kext);
-    }
+  if (nc > 0) {
+    key0_buf[0] = klo0;
+    issue_k(0, p.k + ko0);
+    issue_v(0, p.v + vo0);
+    advance(kext0);
+  }
 
   // the unit's tuples' K/V metadata (nt <= kAttnMaxUnitTuples: host guarantee)
   AttnKv kv{};
