@@ -153,6 +153,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
   const AttnUnitMeta& um = p.meta[blockIdx.x];
   const int nt = ld_uniform(&um.nt);
   const int nc = ld_uniform(&um.nc);  // chunks of the walk, up to the first past the tile's last query
+  // leading chunks that no query of the tile masks, rounded down to even so
+  // that the rest of the walk starts on buffer 0
+  const int n_plain = ld_uniform(&um.n_plain) & ~1;
   const int q_lo = ld_uniform(&um.q_lo);
   const int64_t qoff = ld_uniform(&um.qoff), ooff = ld_uniform(&um.ooff);
   // the first tuple's K/V record, read with the fields above (one round trip
@@ -396,7 +399,29 @@ __global__ __launch_bounds__(kThreads, 2) void attn_kernel(const AttnArgs p) {
   wait_loads();
   if (nc > 0) convert_v(0);
   __syncthreads();
-  for (int j0 = 0; j0 < nc; j0 += NBUF) {
+  // Chunks that no query of the tile masks run in a loop of their own with
+  // the unmasked chunk code alone: with one path through the loop, O keeps
+  // its registers from one chunk to the next (where the masked, unmasked
+  // and fully masked paths meet, the compiler moves all of O between
+  // register sets after each chunk's last MFMA).
+  for (int j0 = 0; j0 < n_plain; j0 += NBUF) {
+#pragma unroll
+    for (int e = 0; e < NBUF; ++e) {
+      const int j = j0 + e;  // < n_plain (even)
+      const char *kb = nullptr, *vb = nullptr;
+      const bool more = j + 1 < nc;
+      if (more) next_chunk(1 - e, kb, vb);
+      compute_chunk_impl(e, Bool<false>{}, [&](int q) {
+        if (more) issue_piece(1 - e, q, kb, vb);
+      });
+      if (more) {
+        wait_loads();
+        convert_v(1 - e);
+      }
+      __syncthreads();
+    }
+  }
+  for (int j0 = n_plain; j0 < nc; j0 += NBUF) {
 #pragma unroll
     for (int e = 0; e < NBUF; ++e) {
       const int j = j0 + e;
@@ -593,14 +618,20 @@ __global__ __launch_bounds__(64) void attn_prep_kernel(const AttnArgs p) {
     // the walk's chunks: every kAttnChunkKeys keys of the unit's blocks, in
     // tuple order, up to the first chunk past the tile's last query (later
     // ones are masked for every row under the causal predicate)
-    const int qpos_tile_max = qb.lo[p.q_dim] + u.q0 + kAttnTileRows - 1;
-    int nc = 0;
+    const int qpos_tile_min = qb.lo[p.q_dim] + u.q0, qpos_tile_max = qpos_tile_min + kAttnTileRows - 1;
+    int nc = 0, n_plain = 0;
+    bool plain = true;  // every chunk so far lies wholly before the tile's first query
     for (int t = 0; t < nt; ++t) {
       const DevBlk& kb = p.blk_k[p.tuples[(int64_t)(tb + t) * 4 + 2]];
       const int klo = kb.lo[p.k_dim], kext = kb.ext[p.k_dim];
-      for (int c0 = 0; c0 < kext && !(p.causal && klo + c0 > qpos_tile_max); c0 += kAttnChunkKeys) ++nc;
+      for (int c0 = 0; c0 < kext && !(p.causal && klo + c0 > qpos_tile_max); c0 += kAttnChunkKeys) {
+        ++nc;
+        plain = plain && !(p.causal && klo + c0 + kAttnChunkKeys - 1 > qpos_tile_min);
+        n_plain += plain;
+      }
     }
     um.nc = nc;
+    um.n_plain = n_plain;
   }
   for (int t = lane; t < te - tb && t < kAttnMaxUnitTuples; t += 64) {
     const int32_t* tp = p.tuples + (int64_t)(tb + t) * 4;

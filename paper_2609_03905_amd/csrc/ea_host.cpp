@@ -1412,6 +1412,7 @@ int get_joinagg_plan(const char* spec_str, const Spec& sp, int32_t join_op, int3
     a.n_units = (int32_t)p->n_work;
     a.q_dim = oi.q_dim;
     a.k_dim = oi.k_dim;
+    a.causal = oi.causal;  // the walk's causal cut and its unmasked leading chunks (a plan holds one rule)
     a.meta = p->attn_meta;
     a.overflow = (int32_t*)(p->dmem2 + foff);
     EA_HIP_TRY(launch_attention_prep(a, s));

@@ -343,7 +343,7 @@ struct AttnUnitMeta {
   int64_t qoff, ooff;  // byte offsets of the unit's Q and O blocks
   int32_t q_lo, nt;    // query position of the Q block's first row; the unit's tuples
   int32_t nc;          // kAttnChunkKeys-key chunks of the unit's walk (causal cut applied)
-  int32_t pad;
+  int32_t n_plain;     // leading chunks of the walk that the causal rule masks for no query of the tile
   AttnKv kv[kAttnMaxUnitTuples];
 };
 
