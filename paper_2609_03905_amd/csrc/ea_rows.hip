@@ -122,16 +122,23 @@ __device__ __forceinline__ void unpack<float>(const uint4& v, float (&f)[8]) {
 // AFF: affine layout (RowArgs::affine): addresses come from the task record
 // and the strides, so the row loads go out at once; otherwise each wave
 // first builds its row's segment table from the join's tuples.
-template <typename XT, bool SOFTMAX, int K, bool AFF>
-__global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
+// WPR: wavefronts per row.  2 halves the registers and the serial work of a
+// long row (RMSNorm on the affine layout with bf16 weights only): each wave
+// takes K chunks of its half, and the two partial sums of squares meet in LDS.
+template <typename XT, bool SOFTMAX, int K, bool AFF, int WPR = 1>
+__global__ __launch_bounds__(kThreads * WPR) void rows_vec_kernel(RowArgs a) {
+  static_assert(WPR == 1 || (WPR == 2 && !SOFTMAX && AFF && sizeof(XT) == 2), "split rows: bf16 RMSNorm, affine");
   __shared__ SegTable tabs[AFF ? 1 : kThreads / 64];
+  __shared__ float s_half[WPR == 2 ? kRowsPerTask * 2 : 1];
   // RMSNorm: the weights of the group's row, in the row's chunk order as
   // fp32 (EPC values per chunk), staged once for the workgroup's rows
   constexpr int ES = sizeof(XT), EPC = 16 / ES;
-  __shared__ float sw[SOFTMAX ? 1 : K * 64 * EPC];
+  __shared__ float sw[SOFTMAX ? 1 : K * WPR * 64 * EPC];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int wrow = wid / WPR;                   // the wave's row of the task
+  const int cbase = (wid % WPR) * K * 64;       // first chunk of the wave's part of the row
   const RowTask& task = a.tasks[blockIdx.x];
-  const bool active = wid < ld_uniform(&task.nrows);  // waves past the task's rows only help stage the weights
+  const bool active = wrow < ld_uniform(&task.nrows);  // waves past the task's rows only help stage the weights
   const int esy = a.dt_y == EA_F32 ? 4 : 2;
   SegTable& st = tabs[AFF ? 0 : wid];
   int total, nseg;
@@ -141,9 +148,9 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
   if constexpr (AFF) {
     nseg = a.nseg;
     total = nseg * a.seg_chunks;
-    const int row = ld_uniform(&task.row0) + wid;
-    xrow = ld_uniform(&task.xrow) + (int64_t)wid * a.seg_len * ES;
-    yrow = ld_uniform(&task.yrow) + (int64_t)wid * a.seg_len * esy;
+    const int row = ld_uniform(&task.row0) + wrow;
+    xrow = ld_uniform(&task.xrow) + (int64_t)wrow * a.seg_len * ES;
+    yrow = ld_uniform(&task.yrow) + (int64_t)wrow * a.seg_len * esy;
     if (SOFTMAX && a.causal) qpos = ld_uniform(&task.qlo) + row % ld_uniform(&task.qext);
   } else {
     ri = row_info(a, wid);  // every row of the task is in the same group
@@ -185,7 +192,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
   bool vis[K];
 #pragma unroll
   for (int k = 0; k < K; ++k) {
-    const int c = k * 64 + lane;
+    const int c = cbase + k * 64 + lane;
     vis[k] = false;
     seg[k] = 0;
     e0s[k] = 0;
@@ -208,7 +215,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
         constexpr bool STREAM = decltype(stream_tag)::value;
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-          const int c = k * 64 + lane;
+          const int c = cbase + k * 64 + lane;
           if (c >= total || vis[k]) continue;
           char* yp = y_at(seg[k], e0s[k]);  // the chunk's EPC outputs, stored as write_row stores them
           if ((a.dt_y == EA_BF16 && ES == 2) || (a.dt_y == EA_F32 && ES == 4)) {
@@ -233,7 +240,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     if (a.dt_w == EA_BF16) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        const int c = k * 64 + lane;
+        const int c = cbase + k * 64 + lane;
         wv[k] = make_uint4(0, 0, 0, 0);
         if (c < total && active) wv[k] = *reinterpret_cast<const uint4*>(w_at(seg[k]) + (int64_t)e0s[k] * 2);
       }
@@ -263,7 +270,7 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     }
     __syncthreads();
   }
-  if (!active) return;
+  if (WPR == 1 && !active) return;  // (split rows: every wave meets the barrier below)
   float scale = 0.0f, m = 0.0f;
   // softmax rows of at most 4 chunks per lane keep their exponentials from
   // the sum for the output, instead of computing them a second time
@@ -366,17 +373,23 @@ __global__ __launch_bounds__(kThreads) void rows_vec_kernel(RowArgs a) {
     l = wave_sum(l);
     scale = m == -INFINITY ? 0.0f : 1.0f / l;
   } else {
-    const float ss = wave_sum(part);
+    float ss = wave_sum(part);
+    if constexpr (WPR == 2) {  // the row's two halves, first half first
+      if (lane == 0) s_half[wid] = ss;
+      __syncthreads();
+      ss = s_half[2 * wrow] + s_half[2 * wrow + 1];
+    }
     scale = 1.0f / sqrtf(ss / (float)a.row_len + a.eps);
   }
   }
+  if (WPR == 2 && !active) return;  // after the barrier: a wave past the task's rows writes nothing
   // write the row, under the output store policy (one branch around the
   // whole loop, see store_out)
   auto write_row = [&](auto stream_tag) {
     constexpr bool STREAM = decltype(stream_tag)::value;
 #pragma unroll
     for (int k = 0; k < K; ++k) {
-      const int c = k * 64 + lane;
+      const int c = cbase + k * 64 + lane;
       if (c >= total) continue;
       if (SOFTMAX && a.causal && !vis[k]) continue;  // stored as zeros above
       const int sg = seg[k];
@@ -474,8 +487,20 @@ void launch_vec(const RowArgs& a, dim3 grid, dim3 block, hipStream_t s) {
   else hipLaunchKernelGGL((rows_vec_kernel<XT, SOFTMAX, K, false>), grid, block, 0, s, a);
 }
 
+// bf16 RMSNorm rows of 8K+ bf16 chunks on the affine layout with bf16
+// weights: two wavefronts per row (kMaxK / 2 chunks per lane each)
+bool split_rows(const RowArgs& a, int64_t chunks, bool softmax) {
+  return !softmax && a.affine && a.dt_x == EA_BF16 && a.dt_w == EA_BF16 && chunks > (kMaxK / 2) * 64;
+}
+
 template <typename XT, bool SOFTMAX>
 void launch_vec_k(const RowArgs& a, int64_t chunks, dim3 grid, dim3 block, hipStream_t s) {
+  if constexpr (!SOFTMAX && sizeof(XT) == 2) {
+    if (split_rows(a, chunks, SOFTMAX)) {
+      hipLaunchKernelGGL((rows_vec_kernel<XT, false, kMaxK / 2, true, 2>), grid, dim3(block.x * 2), 0, s, a);
+      return;
+    }
+  }
   if (chunks <= 4 * 64) launch_vec<XT, SOFTMAX, 4>(a, grid, block, s);
   else if (chunks <= 8 * 64) launch_vec<XT, SOFTMAX, 8>(a, grid, block, s);
   else launch_vec<XT, SOFTMAX, kMaxK>(a, grid, block, s);
