@@ -345,6 +345,24 @@ def test_rmsnorm_vector_path_short_last_segment():
     assert_close(values(Y), expected(ref, "bf16"), what="rmsnorm short last segment")
 
 
+def test_rmsnorm_two_wavefronts_per_row_partial_task():
+    # 8192-element bf16 rows in the block share's 512-blocks with bf16
+    # weights: each row on two wavefronts; 1027 rows leave a last row block of
+    # three rows, so its task has a wavefront pair with no row (it must meet
+    # the halves' barrier and write nothing)
+    T, C = 1027, 8192
+    pt, pc = synth.splits(T, 512), synth.splits(C, 512)
+    x = synth.normal((T, C), 67, dtype="bf16")
+    wv = synth.uniform((C,), 68, 0.5, 1.5, dtype="bf16")
+    X, Wt = upload(x, "bf16", [pt, pc]), upload(wv, "bf16", [pc])
+    Y = empty((T, C), "bf16", [pt, pc])
+    ea.joinagg("tc,c->tc", ea.OP_RMSNORM, ea.AGG_SUM, [X, Wt], Y, eps=1e-5)
+    ref = oracle.rmsnorm(synth.to_f64(x, "bf16"), synth.to_f64(wv, "bf16"), 1e-5)
+    got = values(Y)
+    assert_close(got, expected(ref, "bf16"), what="rmsnorm, two wavefronts per row")
+    assert_close(got[1024:], expected(ref[1024:], "bf16"), what="rmsnorm, partial last task")
+
+
 def test_causal_softmax_two_heads_per_block():
     # equal blocks (affine layout), two heads per block: a group's rows run
     # over both heads, so the query position wraps at the query block's extent
