@@ -9,6 +9,8 @@
 // forms its local partials, aggregates them across lanes (the aggregation
 // across blocks, in a fixed order), and writes the normalised row from the
 // registers.  HBM traffic: one read of the visible inputs, one write.
+// Long bf16 RMSNorm rows (more than 512 chunks) on the affine layout are
+// shared by two wavefronts, whose partial sums of squares meet in LDS.
 //
 // Causal softmax skips the loads of keys after the row's query position and
 // stores zeros there.  Rows too long for registers, or segments that are not
